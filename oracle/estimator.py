@@ -1,0 +1,140 @@
+"""Mean-pooled block-score mask estimator (float64), test infrastructure only.
+
+The paper accepts any lightweight block-level pattern search that yields the
+2D mask M[b,h,i,j] (Sec. 3.1; Sec. 3.2 first paragraph; Sec. 2.1 "pattern
+search overhead" on why it must be cheap per chunk).  It does not define this
+particular selector; the reading implemented here is:
+
+1. q_mean[b,h,i]   = mean of the q_block query rows of Q-block i, head h;
+2. k_mean[b,kvh,j] = mean of the page_size key rows of logical block j,
+   found through the page table (KV-head-major pages, Sec. 3.3);
+3. s[b,h,i,j] = q_mean . k_mean[kvh(h)], for cached blocks j < nC_b only;
+4. keep the top k = ceil(top_frac * nC_b) cached blocks of each row, ranked by
+   score descending then block index ascending; scores are compared in
+   float32, the precision the GPU scores are produced in (the decision is
+   taken in one precision on both sides), with -0.0 equal to +0.0;
+5. OR in the sink blocks {0..sink-1}, the local window
+   {nC-local .. nC-1} (the cached blocks just before the chunk) and the
+   chunk-causal blocks {nC .. nC + (i+1)*q_block/page - 1}; the whole chunk
+   is thereby open after the Q-block union (Sec. 3.1 last paragraph of the
+   overview; App. B.2 last paragraph).
+
+When nC_b = 0 there is neither top-k nor local window.  The unscaled dot
+product is used because a positive softmax scale does not change a ranking.
+
+Parity: pinned (closed-form pooling, brute-force top-k with ties, needle
+recall, popcount bounds) in tests/test_oracle.py.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass
+from typing import List, Sequence
+
+import numpy as np
+
+from .bf16 import bf16_to_f64
+
+
+@dataclass(frozen=True)
+class EstimatorParams:
+    top_frac: float
+    sink_blocks: int = 1
+    local_blocks: int = 4
+
+
+def q_block_means(q_bits: np.ndarray, q_block: int) -> np.ndarray:
+    """q [B, C, Hq, D] bf16 -> q_mean [B, Hq, nQB, D] float64."""
+    q = bf16_to_f64(q_bits)
+    B, C, Hq, D = q.shape
+    nqb = C // q_block
+    out = np.zeros((B, Hq, nqb, D))
+    for i in range(nqb):
+        out[:, :, i, :] = q[:, i * q_block:(i + 1) * q_block, :, :].mean(axis=1)
+    return out
+
+
+def k_block_means(k_pool_bits: np.ndarray, page_table: np.ndarray,
+                  n_blocks: Sequence[int]) -> np.ndarray:
+    """Mean of each logical block's key rows, via the page table.
+
+    Returns [B, Hkv, max_kv_blocks, D] float64; entries j >= n_blocks[b] are 0.
+    """
+    B, Hkv, maxkb = page_table.shape
+    D = k_pool_bits.shape[2]
+    out = np.zeros((B, Hkv, maxkb, D))
+    for b in range(B):
+        for h in range(Hkv):
+            for j in range(int(n_blocks[b])):
+                page = bf16_to_f64(k_pool_bits[page_table[b, h, j]])
+                out[b, h, j] = page.mean(axis=0)
+    return out
+
+
+def block_scores(q_mean: np.ndarray, k_mean: np.ndarray,
+                 n_cached: Sequence[int]) -> List[np.ndarray]:
+    """s[b][h, i, j] = q_mean[b,h,i] . k_mean[b,kvh(h),j] for j < nC_b (float64)."""
+    B, Hq, nqb, D = q_mean.shape
+    Hkv = k_mean.shape[1]
+    ratio = Hq // Hkv
+    out = []
+    for b in range(B):
+        nc = int(n_cached[b])
+        s = np.zeros((Hq, nqb, nc))
+        for h in range(Hq):
+            s[h] = q_mean[b, h] @ k_mean[b, h // ratio, :nc].T
+        out.append(s)
+    return out
+
+
+def select_top_blocks(scores_row: np.ndarray, k: int) -> np.ndarray:
+    """Indices of the k best blocks: score descending, then index ascending.
+
+    ``scores_row`` is compared as given (callers pass float32 values).
+    Numeric comparison makes -0.0 and +0.0 equal, so they tie and the
+    smaller index wins.
+    """
+    n = scores_row.shape[0]
+    idx = np.arange(n)
+    order = np.lexsort((idx, -scores_row.astype(np.float64)))
+    return np.sort(order[:k])
+
+
+def n_selected(top_frac: float, n_cached: int) -> int:
+    """k = ceil(top_frac * nC), computed in float32 like a kernel would."""
+    if n_cached == 0:
+        return 0
+    return min(n_cached, int(math.ceil(float(np.float32(top_frac) * np.float32(n_cached)))))
+
+
+def estimate_masks(q_bits: np.ndarray, k_pool_bits: np.ndarray,
+                   page_table: np.ndarray, cached_len: Sequence[int],
+                   page: int, q_block: int, chunk_len: int, words: int,
+                   params: EstimatorParams, return_parts: bool = False):
+    """Full estimator -> packed masks uint64 [B, Hq, nQB, words].
+
+    Bit j&63 of word j>>6 of row (b,h,i) is M[b,h,i,j].
+    """
+    B, C, Hq, D = q_bits.shape
+    nqb = chunk_len // q_block
+    n_cached = [int(c) // page for c in cached_len]
+    n_blocks = [nc + chunk_len // page for nc in n_cached]
+    qm = q_block_means(q_bits, q_block)
+    km = k_block_means(k_pool_bits, page_table, n_blocks)
+    sc = block_scores(qm, km, n_cached)
+    masks = np.zeros((B, Hq, nqb, words), dtype=np.uint64)
+    for b in range(B):
+        nc = n_cached[b]
+        k = n_selected(params.top_frac, nc)
+        s32 = sc[b].astype(np.float32)
+        for h in range(Hq):
+            for i in range(nqb):
+                sel = set(select_top_blocks(s32[h, i], k).tolist()) if k else set()
+                sel |= set(range(min(params.sink_blocks, nc)))
+                sel |= set(range(max(0, nc - params.local_blocks), nc))
+                sel |= set(range(nc, nc + ((i + 1) * q_block) // page))
+                for j in sel:
+                    masks[b, h, i, j >> 6] |= np.uint64(1) << np.uint64(j & 63)
+    if return_parts:
+        return masks, dict(q_mean=qm, k_mean=km, scores=sc)
+    return masks

@@ -1,0 +1,102 @@
+"""The seeded input generator: bf16 rounding, determinism, paging, workload recipe."""
+import struct
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from synth.configs import RHO_CALIBRATED
+
+
+def _f32_bits(x):
+    return struct.unpack("<I", struct.pack("<f", x))[0]
+
+
+def _bits_f32(u):
+    return struct.unpack("<f", struct.pack("<I", u))[0]
+
+
+def _nearest_bf16(x):
+    """Brute force: the closer of the two bracketing bf16 values, ties to even."""
+    u = _f32_bits(x)
+    lo = u >> 16
+    cands = [lo, lo + 1]
+    vx = Fraction(_bits_f32(u))
+    best = sorted(cands, key=lambda c: (abs(Fraction(_bits_f32(c << 16)) - vx), c & 1))
+    return best[0]
+
+
+def test_bf16_round_halfway_and_random():
+    vals = []
+    for base in (0x3F80, 0x3F81, 0x4000, 0xBF80, 0xC2F7, 0x0080, 0x7F00):
+        for low in (0x0000, 0x0001, 0x7FFF, 0x8000, 0x8001, 0xFFFF):
+            vals.append(_bits_f32((base << 16) | low))
+    vals += list(np.random.default_rng(0).standard_normal(2000).astype(np.float32))
+    got = synth.bf16_round(np.array(vals, dtype=np.float32))
+    want = [_nearest_bf16(float(v)) for v in vals]
+    assert got.tolist() == want
+
+
+def test_same_seed_same_bytes():
+    w = synth.get_workload("tiny_gqa_1k")
+    a, b = synth.make_inputs(w), synth.make_inputs(w)
+    for key in ("q", "k_pool", "v_pool", "page_table", "masks"):
+        assert np.array_equal(a[key], b[key])
+    c = synth.make_inputs(synth.get_workload("tiny_gqa_1k", seed=99))
+    assert not np.array_equal(a["q"], c["q"])
+
+
+def test_page_table_is_bijection(workload_inputs):
+    d = workload_inputs("tiny_gqa_1k")
+    pt = d["page_table"]
+    used = pt[pt >= 0]
+    assert sorted(used.tolist()) == list(range(d["k_pool"].shape[0]))
+    w = synth.get_workload("batched_ragged_4seq")
+    # shared pool of the batched workload, without generating its payload
+    from synth.gen import _page_assignment
+    nkb = [w.n_kv_blocks(b) for b in range(w.batch)]
+    pt, total = _page_assignment(w, nkb)
+    used = pt[pt >= 0]
+    assert total == 8 * sum(nkb) and sorted(used.tolist()) == list(range(total))
+    for b in range(w.batch):
+        assert (pt[b, :, :nkb[b]] >= 0).all() and (pt[b, :, nkb[b]:] == -1).all()
+
+
+def test_tiny_masks_recipe(workload_inputs):
+    d = workload_inputs("tiny_gqa_1k")
+    w = d["workload"]
+    bits = oracle.unpack_masks(d["masks"])
+    nc = w.n_cached_blocks(0)
+    assert bits[0, :, :, 0].all()                                     # sink
+    for i in range(w.n_qblocks):                                      # causal staircase
+        assert bits[0, :, i, nc:nc + i + 1].all() and not bits[0, :, i, nc + i + 1:].any()
+    frac = bits[0, :, :, 1:nc].mean()
+    assert 0.15 < frac < 0.35                                         # Bernoulli(0.25)
+    q = synth.bf16_bits_to_f32(d["q"])
+    assert abs(q.std() - 0.125) < 0.01                                # N(0,1) / sqrt(64)
+
+
+def test_sweep_chunks_share_one_pool():
+    from synth.configs import sweep_chunk
+    w0, w5 = sweep_chunk(0), sweep_chunk(5)
+    assert w0.cached_lens == (0,) and w5.cached_lens == (5 * 2048,)
+    assert w5.n_kv_blocks(0) == 32 * 6 and w5.words == 32
+
+
+def test_calibrated_density_and_needles(oracle_estimate, workload_inputs):
+    """At the calibrated rho the 128K final chunk keeps ~30% of cached blocks after
+    both unions (the paper's 70.2% executed sparsity), and every needle is found."""
+    name = "llama8b_128k_final"
+    d = workload_inputs(name)
+    w = d["workload"]
+    assert w.rho == RHO_CALIBRATED
+    masks, _ = oracle_estimate(name)
+    dens = oracle.union_densities(masks, w.group_size, [w.n_cached_blocks(0)])
+    assert 0.27 <= dens["group_union"] <= 0.33, dens
+    assert dens["pre_union"] < dens["q_union"] < dens["group_union"]
+    bits = oracle.unpack_masks(masks)
+    assert all(bits[b, h, i, j] for (b, kvh, j, h, i) in d["needles"])
+    q = synth.bf16_bits_to_f32(d["q"])
+    assert abs(q.std() - 1.0) < 0.02                                  # still N(0,1) marginally
