@@ -1,0 +1,239 @@
+"""Benchmark of the chunked-prefill block-union attention path on one MI355X.
+
+One step = the whole path on the 128K final chunk (LLaMA-3.1-8B layer shape:
+32 query / 8 KV heads, head_dim 128, 129024 cached tokens + a 2048-token
+chunk, bf16): estimate masks (Q/K block pooling over the whole cache, block
+scores, top-5% + sink + local + causal selection) -> block-union tables ->
+zero-copy paged attention (+ split combine when used).  Inputs are seeded
+synthetic tensors already resident in HBM.  The dense paged baseline (same
+attention kernel over every block) is timed in the same run.
+
+Prints ONE JSON line (see the repository's bench contract).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="llama8b_128k_final")
+    ap.add_argument("--rho", type=float, default=None,
+                    help="override the query-direction weight (0 = literal iid inputs)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-queries", type=int, default=512)
+    return ap.parse_args()
+
+
+def selected_flops(w, ip: np.ndarray, ix: np.ndarray) -> float:
+    """4*D per unmasked (query, key) pair over each group's table.
+
+    Cached blocks are fully visible to every chunk query; the chunk's own
+    blocks contribute the causal triangle C(C+1)/2 per query head.
+    """
+    G = w.num_q_heads // w.group_size
+    C = w.chunk_len
+    tot = 0.0
+    for b in range(w.batch):
+        nc = w.n_cached_blocks(b)
+        for g in range(G):
+            r = b * G + g
+            row = ix[ip[r]:ip[r + 1]]
+            cached = int(np.count_nonzero(row < nc))
+            tot += w.group_size * (C * w.page_size * cached + C * (C + 1) / 2)
+    return tot * 4 * w.head_dim
+
+
+def cpu_baseline(w, d, tables_T, sample_queries: int):
+    """Oracle on the host: full estimator and tables, attention on a sample of
+    queries of one group scaled to the whole chunk (ms for one full step)."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count() or 1
+    params = oracle.EstimatorParams(w.top_frac, w.sink_blocks, w.local_blocks)
+    t0 = time.perf_counter()
+    masks = oracle.estimate_masks(d["q"], d["k_pool"], d["page_table"], d["cached_len"],
+                                  w.page_size, w.q_block, w.chunk_len, w.words, params)
+    t1 = time.perf_counter()
+    T = oracle.block_tables(masks, w.group_size, [w.n_kv_blocks(b) for b in range(w.batch)])
+    t2 = time.perf_counter()
+    rng = np.random.default_rng(0)
+    qs = np.sort(rng.choice(w.chunk_len, size=min(sample_queries, w.chunk_len), replace=False))
+    heads = [(0, h) for h in range(w.group_size)]           # group 0 of sequence 0
+    oracle.chunk_attention(d["q"], d["k_pool"], d["v_pool"], d["page_table"], d["cached_len"],
+                           T, w.group_size, w.sm_scale, heads=heads, queries=qs)
+    t3 = time.perf_counter()
+    scale = (w.batch * w.num_q_heads * w.chunk_len) / (len(heads) * len(qs))
+    total_ms = 1e3 * ((t1 - t0) + (t2 - t1) + (t3 - t2) * scale)
+    return {
+        "value": round(total_ms, 1), "unit": "ms", "cores": int(threads), "kind": "oracle",
+        "sample": (f"estimator + tables on the full chunk; fp64 attention on {len(qs)} queries x "
+                   f"{len(heads)} heads of group 0, scaled x{scale:.0f} to all queries"),
+        "stage_ms": {"estimate": round(1e3 * (t1 - t0), 1), "tables": round(1e3 * (t2 - t1), 1),
+                     "attention_scaled": round(1e3 * (t3 - t2) * scale, 1)},
+        "host": platform.processor() or platform.machine(),
+        "os_cpu_count": os.cpu_count(),
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: the path shards by (sequence, KV group) with no "
+              "exchange, and multi-GPU runs are not part of this build; use --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import paper_2605_16839_amd as ca
+    import synth
+
+    w = synth.get_workload(args.workload)
+    if args.rho is not None:
+        w = synth.get_workload(args.workload, rho=args.rho)
+    d = synth.make_inputs(w)
+    dev = "cuda"
+    bf = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
+    q, kp, vp = bf(d["q"]), bf(d["k_pool"]), bf(d["v_pool"])
+    pt = torch.from_numpy(d["page_table"]).to(dev)
+    p = ca.Problem.from_workload(w, device=dev)
+    gs = w.group_size
+    G = w.num_q_heads // gs
+    R = w.batch * G
+    bufs = {}
+    tables = (torch.empty(R + 1, dtype=torch.int32, device=dev),
+              torch.empty(R * w.max_kv_blocks, dtype=torch.int32, device=dev))
+    tws = torch.empty(max(ca.tables_workspace_bytes(p, gs), 1), dtype=torch.uint8, device=dev)
+    aws_n = ca.attention_workspace_bytes(p, gs, 0)
+    aws = torch.empty(aws_n, dtype=torch.uint8, device=dev) if aws_n else None
+    dws_n = ca.attention_workspace_bytes(p, w.num_q_heads // w.num_kv_heads, 0)
+    dws = torch.empty(dws_n, dtype=torch.uint8, device=dev) if dws_n else None
+    out = torch.empty_like(q)
+    out_dense = torch.empty_like(q)
+    lse = torch.empty((w.batch, w.num_q_heads, w.chunk_len), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+
+    def step(marks=None):
+        if marks:
+            marks[0].record(stream)
+        masks, _ = ca.estimate_masks(p, q, kp, pt, w.top_frac, w.sink_blocks, w.local_blocks,
+                                     bufs=bufs)
+        if marks:
+            marks[1].record(stream)
+        ca.build_block_tables(p, masks, gs, out=tables, ws=tws)
+        if marks:
+            marks[2].record(stream)
+        ca.chunk_attention(p, q, (kp, vp), pt, tables, gs, w.sm_scale, num_splits=0, out=out,
+                           lse=lse, ws=aws)
+        if marks:
+            marks[3].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # ---- timed region: K whole steps ----
+    start, stop = ev(), ev()
+    torch.cuda.synchronize()
+    start.record(stream)
+    for _ in range(args.steps):
+        step()
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = start.elapsed_time(stop) / args.steps
+
+    # ---- per-stage split (separate pass with events between stages) ----
+    stage = {"estimate": [], "tables": [], "attention": []}
+    for _ in range(args.steps):
+        m = [ev() for _ in range(4)]
+        step(m)
+        torch.cuda.synchronize()
+        stage["estimate"].append(m[0].elapsed_time(m[1]))
+        stage["tables"].append(m[1].elapsed_time(m[2]))
+        stage["attention"].append(m[2].elapsed_time(m[3]))
+    st_ms = {k: float(np.median(v)) for k, v in stage.items()}
+
+    # ---- dense paged baseline ----
+    dargs = dict(num_splits=0, out=out_dense, ws=dws)
+    for _ in range(args.warmup):
+        ca.dense_paged_chunk_attention(p, q, (kp, vp), pt, w.sm_scale, **dargs)
+    torch.cuda.synchronize()
+    ds, de = ev(), ev()
+    ds.record(stream)
+    for _ in range(args.steps):
+        ca.dense_paged_chunk_attention(p, q, (kp, vp), pt, w.sm_scale, **dargs)
+    de.record(stream)
+    torch.cuda.synchronize()
+    dense_ms = ds.elapsed_time(de) / args.steps
+
+    ip = tables[0].cpu().numpy()
+    ix = tables[1].cpu().numpy()
+    f_sel = selected_flops(w, ip, ix)
+    f_dense = w.dense_flops()
+    attn_tflops = f_sel / (st_ms["attention"] * 1e-3) / 1e12
+    dense_tflops = f_dense / (dense_ms * 1e-3) / 1e12
+    ncached = sum(w.n_cached_blocks(b) for b in range(w.batch)) * G
+    sel_cached = sum(int(np.count_nonzero(ix[ip[r]:ip[r + 1]] <
+                                          w.n_cached_blocks(r // G))) for r in range(R))
+    density = sel_cached / max(ncached, 1)
+
+    res = {
+        "metric": "128K final-chunk attention ms, speedup vs dense paged, MFMA util",
+        "value": round(ms_per_step, 4),
+        "unit": "ms",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "batch": w.batch, "num_q_heads": w.num_q_heads,
+                   "num_kv_heads": w.num_kv_heads, "head_dim": w.head_dim,
+                   "cached_tokens": list(w.cached_lens), "chunk_len": w.chunk_len,
+                   "top_frac": w.top_frac, "rho": w.rho, "group_size": gs},
+        "stage_ms": {k: round(v, 4) for k, v in st_ms.items()},
+        "dense_ms": round(dense_ms, 4),
+        "speedup_vs_dense": round(dense_ms / ms_per_step, 3),
+        "speedup_vs_dense_kernel_only": round(dense_ms / st_ms["attention"], 3),
+        "executed_cached_density": round(density, 4),
+        "attention_tflops_selected": round(attn_tflops, 1),
+        "dense_tflops": round(dense_tflops, 1),
+        "mfma_util_time_based": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
+        "roofline": {"bound": "mfma", "achieved": round(attn_tflops, 1),
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None},
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        nkb = [w.n_kv_blocks(b) for b in range(w.batch)]
+        res["cpu_baseline"] = cpu_baseline(w, d, None, args.cpu_sample_queries)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

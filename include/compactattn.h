@@ -1,0 +1,207 @@
+/*
+ * compactattn.h -- C ABI of the chunked-prefill block-union attention path
+ * (CompactAttention, arXiv 2605.16839) for AMD Instinct MI355X (gfx950).
+ *
+ * The path, per chunk of a chunked prefill:
+ *
+ *   1. estimate   2D block masks M[b,h,i,j] from mean-pooled Q and K blocks
+ *                 (a lightweight block-level selector; the paper accepts any
+ *                 such pattern search, Sec. 3.1 and Sec. 3.2 first paragraph);
+ *   2. tables     Q-block union, intra-group union and the per-group table
+ *                 T[b,g] = { j : exists h in H(g), exists i, M[b,h,i,j] = 1 }
+ *                 (Sec. 3.2, the three displayed equations), as CSR
+ *                 kv_indptr / kv_indices (Sec. 3.3, App. B.2);
+ *   3. attention  dense attention of every chunk query over exactly the blocks
+ *                 of its group's table, read in place from the paged pool
+ *                 (zero-copy, Sec. 3.3), causal in absolute positions
+ *                 (App. B.2, last paragraph);
+ *   plus a dense paged baseline (every block of the sequence).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - All pointers are DEVICE memory unless the name ends in _host.  The
+ *   caller allocates and owns every buffer; the library allocates nothing
+ *   and keeps no state besides a thread-local error string.
+ * - bf16 tensors are passed as uint16_t bit patterns.  All tensors are dense
+ *   row-major (C order) with the shapes given below.
+ * - KV cache: KV-head-major pages (Sec. 3.3, Fig. 4).  Logical block j of
+ *   (sequence b, KV head kvh) is physical page page_table[b, kvh, j] of
+ *   k_pool / v_pool, each [P, page_size, head_dim]; one page id addresses the
+ *   K page and the V page.  page_table is int32 [B, Hkv, max_kv_blocks];
+ *   entries at j >= nKB_b are ignored.
+ * - Per sequence b: cached_len[b] tokens are already in the cache and the
+ *   chunk adds chunk_len tokens, so nC_b = cached_len[b] / page_size cached
+ *   blocks and nKB_b = nC_b + chunk_len / page_size blocks in total; chunk
+ *   token t sits at absolute position cached_len[b] + t, key r of block j at
+ *   page_size * j + r.
+ * - Query head h belongs to KV head h / (Hq / Hkv) and to execution group
+ *   h / group_size (contiguous heads, Sec. 3.2 and App. B.1: the KV group by
+ *   default, or 4-head sub-groups of a larger KV group).  group_size must
+ *   divide Hq / Hkv.
+ * - Masks are uint64 [B, Hq, nQB, W], W = ceil(max_kv_blocks / 64),
+ *   nQB = chunk_len / q_block: bit (j & 63) of word (j >> 6) of row (b,h,i)
+ *   is M[b,h,i,j].  Only blocks j < nKB_b are meaningful.
+ * - Tables: kv_indptr int32 [B*G + 1] and kv_indices int32 (capacity
+ *   B*G*max_kv_blocks); row r = b*G + g lists T[b,g] as ascending LOGICAL
+ *   block ids in kv_indices[kv_indptr[r] .. kv_indptr[r+1]).
+ * - `stream` is a hipStream_t (NULL = the default stream).  Every call only
+ *   enqueues work on it and returns without synchronising, except
+ *   ca_validate_tables.
+ * - Argument and shape errors are reported before anything is enqueued; a
+ *   failed launch returns CA_ERR_HIP with the HIP error text available from
+ *   ca_last_error_detail().
+ */
+#ifndef COMPACTATTN_H
+#define COMPACTATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define CA_ABI_VERSION 1
+
+typedef enum ca_status {
+  CA_OK = 0,
+  CA_ERR_NULL = 1,          /* a required pointer is NULL                       */
+  CA_ERR_SHAPE = 2,         /* a size is out of range or inconsistent           */
+  CA_ERR_UNALIGNED = 3,     /* a length is not a multiple of page_size/q_block  */
+  CA_ERR_GROUP = 4,         /* group_size does not divide Hq / Hkv              */
+  CA_ERR_WORKSPACE = 5,     /* workspace missing or too small                   */
+  CA_ERR_UNSUPPORTED = 6,   /* head_dim / page_size / q_block not built for     */
+  CA_ERR_INVALID_TABLE = 7, /* ca_validate_tables found a malformed table       */
+  CA_ERR_HIP = 8            /* a HIP runtime call or kernel launch failed       */
+} ca_status;
+
+typedef struct ca_problem {
+  int32_t batch;             /* B >= 1                                          */
+  int32_t num_q_heads;       /* Hq                                              */
+  int32_t num_kv_heads;      /* Hkv, divides Hq                                 */
+  int32_t head_dim;          /* D, 64 or 128                                    */
+  int32_t page_size;         /* tokens per KV block == page; must be 64         */
+  int32_t q_block;           /* query block of the masks: 64 or 128             */
+  int32_t chunk_len;         /* C >= 1; multiple of page_size and q_block       */
+  int32_t max_kv_blocks;     /* row stride of page_table, >= max_b nKB_b, <= 16384 */
+  const int32_t* cached_len_host; /* HOST [B]: multiples of page_size, may be 0 */
+  const int32_t* cached_len;      /* DEVICE [B]: the same values                */
+} ca_problem;
+
+int ca_abi_version(void);
+const char* ca_status_string(ca_status s);
+/* Thread-local detail of the last error returned on this thread ("" if none). */
+const char* ca_last_error_detail(void);
+
+/* Host-only validation of a problem (and of group_size if > 0); enqueues
+ * nothing and needs no GPU.  Every entry point below performs it first. */
+ca_status ca_check_problem(const ca_problem* p, int32_t group_size);
+
+/* ------------------------------------------------------------------------
+ * 1. Estimator (the selector; see the file header).  Stage by stage:
+ *    q_mean[b,h,i]   = mean of the q_block query rows of Q-block i, head h
+ *    k_mean[b,kvh,j] = mean of the page_size key rows of block j
+ *    scores[b,h,i,j] = q_mean[b,h,i] . k_mean[b,kvh(h),j], j < nC_b
+ *    masks: top k = ceil(top_frac * nC_b) (float32 product, at most nC_b)
+ *           cached blocks per row by score descending then j ascending
+ *           (-0.0 ranks equal to +0.0), OR sink blocks {0..sink_blocks-1},
+ *           OR the local window {nC_b-local_blocks .. nC_b-1}, OR the
+ *           chunk-causal blocks {nC_b .. nC_b + (i+1)*q_block/page_size - 1},
+ *           all clipped to [0, nKB_b); every other bit of the row is 0.
+ * Pooling and scores accumulate in float32.
+ * ---------------------------------------------------------------------- */
+
+/* q bf16 [B, C, Hq, D] -> q_mean fp32 [B, Hq, nQB, D]. */
+ca_status ca_pool_q_blocks(const ca_problem* p, const uint16_t* q, float* q_mean,
+                           void* stream);
+
+/* k_mean fp32 [B, Hkv, max_kv_blocks, D]: blocks j in [first_block, nKB_b) of
+ * every sequence are (re)computed from k_pool; the others are left untouched,
+ * so a caller that keeps k_mean across chunks passes first_block = the number
+ * of blocks pooled by earlier chunks. */
+ca_status ca_pool_k_blocks(const ca_problem* p, const uint16_t* k_pool,
+                           const int32_t* page_table, int32_t first_block,
+                           float* k_mean, void* stream);
+
+/* scores fp32 [B, Hq, nQB, max_kv_blocks]; only j < nC_b is written. */
+ca_status ca_block_scores(const ca_problem* p, const float* q_mean,
+                          const float* k_mean, float* scores, void* stream);
+
+/* scores (as above, finite values) -> masks uint64 [B, Hq, nQB, W]. */
+ca_status ca_select_blocks(const ca_problem* p, const float* scores, float top_frac,
+                           int32_t sink_blocks, int32_t local_blocks,
+                           uint64_t* masks, void* stream);
+
+/* All four stages in order. */
+ca_status ca_estimate_masks(const ca_problem* p, const uint16_t* q,
+                            const uint16_t* k_pool, const int32_t* page_table,
+                            float top_frac, int32_t sink_blocks, int32_t local_blocks,
+                            int32_t k_mean_first_block, float* q_mean, float* k_mean,
+                            float* scores, uint64_t* masks, void* stream);
+
+/* ------------------------------------------------------------------------
+ * 2. Block tables (Sec. 3.2): bitwise OR over the nQB mask rows of every
+ *    head of each group, compaction of the set bits j < nKB_b into the CSR
+ *    pair.  Integer only; deterministic (no atomics on the output).
+ *    Workspace: ca_tables_workspace_bytes(p, group_size) bytes of device
+ *    memory, contents irrelevant on entry.
+ * ---------------------------------------------------------------------- */
+size_t ca_tables_workspace_bytes(const ca_problem* p, int32_t group_size);
+
+ca_status ca_build_block_tables(const ca_problem* p, const uint64_t* masks,
+                                int32_t group_size, int32_t* kv_indptr,
+                                int32_t* kv_indices, void* ws, size_t ws_bytes,
+                                void* stream);
+
+/* ------------------------------------------------------------------------
+ * 3. Chunk attention over the tables (Sec. 3.3, App. B.2).
+ *    q bf16 [B, C, Hq, D]; out bf16 [B, C, Hq, D]; lse fp32 [B, Hq, C]
+ *    (natural-log log-sum-exp of the scaled scores, may be NULL).
+ *    For query (b, h, t) and every key of every block j in T[b, h/group_size]
+ *    with key position <= cached_len[b] + t:
+ *        out = softmax(sm_scale * q.k) . v      (bf16 MFMA, fp32 softmax)
+ *    Table entries must be ascending and < nKB_b; blocks are read in place
+ *    through page_table (no gather).  A query that sees no key gets out = 0,
+ *    lse = -inf.
+ *    num_splits: 1 = one pass per query tile; > 1 = the table of each row is
+ *    cut into that many consecutive pieces whose partial results are merged
+ *    by log-sum-exp (needs workspace); 0 = let the library choose (it uses
+ *    splits only when the query tiles alone cannot fill the GPU and the
+ *    workspace is large enough).  Workspace:
+ *    ca_attention_workspace_bytes(p, group_size, num_splits) bytes (0 when no
+ *    split is needed; for num_splits = 0 it returns the size that lets the
+ *    library pick freely).
+ * ---------------------------------------------------------------------- */
+size_t ca_attention_workspace_bytes(const ca_problem* p, int32_t group_size,
+                                    int32_t num_splits);
+
+ca_status ca_chunk_attention(const ca_problem* p, const uint16_t* q,
+                             const uint16_t* k_pool, const uint16_t* v_pool,
+                             const int32_t* page_table, const int32_t* kv_indptr,
+                             const int32_t* kv_indices, int32_t group_size,
+                             float sm_scale, int32_t num_splits, uint16_t* out,
+                             float* lse, void* ws, size_t ws_bytes, void* stream);
+
+/* Dense paged baseline: the same kernel with T[b,g] = every block 0..nKB_b-1
+ * (the table an all-ones mask gives), without reading any table. */
+ca_status ca_dense_paged_chunk_attention(const ca_problem* p, const uint16_t* q,
+                                         const uint16_t* k_pool, const uint16_t* v_pool,
+                                         const int32_t* page_table, float sm_scale,
+                                         int32_t num_splits, uint16_t* out, float* lse,
+                                         void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Debug helper: synchronises `stream`, copies the tables to the host and
+ * checks kv_indptr[0] == 0, non-decreasing row bounds within capacity,
+ * entries strictly ascending and < nKB_b, and (if require_chunk_open) that
+ * every chunk block nC_b..nKB_b-1 is present.  Returns CA_ERR_INVALID_TABLE
+ * with a description in ca_last_error_detail() on the first violation.
+ * ---------------------------------------------------------------------- */
+ca_status ca_validate_tables(const ca_problem* p, int32_t group_size,
+                             const int32_t* kv_indptr, const int32_t* kv_indices,
+                             int32_t require_chunk_open, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* COMPACTATTN_H */

@@ -107,34 +107,47 @@ def n_selected(top_frac: float, n_cached: int) -> int:
     return min(n_cached, int(math.ceil(float(np.float32(top_frac) * np.float32(n_cached)))))
 
 
-def estimate_masks(q_bits: np.ndarray, k_pool_bits: np.ndarray,
-                   page_table: np.ndarray, cached_len: Sequence[int],
-                   page: int, q_block: int, chunk_len: int, words: int,
-                   params: EstimatorParams, return_parts: bool = False):
-    """Full estimator -> packed masks uint64 [B, Hq, nQB, words].
+def masks_from_scores(scores32: Sequence[np.ndarray], n_cached: Sequence[int],
+                      page: int, q_block: int, words: int,
+                      params: EstimatorParams) -> np.ndarray:
+    """Step 4-5: float32 scores per sequence ([Hq, nQB, nC_b]) -> packed masks.
 
     Bit j&63 of word j>>6 of row (b,h,i) is M[b,h,i,j].
     """
-    B, C, Hq, D = q_bits.shape
-    nqb = chunk_len // q_block
-    n_cached = [int(c) // page for c in cached_len]
-    n_blocks = [nc + chunk_len // page for nc in n_cached]
-    qm = q_block_means(q_bits, q_block)
-    km = k_block_means(k_pool_bits, page_table, n_blocks)
-    sc = block_scores(qm, km, n_cached)
+    B = len(scores32)
+    Hq, nqb = scores32[0].shape[:2]
     masks = np.zeros((B, Hq, nqb, words), dtype=np.uint64)
     for b in range(B):
-        nc = n_cached[b]
+        nc = int(n_cached[b])
         k = n_selected(params.top_frac, nc)
-        s32 = sc[b].astype(np.float32)
         for h in range(Hq):
             for i in range(nqb):
-                sel = set(select_top_blocks(s32[h, i], k).tolist()) if k else set()
+                sel = set(select_top_blocks(scores32[b][h, i], k).tolist()) if k else set()
                 sel |= set(range(min(params.sink_blocks, nc)))
                 sel |= set(range(max(0, nc - params.local_blocks), nc))
                 sel |= set(range(nc, nc + ((i + 1) * q_block) // page))
                 for j in sel:
                     masks[b, h, i, j >> 6] |= np.uint64(1) << np.uint64(j & 63)
+    return masks
+
+
+def estimate_masks(q_bits: np.ndarray, k_pool_bits: np.ndarray,
+                   page_table: np.ndarray, cached_len: Sequence[int],
+                   page: int, q_block: int, chunk_len: int, words: int,
+                   params: EstimatorParams, return_parts: bool = False,
+                   k_mean: np.ndarray = None):
+    """Full estimator -> packed masks uint64 [B, Hq, nQB, words].
+
+    ``k_mean`` may carry block means pooled earlier (they do not depend on
+    the chunk); blocks it does not cover must not be needed.
+    """
+    n_cached = [int(c) // page for c in cached_len]
+    n_blocks = [nc + chunk_len // page for nc in n_cached]
+    qm = q_block_means(q_bits, q_block)
+    km = k_mean if k_mean is not None else k_block_means(k_pool_bits, page_table, n_blocks)
+    sc = block_scores(qm, km, n_cached)
+    masks = masks_from_scores([s.astype(np.float32) for s in sc], n_cached, page, q_block,
+                              words, params)
     if return_parts:
         return masks, dict(q_mean=qm, k_mean=km, scores=sc)
     return masks

@@ -1,0 +1,374 @@
+// C ABI of libcompactattn: host-side validation and launch glue.
+// The meaning of every entry point is documented in include/compactattn.h.
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+#include <vector>
+
+#include "compactattn.h"
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace {
+
+thread_local std::string g_detail;
+
+ca_status fail(ca_status s, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+ca_status fail(ca_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_detail = buf;
+  return s;
+}
+
+ca_status ok() {
+  g_detail.clear();
+  return CA_OK;
+}
+
+ca_status hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return ok();
+  return fail(CA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Validates p (and group_size when > 0) and fills d.
+ca_status check(const ca_problem* p, int32_t group_size, ca::Dims* d) {
+  if (p == nullptr) return fail(CA_ERR_NULL, "problem is NULL");
+  if (p->cached_len_host == nullptr) return fail(CA_ERR_NULL, "cached_len_host is NULL");
+  if (p->batch < 1 || p->num_q_heads < 1 || p->num_kv_heads < 1)
+    return fail(CA_ERR_SHAPE, "batch, num_q_heads and num_kv_heads must be >= 1");
+  if (p->num_q_heads % p->num_kv_heads != 0)
+    return fail(CA_ERR_SHAPE, "num_kv_heads (%d) must divide num_q_heads (%d)",
+                p->num_kv_heads, p->num_q_heads);
+  if (p->head_dim != 64 && p->head_dim != 128)
+    return fail(CA_ERR_UNSUPPORTED, "head_dim %d not supported (64, 128)", p->head_dim);
+  if (p->page_size != ca::kPage)
+    return fail(CA_ERR_UNSUPPORTED, "page_size %d not supported (64)", p->page_size);
+  if (p->q_block != 64 && p->q_block != 128)
+    return fail(CA_ERR_UNSUPPORTED, "q_block %d not supported (64, 128)", p->q_block);
+  if (p->chunk_len < 1) return fail(CA_ERR_SHAPE, "chunk_len must be >= 1");
+  if (p->chunk_len % p->page_size != 0 || p->chunk_len % p->q_block != 0)
+    return fail(CA_ERR_UNALIGNED, "chunk_len %d must be a multiple of page_size and q_block",
+                p->chunk_len);
+  if (p->max_kv_blocks < 1 || p->max_kv_blocks > ca::kMaxKvBlocks)
+    return fail(CA_ERR_SHAPE, "max_kv_blocks %d out of range [1, %d]", p->max_kv_blocks,
+                ca::kMaxKvBlocks);
+  const int chunk_blocks = p->chunk_len / p->page_size;
+  int max_nc = 0;
+  for (int b = 0; b < p->batch; ++b) {
+    const int c = p->cached_len_host[b];
+    if (c < 0 || c % p->page_size != 0)
+      return fail(CA_ERR_UNALIGNED, "cached_len[%d] = %d is not a non-negative multiple of %d",
+                  b, c, p->page_size);
+    const long long nkb = (long long)(c / p->page_size) + chunk_blocks;
+    if (nkb > p->max_kv_blocks)
+      return fail(CA_ERR_SHAPE, "sequence %d needs %lld blocks > max_kv_blocks %d", b, nkb,
+                  p->max_kv_blocks);
+    if (c / p->page_size > max_nc) max_nc = c / p->page_size;
+  }
+  if (group_size > 0) {
+    const int ratio = p->num_q_heads / p->num_kv_heads;
+    if (ratio % group_size != 0)
+      return fail(CA_ERR_GROUP, "group_size %d must divide Hq/Hkv = %d", group_size, ratio);
+  }
+  if (d != nullptr) {
+    d->B = p->batch;
+    d->Hq = p->num_q_heads;
+    d->Hkv = p->num_kv_heads;
+    d->D = p->head_dim;
+    d->page = p->page_size;
+    d->q_block = p->q_block;
+    d->C = p->chunk_len;
+    d->max_kv_blocks = p->max_kv_blocks;
+    d->nqb = p->chunk_len / p->q_block;
+    d->W = (p->max_kv_blocks + 63) / 64;
+    d->chunk_blocks = chunk_blocks;
+    d->max_nc = max_nc;
+    d->max_nkb = max_nc + chunk_blocks;
+  }
+  return ok();
+}
+
+ca_status need_device(const ca_problem* p) {
+  if (p->cached_len == nullptr) return fail(CA_ERR_NULL, "cached_len (device) is NULL");
+  return CA_OK;
+}
+
+ca_status attention_tile_ok(const ca::Dims& d, int group_size) {
+  if (128 % group_size != 0)
+    return fail(CA_ERR_UNSUPPORTED, "group_size %d must divide 128", group_size);
+  const int qt = ca::attn_query_tile(group_size);
+  if (d.C % qt != 0)
+    return fail(CA_ERR_UNSUPPORTED, "chunk_len %d must be a multiple of %d for group_size %d",
+                d.C, qt, group_size);
+  return CA_OK;
+}
+
+// Splits chosen when the caller passes num_splits = 0.
+int auto_splits(const ca::Dims& d, int group_size, size_t ws_bytes, bool have_ws) {
+  const int base = ca::attn_base_workgroups(d, group_size);
+  const int target = 2 * 256;  // two resident workgroups on each of 256 CUs
+  if (base >= target || !have_ws) return 1;
+  int s = (target + base - 1) / base;
+  const int max_by_len = d.max_nkb / 4 > 1 ? d.max_nkb / 4 : 1;
+  if (s > max_by_len) s = max_by_len;
+  if (s > 16) s = 16;
+  while (s > 1 && ca::attn_ws_bytes(d, s) > ws_bytes) --s;
+  return s < 1 ? 1 : s;
+}
+
+ca_status run_attention(const ca_problem* p, const uint16_t* q, const uint16_t* k_pool,
+                        const uint16_t* v_pool, const int32_t* page_table,
+                        const int32_t* kv_indptr, const int32_t* kv_indices, int32_t group_size,
+                        float sm_scale, int32_t num_splits, uint16_t* out, float* lse, void* ws,
+                        size_t ws_bytes, void* stream, bool dense) {
+  ca::Dims d;
+  ca_status s = check(p, group_size, &d);
+  if (s != CA_OK) return s;
+  if ((s = need_device(p)) != CA_OK) return s;
+  if (!q || !k_pool || !v_pool || !page_table || !out)
+    return fail(CA_ERR_NULL, "q, k_pool, v_pool, page_table and out are required");
+  if (!dense && (!kv_indptr || !kv_indices))
+    return fail(CA_ERR_NULL, "kv_indptr and kv_indices are required");
+  if ((s = attention_tile_ok(d, group_size)) != CA_OK) return s;
+  if (num_splits < 0 || num_splits > 64)
+    return fail(CA_ERR_SHAPE, "num_splits %d out of range [0, 64]", num_splits);
+  int splits = num_splits;
+  if (splits == 0) splits = auto_splits(d, group_size, ws_bytes, ws != nullptr);
+  if (splits > 1) {
+    const size_t need = ca::attn_ws_bytes(d, splits);
+    if (ws == nullptr || ws_bytes < need)
+      return fail(CA_ERR_WORKSPACE, "attention with %d splits needs %zu workspace bytes, got %zu",
+                  splits, need, ws == nullptr ? (size_t)0 : ws_bytes);
+  }
+  ca::AttnLaunch L;
+  L.q = q;
+  L.k_pool = k_pool;
+  L.v_pool = v_pool;
+  L.page_table = page_table;
+  L.kv_indptr = kv_indptr;
+  L.kv_indices = kv_indices;
+  L.cached_len = p->cached_len;
+  L.out = out;
+  L.lse = lse;
+  L.group_size = group_size;
+  L.sm_scale = sm_scale;
+  L.splits = splits;
+  L.ws = ws;
+  L.dense = dense;
+  return hip_status(ca::launch_attention(d, L, static_cast<hipStream_t>(stream)),
+                    dense ? "dense paged attention launch" : "chunk attention launch");
+}
+
+}  // namespace
+
+extern "C" {
+
+int ca_abi_version(void) { return CA_ABI_VERSION; }
+
+const char* ca_status_string(ca_status s) {
+  switch (s) {
+    case CA_OK: return "CA_OK";
+    case CA_ERR_NULL: return "CA_ERR_NULL";
+    case CA_ERR_SHAPE: return "CA_ERR_SHAPE";
+    case CA_ERR_UNALIGNED: return "CA_ERR_UNALIGNED";
+    case CA_ERR_GROUP: return "CA_ERR_GROUP";
+    case CA_ERR_WORKSPACE: return "CA_ERR_WORKSPACE";
+    case CA_ERR_UNSUPPORTED: return "CA_ERR_UNSUPPORTED";
+    case CA_ERR_INVALID_TABLE: return "CA_ERR_INVALID_TABLE";
+    case CA_ERR_HIP: return "CA_ERR_HIP";
+  }
+  return "CA_ERR_UNKNOWN";
+}
+
+const char* ca_last_error_detail(void) { return g_detail.c_str(); }
+
+ca_status ca_check_problem(const ca_problem* p, int32_t group_size) {
+  return check(p, group_size, nullptr);
+}
+
+ca_status ca_pool_q_blocks(const ca_problem* p, const uint16_t* q, float* q_mean, void* stream) {
+  ca::Dims d;
+  ca_status s = check(p, 0, &d);
+  if (s != CA_OK) return s;
+  if (!q || !q_mean) return fail(CA_ERR_NULL, "q and q_mean are required");
+  return hip_status(ca::launch_pool_q(d, q, q_mean, static_cast<hipStream_t>(stream)),
+                    "pool_q launch");
+}
+
+ca_status ca_pool_k_blocks(const ca_problem* p, const uint16_t* k_pool,
+                           const int32_t* page_table, int32_t first_block, float* k_mean,
+                           void* stream) {
+  ca::Dims d;
+  ca_status s = check(p, 0, &d);
+  if (s != CA_OK) return s;
+  if ((s = need_device(p)) != CA_OK) return s;
+  if (!k_pool || !page_table || !k_mean)
+    return fail(CA_ERR_NULL, "k_pool, page_table and k_mean are required");
+  if (first_block < 0) return fail(CA_ERR_SHAPE, "first_block must be >= 0");
+  return hip_status(ca::launch_pool_k(d, k_pool, page_table, p->cached_len, first_block,
+                                      k_mean, static_cast<hipStream_t>(stream)),
+                    "pool_k launch");
+}
+
+ca_status ca_block_scores(const ca_problem* p, const float* q_mean, const float* k_mean,
+                          float* scores, void* stream) {
+  ca::Dims d;
+  ca_status s = check(p, 0, &d);
+  if (s != CA_OK) return s;
+  if ((s = need_device(p)) != CA_OK) return s;
+  if (!q_mean || !k_mean || !scores)
+    return fail(CA_ERR_NULL, "q_mean, k_mean and scores are required");
+  return hip_status(ca::launch_scores(d, q_mean, k_mean, p->cached_len, scores,
+                                      static_cast<hipStream_t>(stream)),
+                    "scores launch");
+}
+
+ca_status ca_select_blocks(const ca_problem* p, const float* scores, float top_frac,
+                           int32_t sink_blocks, int32_t local_blocks, uint64_t* masks,
+                           void* stream) {
+  ca::Dims d;
+  ca_status s = check(p, 0, &d);
+  if (s != CA_OK) return s;
+  if ((s = need_device(p)) != CA_OK) return s;
+  if (!scores || !masks) return fail(CA_ERR_NULL, "scores and masks are required");
+  if (!(top_frac >= 0.f && top_frac <= 1.f))
+    return fail(CA_ERR_SHAPE, "top_frac must be in [0, 1]");
+  if (sink_blocks < 0 || local_blocks < 0)
+    return fail(CA_ERR_SHAPE, "sink_blocks and local_blocks must be >= 0");
+  const size_t lds = (size_t)(d.max_nc > 0 ? d.max_nc : 1) * sizeof(uint32_t);
+  if (lds > 48 * 1024) {
+    // the keys of one row live in LDS; raise the dynamic LDS cap for long caches
+    hipError_t e = ca::raise_select_lds((int)lds);
+    if (e != hipSuccess) return hip_status(e, "raise select LDS limit");
+  }
+  return hip_status(ca::launch_select(d, scores, p->cached_len, top_frac, sink_blocks,
+                                      local_blocks, masks, static_cast<hipStream_t>(stream)),
+                    "select launch");
+}
+
+ca_status ca_estimate_masks(const ca_problem* p, const uint16_t* q, const uint16_t* k_pool,
+                            const int32_t* page_table, float top_frac, int32_t sink_blocks,
+                            int32_t local_blocks, int32_t k_mean_first_block, float* q_mean,
+                            float* k_mean, float* scores, uint64_t* masks, void* stream) {
+  ca_status s = ca_pool_q_blocks(p, q, q_mean, stream);
+  if (s != CA_OK) return s;
+  if ((s = ca_pool_k_blocks(p, k_pool, page_table, k_mean_first_block, k_mean, stream)) != CA_OK)
+    return s;
+  if ((s = ca_block_scores(p, q_mean, k_mean, scores, stream)) != CA_OK) return s;
+  return ca_select_blocks(p, scores, top_frac, sink_blocks, local_blocks, masks, stream);
+}
+
+size_t ca_tables_workspace_bytes(const ca_problem* p, int32_t group_size) {
+  ca::Dims d;
+  if (group_size < 1 || check(p, group_size, &d) != CA_OK) return 0;
+  return ca::tables_ws_bytes(d, group_size);
+}
+
+ca_status ca_build_block_tables(const ca_problem* p, const uint64_t* masks, int32_t group_size,
+                                int32_t* kv_indptr, int32_t* kv_indices, void* ws,
+                                size_t ws_bytes, void* stream) {
+  ca::Dims d;
+  if (group_size < 1) return fail(CA_ERR_GROUP, "group_size must be >= 1");
+  ca_status s = check(p, group_size, &d);
+  if (s != CA_OK) return s;
+  if ((s = need_device(p)) != CA_OK) return s;
+  if (!masks || !kv_indptr || !kv_indices)
+    return fail(CA_ERR_NULL, "masks, kv_indptr and kv_indices are required");
+  const size_t need = ca::tables_ws_bytes(d, group_size);
+  if (ws == nullptr || ws_bytes < need)
+    return fail(CA_ERR_WORKSPACE, "tables need %zu workspace bytes, got %zu", need,
+                ws == nullptr ? (size_t)0 : ws_bytes);
+  return hip_status(ca::launch_tables(d, masks, p->cached_len, group_size, kv_indptr,
+                                      kv_indices, ws, static_cast<hipStream_t>(stream)),
+                    "tables launch");
+}
+
+size_t ca_attention_workspace_bytes(const ca_problem* p, int32_t group_size, int32_t num_splits) {
+  ca::Dims d;
+  if (group_size < 1 || check(p, group_size, &d) != CA_OK) return 0;
+  if (num_splits < 0 || num_splits > 64) return 0;
+  int s = num_splits;
+  if (s == 0) s = auto_splits(d, group_size, (size_t)-1, true);
+  return ca::attn_ws_bytes(d, s);
+}
+
+ca_status ca_chunk_attention(const ca_problem* p, const uint16_t* q, const uint16_t* k_pool,
+                             const uint16_t* v_pool, const int32_t* page_table,
+                             const int32_t* kv_indptr, const int32_t* kv_indices,
+                             int32_t group_size, float sm_scale, int32_t num_splits,
+                             uint16_t* out, float* lse, void* ws, size_t ws_bytes,
+                             void* stream) {
+  if (group_size < 1) return fail(CA_ERR_GROUP, "group_size must be >= 1");
+  return run_attention(p, q, k_pool, v_pool, page_table, kv_indptr, kv_indices, group_size,
+                       sm_scale, num_splits, out, lse, ws, ws_bytes, stream, false);
+}
+
+ca_status ca_dense_paged_chunk_attention(const ca_problem* p, const uint16_t* q,
+                                         const uint16_t* k_pool, const uint16_t* v_pool,
+                                         const int32_t* page_table, float sm_scale,
+                                         int32_t num_splits, uint16_t* out, float* lse,
+                                         void* ws, size_t ws_bytes, void* stream) {
+  if (p == nullptr) return fail(CA_ERR_NULL, "problem is NULL");
+  if (p->num_kv_heads < 1 || p->num_q_heads < p->num_kv_heads)
+    return fail(CA_ERR_SHAPE, "num_q_heads must be >= num_kv_heads >= 1");
+  // one execution group per KV head: every head of the KV group shares the table
+  int gs = p->num_q_heads / p->num_kv_heads;
+  while (gs > 1 && 128 % gs != 0) --gs;
+  return run_attention(p, q, k_pool, v_pool, page_table, nullptr, nullptr, gs, sm_scale,
+                       num_splits, out, lse, ws, ws_bytes, stream, true);
+}
+
+ca_status ca_validate_tables(const ca_problem* p, int32_t group_size, const int32_t* kv_indptr,
+                             const int32_t* kv_indices, int32_t require_chunk_open,
+                             void* stream) {
+  ca::Dims d;
+  if (group_size < 1) return fail(CA_ERR_GROUP, "group_size must be >= 1");
+  ca_status s = check(p, group_size, &d);
+  if (s != CA_OK) return s;
+  if (!kv_indptr || !kv_indices) return fail(CA_ERR_NULL, "kv_indptr and kv_indices are required");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return hip_status(e, "stream synchronize");
+  const int G = d.Hq / group_size;
+  const int R = d.B * G;
+  const size_t cap = (size_t)R * d.max_kv_blocks;
+  std::vector<int32_t> ip(R + 1);
+  if ((e = hipMemcpy(ip.data(), kv_indptr, (R + 1) * sizeof(int32_t), hipMemcpyDeviceToHost)) !=
+      hipSuccess)
+    return hip_status(e, "copy kv_indptr");
+  if (ip[0] != 0) return fail(CA_ERR_INVALID_TABLE, "kv_indptr[0] = %d, expected 0", ip[0]);
+  for (int r = 0; r < R; ++r)
+    if (ip[r + 1] < ip[r] || (size_t)ip[r + 1] > cap)
+      return fail(CA_ERR_INVALID_TABLE, "kv_indptr[%d..%d] = %d..%d is not a valid range", r,
+                  r + 1, ip[r], ip[r + 1]);
+  std::vector<int32_t> ix(ip[R] > 0 ? ip[R] : 1);
+  if (ip[R] > 0 && (e = hipMemcpy(ix.data(), kv_indices, ip[R] * sizeof(int32_t),
+                                  hipMemcpyDeviceToHost)) != hipSuccess)
+    return hip_status(e, "copy kv_indices");
+  for (int r = 0; r < R; ++r) {
+    const int b = r / G;
+    const int nc = p->cached_len_host[b] / d.page;
+    const int nkb = nc + d.chunk_blocks;
+    int prev = -1, chunk_seen = 0;
+    for (int x = ip[r]; x < ip[r + 1]; ++x) {
+      const int j = ix[x];
+      if (j <= prev || j < 0 || j >= nkb)
+        return fail(CA_ERR_INVALID_TABLE, "row %d entry %d = %d (previous %d, nKB %d)", r,
+                    x - ip[r], j, prev, nkb);
+      if (j >= nc) ++chunk_seen;
+      prev = j;
+    }
+    if (require_chunk_open && chunk_seen != d.chunk_blocks)
+      return fail(CA_ERR_INVALID_TABLE, "row %d holds %d of the %d chunk blocks", r, chunk_seen,
+                  d.chunk_blocks);
+  }
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,318 @@
+// Mean-pooled block-score selector: Q/K block pooling, block scores and the
+// exact top-k + sink + local + chunk-causal mask emission.
+//
+// The paper plugs any lightweight block-level pattern search in front of the
+// block union (Sec. 3.1, Sec. 3.2 first paragraph); per-chunk search cost is
+// first-order under chunked prefill (Sec. 2.1), so every stage here is a
+// single streaming pass: pooling is HBM-bound, scores are a tiny fp32
+// contraction, selection is an in-LDS radix select per mask row.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace ca {
+
+// ---------------------------------------------------------------------------
+// Pooling: one wavefront reduces `rows` rows of D bf16 (row stride `stride`
+// elements) to their fp32 mean.  Lane l reads 16 bytes of row (l / CPR) +
+// k*RPI, so each load instruction covers RPI whole rows contiguously.
+// ---------------------------------------------------------------------------
+template <int D>
+__device__ __forceinline__ void pool_rows(const uint16_t* __restrict__ base, size_t stride,
+                                          int rows, float* __restrict__ out) {
+  constexpr int CPR = D / 8;           // 16-byte chunks per row
+  constexpr int RPI = kWave / CPR;     // rows per load instruction
+  const int l = lane_id();
+  const int chunk = l % CPR;
+  float acc[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) acc[e] = 0.f;
+  for (int r = l / CPR; r < rows; r += RPI) {
+    const uint4 v = *reinterpret_cast<const uint4*>(base + (size_t)r * stride + chunk * 8);
+    acc[0] += bf16_lo(v.x); acc[1] += bf16_hi(v.x);
+    acc[2] += bf16_lo(v.y); acc[3] += bf16_hi(v.y);
+    acc[4] += bf16_lo(v.z); acc[5] += bf16_hi(v.z);
+    acc[6] += bf16_lo(v.w); acc[7] += bf16_hi(v.w);
+  }
+#pragma unroll
+  for (int o = CPR; o < kWave; o <<= 1) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] += __shfl_xor(acc[e], o, kWave);
+  }
+  if (l < CPR) {
+    const float inv = 1.0f / (float)rows;
+    float4* dst = reinterpret_cast<float4*>(out + chunk * 8);
+    dst[0] = make_float4(acc[0] * inv, acc[1] * inv, acc[2] * inv, acc[3] * inv);
+    dst[1] = make_float4(acc[4] * inv, acc[5] * inv, acc[6] * inv, acc[7] * inv);
+  }
+}
+
+// One wave per (b, h, i).
+template <int D>
+__global__ __launch_bounds__(256) void pool_q_kernel(const uint16_t* __restrict__ q,
+                                                     float* __restrict__ q_mean, int B, int C,
+                                                     int Hq, int q_block, int nqb) {
+  const int w = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (w >= B * Hq * nqb) return;
+  const int i = w % nqb;
+  const int h = (w / nqb) % Hq;
+  const int b = w / (nqb * Hq);
+  const uint16_t* base = q + (((size_t)b * C + (size_t)i * q_block) * Hq + h) * D;
+  pool_rows<D>(base, (size_t)Hq * D, q_block, q_mean + (size_t)w * D);
+}
+
+// One wave per (b, kvh, j), j in [first_block, nKB_b).
+template <int D>
+__global__ __launch_bounds__(256) void pool_k_kernel(const uint16_t* __restrict__ k_pool,
+                                                     const int32_t* __restrict__ page_table,
+                                                     const int32_t* __restrict__ cached_len,
+                                                     float* __restrict__ k_mean, int Hkv,
+                                                     int max_kv_blocks, int chunk_blocks,
+                                                     int first_block) {
+  const int bk = blockIdx.y;  // b * Hkv + kvh
+  const int b = bk / Hkv;
+  const int j = first_block + blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int nkb = cached_len[b] / kPage + chunk_blocks;
+  if (j >= nkb) return;
+  const int page = page_table[(size_t)bk * max_kv_blocks + j];
+  pool_rows<D>(k_pool + (size_t)page * kPage * D, D, kPage,
+               k_mean + ((size_t)bk * max_kv_blocks + j) * D);
+}
+
+// ---------------------------------------------------------------------------
+// Scores: for one (b, kvh), the ratio*nQB pooled query rows are contiguous in
+// q_mean and the matching score rows are contiguous too.  A workgroup
+// computes a 64-row x 64-block tile with fp32 FMAs (d ascending), staging
+// 32-wide slices of both operands in LDS.
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(256) void scores_kernel(const float* __restrict__ q_mean,
+                                                     const float* __restrict__ k_mean,
+                                                     const int32_t* __restrict__ cached_len,
+                                                     float* __restrict__ scores, int Hq, int Hkv,
+                                                     int nqb, int max_kv_blocks) {
+  constexpr int DS = 32;
+  __shared__ float qs[64][DS + 1];
+  __shared__ float ks[64][DS + 1];
+  const int bk = blockIdx.z;
+  const int b = bk / Hkv, kvh = bk % Hkv;
+  const int ratio = Hq / Hkv;
+  const int nrows = ratio * nqb;
+  const int nc = cached_len[b] / kPage;
+  const int j0 = blockIdx.x * 64, r0 = blockIdx.y * 64;
+  if (j0 >= nc) return;
+  const size_t row_base = ((size_t)b * Hq + (size_t)kvh * ratio) * nqb;
+  const float* qrow = q_mean + row_base * D;
+  const float* krow = k_mean + ((size_t)bk * max_kv_blocks) * D;
+  const int t = threadIdx.x;
+  const int tr = t >> 4, tc = t & 15;
+  float acc[4][4];
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) acc[a][c] = 0.f;
+  for (int d0 = 0; d0 < D; d0 += DS) {
+    for (int x = t; x < 64 * DS; x += 256) {
+      const int r = x / DS, d = x % DS;
+      qs[r][d] = (r0 + r < nrows) ? qrow[(size_t)(r0 + r) * D + d0 + d] : 0.f;
+      ks[r][d] = (j0 + r < nc) ? krow[(size_t)(j0 + r) * D + d0 + d] : 0.f;
+    }
+    __syncthreads();
+#pragma unroll 4
+    for (int d = 0; d < DS; ++d) {
+      float qv[4], kv[4];
+#pragma unroll
+      for (int a = 0; a < 4; ++a) qv[a] = qs[tr + 16 * a][d];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) kv[c] = ks[tc + 16 * c][d];
+#pragma unroll
+      for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) acc[a][c] = fmaf(qv[a], kv[c], acc[a][c]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int a = 0; a < 4; ++a) {
+    const int r = r0 + tr + 16 * a;
+    if (r >= nrows) continue;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int j = j0 + tc + 16 * c;
+      if (j < nc) scores[(row_base + r) * max_kv_blocks + j] = acc[a][c];
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Selection: one workgroup (4 waves) per mask row (b, h, i).
+// Scores become order-preserving uint32 keys (-0.0 folded onto +0.0); a
+// 4-pass, 8-bit radix select finds the k-th largest key T and how many keys
+// equal to T still have to be taken; those are the ones with the smallest
+// block index (ranked by a ballot/prefix count).  Words of the mask are then
+// emitted directly from wave ballots: wave v of a 256-block slab owns word
+// slab/64 + v.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint32_t order_key(float f) {
+  uint32_t u = __float_as_uint(f);
+  if (u == 0x80000000u) u = 0u;
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// Block-wide inclusive scan of one int per thread (256 threads).
+__device__ __forceinline__ int block_scan_256(int v, int* wave_tot) {
+  const int w = threadIdx.x >> 6;
+  int incl = wave_inclusive_scan(v);
+  if (lane_id() == 63) wave_tot[w] = incl;
+  __syncthreads();
+  int add = 0;
+  for (int x = 0; x < w; ++x) add += wave_tot[x];
+  __syncthreads();
+  return incl + add;
+}
+
+__global__ __launch_bounds__(256) void select_kernel(const float* __restrict__ scores,
+                                                     const int32_t* __restrict__ cached_len,
+                                                     uint64_t* __restrict__ masks, int Hq,
+                                                     int nqb, int max_kv_blocks, int W,
+                                                     int chunk_blocks, int qblock_blocks,
+                                                     float top_frac, int sink_blocks,
+                                                     int local_blocks) {
+  extern __shared__ uint32_t keys[];
+  __shared__ int hist[256];
+  __shared__ int wave_tot[4];
+  __shared__ int sh_digit, sh_above;
+  const int row = blockIdx.x;
+  const int t = threadIdx.x;
+  const int wv = t >> 6;
+  const int i = row % nqb;
+  const int b = row / (nqb * Hq);
+  const int nc = cached_len[b] / kPage;
+  const int nkb = nc + chunk_blocks;
+  int k = 0;
+  if (nc > 0) {
+    k = (int)ceilf(top_frac * (float)nc);
+    k = k < 0 ? 0 : (k > nc ? nc : k);
+  }
+  const float* s = scores + (size_t)row * max_kv_blocks;
+  for (int j = t; j < nc; j += 256) keys[j] = order_key(s[j]);
+  __syncthreads();
+
+  const bool take_all = (k == nc);
+  uint32_t prefix = 0u, pmask = 0u;
+  int remaining = k;
+  if (k > 0 && !take_all) {
+    for (int shift = 24; shift >= 0; shift -= 8) {
+      hist[t] = 0;
+      __syncthreads();
+      for (int j = t; j < nc; j += 256) {
+        const uint32_t key = keys[j];
+        if ((key & pmask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1);
+      }
+      __syncthreads();
+      // thread t <-> digit 255 - t: the inclusive scan counts keys with digit >= d
+      const int d = 255 - t;
+      const int c = hist[d];
+      const int incl = block_scan_256(c, wave_tot);
+      const int excl = incl - c;
+      if (excl < remaining && remaining <= incl) {
+        sh_digit = d;
+        sh_above = excl;
+      }
+      __syncthreads();
+      prefix |= (uint32_t)sh_digit << shift;
+      pmask |= 0xffu << shift;
+      remaining -= sh_above;
+      __syncthreads();
+    }
+  }
+  const uint32_t T = prefix;
+
+  const int causal_end = nc + (i + 1) * qblock_blocks;
+  const int sink_end = sink_blocks < nc ? sink_blocks : nc;
+  const int local_begin = nc - local_blocks;
+  int carry = 0;  // keys equal to T already seen, in block order
+  uint64_t* mrow = masks + (size_t)row * W;
+  for (int base = 0; base < W * 64; base += 256) {
+    const int j = base + t;
+    const bool cached = j < nc;
+    const uint32_t key = cached ? keys[j] : 0u;
+    const bool eq = cached && k > 0 && !take_all && key == T;
+    const uint64_t bal = __ballot(eq);
+    if (lane_id() == 0) wave_tot[wv] = __popcll(bal);
+    __syncthreads();
+    int before = carry, total = 0;
+    for (int x = 0; x < 4; ++x) {
+      if (x < wv) before += wave_tot[x];
+      total += wave_tot[x];
+    }
+    const int rank = before + lanes_below(bal);
+    const bool sel = cached && (take_all || (k > 0 && (key > T || (eq && rank < remaining))));
+    const bool forced = j < nkb && ((j < sink_end) || (j >= local_begin && j < nc) ||
+                                    (j >= nc && j < causal_end));
+    const uint64_t word = __ballot(sel || forced);
+    const int widx = j >> 6;
+    if (lane_id() == 0 && widx < W) mrow[widx] = word;
+    carry += total;
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// launchers
+// ---------------------------------------------------------------------------
+hipError_t launch_pool_q(const Dims& d, const uint16_t* q, float* q_mean, hipStream_t st) {
+  const int waves = d.B * d.Hq * d.nqb;
+  dim3 grid((waves + 3) / 4);
+  if (d.D == 128)
+    pool_q_kernel<128><<<grid, 256, 0, st>>>(q, q_mean, d.B, d.C, d.Hq, d.q_block, d.nqb);
+  else
+    pool_q_kernel<64><<<grid, 256, 0, st>>>(q, q_mean, d.B, d.C, d.Hq, d.q_block, d.nqb);
+  return hipGetLastError();
+}
+
+hipError_t launch_pool_k(const Dims& d, const uint16_t* k_pool, const int32_t* page_table,
+                         const int32_t* cached_len, int first_block, float* k_mean,
+                         hipStream_t st) {
+  const int span = d.max_nkb - first_block;
+  if (span <= 0) return hipSuccess;
+  dim3 grid((span + 3) / 4, d.B * d.Hkv);
+  if (d.D == 128)
+    pool_k_kernel<128><<<grid, 256, 0, st>>>(k_pool, page_table, cached_len, k_mean, d.Hkv,
+                                             d.max_kv_blocks, d.chunk_blocks, first_block);
+  else
+    pool_k_kernel<64><<<grid, 256, 0, st>>>(k_pool, page_table, cached_len, k_mean, d.Hkv,
+                                            d.max_kv_blocks, d.chunk_blocks, first_block);
+  return hipGetLastError();
+}
+
+hipError_t launch_scores(const Dims& d, const float* q_mean, const float* k_mean,
+                         const int32_t* cached_len, float* scores, hipStream_t st) {
+  if (d.max_nc <= 0) return hipSuccess;
+  const int nrows = (d.Hq / d.Hkv) * d.nqb;
+  dim3 grid((d.max_nc + 63) / 64, (nrows + 63) / 64, d.B * d.Hkv);
+  if (d.D == 128)
+    scores_kernel<128><<<grid, 256, 0, st>>>(q_mean, k_mean, cached_len, scores, d.Hq, d.Hkv,
+                                             d.nqb, d.max_kv_blocks);
+  else
+    scores_kernel<64><<<grid, 256, 0, st>>>(q_mean, k_mean, cached_len, scores, d.Hq, d.Hkv,
+                                            d.nqb, d.max_kv_blocks);
+  return hipGetLastError();
+}
+
+hipError_t raise_select_lds(int bytes) {
+  return hipFuncSetAttribute(reinterpret_cast<const void*>(&select_kernel),
+                             hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+}
+
+hipError_t launch_select(const Dims& d, const float* scores, const int32_t* cached_len,
+                         float top_frac, int sink_blocks, int local_blocks, uint64_t* masks,
+                         hipStream_t st) {
+  dim3 grid(d.B * d.Hq * d.nqb);
+  const size_t lds = (size_t)(d.max_nc > 0 ? d.max_nc : 1) * sizeof(uint32_t);
+  select_kernel<<<grid, 256, lds, st>>>(scores, cached_len, masks, d.Hq, d.nqb,
+                                        d.max_kv_blocks, d.W, d.chunk_blocks,
+                                        d.q_block / kPage, top_frac, sink_blocks, local_blocks);
+  return hipGetLastError();
+}
+
+}  // namespace ca

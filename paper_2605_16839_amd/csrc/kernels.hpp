@@ -1,0 +1,56 @@
+// Internal launcher interface between the C ABI (api.hip) and the kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ca {
+
+// Validated problem sizes, derived once on the host.
+struct Dims {
+  int B, Hq, Hkv, D, page, q_block, C, max_kv_blocks;
+  int nqb;           // C / q_block
+  int W;             // mask words per row
+  int chunk_blocks;  // C / page
+  int max_nc;        // max_b cached blocks
+  int max_nkb;       // max_b cached + chunk blocks
+};
+
+hipError_t launch_pool_q(const Dims& d, const uint16_t* q, float* q_mean, hipStream_t st);
+hipError_t launch_pool_k(const Dims& d, const uint16_t* k_pool, const int32_t* page_table,
+                         const int32_t* cached_len, int first_block, float* k_mean,
+                         hipStream_t st);
+hipError_t launch_scores(const Dims& d, const float* q_mean, const float* k_mean,
+                         const int32_t* cached_len, float* scores, hipStream_t st);
+hipError_t launch_select(const Dims& d, const float* scores, const int32_t* cached_len,
+                         float top_frac, int sink_blocks, int local_blocks, uint64_t* masks,
+                         hipStream_t st);
+hipError_t raise_select_lds(int bytes);
+
+size_t tables_ws_bytes(const Dims& d, int group_size);
+hipError_t launch_tables(const Dims& d, const uint64_t* masks, const int32_t* cached_len,
+                         int group_size, int32_t* kv_indptr, int32_t* kv_indices, void* ws,
+                         hipStream_t st);
+
+// Attention over per-group tables (dense = identity tables, no table read).
+struct AttnLaunch {
+  const uint16_t* q;
+  const uint16_t* k_pool;
+  const uint16_t* v_pool;
+  const int32_t* page_table;
+  const int32_t* kv_indptr;
+  const int32_t* kv_indices;
+  const int32_t* cached_len;
+  uint16_t* out;
+  float* lse;
+  int group_size;
+  float sm_scale;
+  int splits;        // >= 1
+  void* ws;          // partials when splits > 1
+  bool dense;
+};
+int attn_query_tile(int group_size);                    // chunk queries per workgroup
+int attn_base_workgroups(const Dims& d, int group_size);
+size_t attn_ws_bytes(const Dims& d, int splits);
+hipError_t launch_attention(const Dims& d, const AttnLaunch& a, hipStream_t st);
+
+}  // namespace ca

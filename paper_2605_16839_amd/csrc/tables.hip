@@ -1,0 +1,124 @@
+// Block-union tables: Q-block union + intra-group union (bitwise OR) and
+// compaction of the union bitmask into CSR kv_indptr / kv_indices
+// (Sec. 3.2 displayed equations; App. B.2 for the CSR pair).
+//
+// Two launches, both integer-only and deterministic:
+//   union_kernel   one workgroup per table row r = b*G + g: OR the
+//                  group_size*nQB mask rows of the group word by word in LDS
+//                  (ds_or_b64), clip to nKB_b, store the row's union words and
+//                  its popcount;
+//   compact_kernel one workgroup per row: row offset = sum of the counts of
+//                  earlier rows (no atomics), then 256-block slabs are
+//                  compacted with wave ballots + a 4-wave prefix in LDS, which
+//                  writes the set block ids in ascending order.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace ca {
+
+constexpr int kMaxWords = kMaxKvBlocks / 64;
+
+__global__ __launch_bounds__(256) void union_kernel(const uint64_t* __restrict__ masks,
+                                                    const int32_t* __restrict__ cached_len,
+                                                    uint64_t* __restrict__ gwords,
+                                                    int32_t* __restrict__ counts, int Hq,
+                                                    int nqb, int W, int group_size, int G,
+                                                    int chunk_blocks) {
+  __shared__ unsigned long long acc[kMaxWords];
+  __shared__ int red[4];
+  const int r = blockIdx.x;
+  const int b = r / G, g = r % G;
+  const int t = threadIdx.x;
+  const int nkb = cached_len[b] / kPage + chunk_blocks;
+  for (int w = t; w < W; w += 256) acc[w] = 0ull;
+  __syncthreads();
+  const int rows = group_size * nqb;
+  const uint64_t* src = masks + ((size_t)b * Hq + (size_t)g * group_size) * nqb * W;
+  if (W <= 256 && (256 % W) == 0) {
+    // fixed word per thread: OR privately, then one LDS atomic
+    const int w = t % W;
+    unsigned long long v = 0ull;
+    for (int row = t / W; row < rows; row += 256 / W) v |= src[(size_t)row * W + w];
+    if (v) atomicOr(&acc[w], v);
+  } else {
+    for (int x = t; x < rows * W; x += 256) {
+      const unsigned long long v = src[x];
+      if (v) atomicOr(&acc[x % W], v);
+    }
+  }
+  __syncthreads();
+  int cnt = 0;
+  for (int w = t; w < W; w += 256) {
+    unsigned long long v = acc[w];
+    const int lo = w * 64;
+    if (lo >= nkb) v = 0ull;
+    else if (nkb - lo < 64) v &= (~0ull >> (64 - (nkb - lo)));
+    gwords[(size_t)r * W + w] = v;
+    cnt += __popcll(v);
+  }
+  cnt = wave_sum(cnt);
+  if (lane_id() == 0) red[t >> 6] = cnt;
+  __syncthreads();
+  if (t == 0) counts[r] = red[0] + red[1] + red[2] + red[3];
+}
+
+__global__ __launch_bounds__(256) void compact_kernel(const uint64_t* __restrict__ gwords,
+                                                      const int32_t* __restrict__ counts,
+                                                      int32_t* __restrict__ kv_indptr,
+                                                      int32_t* __restrict__ kv_indices, int W) {
+  __shared__ int red[4];
+  __shared__ int wave_tot[4];
+  const int r = blockIdx.x;
+  const int t = threadIdx.x;
+  const int wv = t >> 6;
+  int part = 0;
+  for (int x = t; x < r; x += 256) part += counts[x];
+  part = wave_sum(part);
+  if (lane_id() == 0) red[wv] = part;
+  __syncthreads();
+  const int row_start = red[0] + red[1] + red[2] + red[3];
+  if (t == 0) {
+    if (r == 0) kv_indptr[0] = 0;
+    kv_indptr[r + 1] = row_start + counts[r];
+  }
+  const uint64_t* gw = gwords + (size_t)r * W;
+  int carry = 0;
+  for (int base = 0; base < W * 64; base += 256) {
+    const int j = base + t;
+    const int w = j >> 6;
+    const bool bit = (w < W) && ((gw[w] >> (j & 63)) & 1ull);
+    const uint64_t bal = __ballot(bit);
+    if (lane_id() == 0) wave_tot[wv] = __popcll(bal);
+    __syncthreads();
+    int before = carry, total = 0;
+    for (int x = 0; x < 4; ++x) {
+      if (x < wv) before += wave_tot[x];
+      total += wave_tot[x];
+    }
+    if (bit) kv_indices[row_start + before + lanes_below(bal)] = j;
+    carry += total;
+    __syncthreads();
+  }
+}
+
+size_t tables_ws_bytes(const Dims& d, int group_size) {
+  const size_t R = (size_t)d.B * (d.Hq / group_size);
+  return R * d.W * sizeof(uint64_t) + R * sizeof(int32_t);
+}
+
+hipError_t launch_tables(const Dims& d, const uint64_t* masks, const int32_t* cached_len,
+                         int group_size, int32_t* kv_indptr, int32_t* kv_indices, void* ws,
+                         hipStream_t st) {
+  const int G = d.Hq / group_size;
+  const int R = d.B * G;
+  uint64_t* gwords = static_cast<uint64_t*>(ws);
+  int32_t* counts = reinterpret_cast<int32_t*>(gwords + (size_t)R * d.W);
+  union_kernel<<<R, 256, 0, st>>>(masks, cached_len, gwords, counts, d.Hq, d.nqb, d.W,
+                                  group_size, G, d.chunk_blocks);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  compact_kernel<<<R, 256, 0, st>>>(gwords, counts, kv_indptr, kv_indices, d.W);
+  return hipGetLastError();
+}
+
+}  // namespace ca

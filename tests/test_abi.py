@@ -1,0 +1,99 @@
+"""The C-ABI library: it loads, exports every declared entry point, and its
+host-side validation rejects bad problems before anything is enqueued.
+No compute call is made here (no GPU in this tier)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "compactattn.h")
+
+ca = pytest.importorskip("paper_2605_16839_amd")
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    names = set(re.findall(r"\b(ca_[a-z_0-9]+)\s*\(", src))
+    return names
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(ca.LIB_PATH):
+        pytest.fail("libcompactattn.so is not built (run __graft_entry__.build())")
+    return ca.load()
+
+
+def test_exports_every_declared_symbol(lib):
+    declared = _declared()
+    assert declared, "no declarations parsed"
+    assert declared == set(ca.EXPORTED)
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert lib.ca_abi_version() == 1
+
+
+def _prob(**kw):
+    base = dict(batch=1, num_q_heads=32, num_kv_heads=8, head_dim=128, q_block=128,
+                chunk_len=2048, max_kv_blocks=2048, cached_len=[129024], device=None)
+    base.update(kw)
+    return ca.Problem(**base)
+
+
+def _status(p, group_size=4):
+    return ca.load().ca_check_problem(p.ref, group_size)
+
+
+def test_valid_problems(lib):
+    assert _status(_prob()) == 0
+    assert _status(_prob(batch=4, cached_len=[16384, 32768, 65536, 126976], max_kv_blocks=2016)) == 0
+    assert _status(_prob(num_q_heads=4, num_kv_heads=1, head_dim=64, q_block=64, chunk_len=256,
+                         max_kv_blocks=20, cached_len=[1024])) == 0
+    assert _status(_prob(cached_len=[0])) == 0
+
+
+@pytest.mark.parametrize("kw,group,code", [
+    (dict(head_dim=96), 4, "CA_ERR_UNSUPPORTED"),
+    (dict(q_block=32), 4, "CA_ERR_UNSUPPORTED"),
+    (dict(chunk_len=2000), 4, "CA_ERR_UNALIGNED"),
+    (dict(cached_len=[129000]), 4, "CA_ERR_UNALIGNED"),
+    (dict(cached_len=[-64]), 4, "CA_ERR_UNALIGNED"),
+    (dict(cached_len=[129088]), 4, "CA_ERR_SHAPE"),           # needs 2049 blocks
+    (dict(max_kv_blocks=20000, cached_len=[64]), 4, "CA_ERR_SHAPE"),
+    (dict(num_kv_heads=5), 4, "CA_ERR_SHAPE"),
+    (dict(), 3, "CA_ERR_GROUP"),
+    (dict(), 8, "CA_ERR_GROUP"),
+    (dict(batch=0, cached_len=[]), 4, "CA_ERR_SHAPE"),
+])
+def test_invalid_problems(lib, kw, group, code):
+    s = _status(_prob(**kw), group)
+    assert lib.ca_status_string(s).decode() == code
+    assert lib.ca_last_error_detail().decode() != ""
+
+
+def test_null_problem_and_null_buffers(lib):
+    assert lib.ca_status_string(lib.ca_check_problem(None, 4)).decode() == "CA_ERR_NULL"
+    p = _prob()
+    # device cached_len missing: rejected before any launch
+    s = lib.ca_build_block_tables(p.ref, None, 4, None, None, None, 0, None)
+    assert lib.ca_status_string(s).decode() == "CA_ERR_NULL"
+    s = lib.ca_chunk_attention(p.ref, None, None, None, None, None, None, 4, 0.1, 1,
+                               None, None, None, 0, None)
+    assert lib.ca_status_string(s).decode() == "CA_ERR_NULL"
+
+
+def test_workspace_sizes(lib):
+    p = _prob()
+    # union words (8 rows x 32 words x 8 B) + 8 counts
+    assert ca.tables_workspace_bytes(p, 4) == 8 * 32 * 8 + 8 * 4
+    assert ca.attention_workspace_bytes(p, 4, 1) == 0
+    assert ca.attention_workspace_bytes(p, 4, 2) == 2 * 32 * 2048 * 129 * 4
+    # 512 query tiles already fill the GPU: automatic choice needs no workspace
+    assert ca.attention_workspace_bytes(p, 4, 0) == 0
+    tiny = _prob(num_q_heads=4, num_kv_heads=1, head_dim=64, q_block=64, chunk_len=256,
+                 max_kv_blocks=20, cached_len=[1024])
+    assert ca.attention_workspace_bytes(tiny, 4, 0) > 0
+    assert ca.tables_workspace_bytes(p, 3) == 0        # invalid group -> 0

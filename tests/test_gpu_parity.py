@@ -1,0 +1,396 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Tables and masks are compared bit for bit; attention outputs within the
+tolerances of tests/_helpers.py.  Inputs come from the seeded generator;
+nothing the GPU computes is ever fed to the oracle.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from _helpers import (bf16_dev, bf16_host_f64, compare_attention, device_inputs, i32_dev,
+                      rows_by_head, sample_rows, u64_dev, u64_host)
+
+pytestmark = pytest.mark.gpu
+
+ca = pytest.importorskip("paper_2605_16839_amd")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    ca.load()
+
+
+def _problem(w):
+    return ca.Problem.from_workload(w)
+
+
+def _params(w):
+    return oracle.EstimatorParams(w.top_frac, w.sink_blocks, w.local_blocks)
+
+
+def _oracle_tables(masks, w):
+    nkb = [w.n_kv_blocks(b) for b in range(w.batch)]
+    T = oracle.block_tables(masks, w.group_size, nkb)
+    return T, oracle.tables_to_csr(T)
+
+
+def _gpu_tables(p, masks_np, gs):
+    ip, ix = ca.build_block_tables(p, u64_dev(masks_np), gs)
+    torch.cuda.synchronize()
+    return ip.cpu().numpy(), ix.cpu().numpy()
+
+
+def _assert_tables_equal(gpu, ref):
+    ip, ix = gpu
+    rip, rix = ref
+    assert np.array_equal(ip, rip), "kv_indptr differs"
+    assert np.array_equal(ix[:rip[-1]], rix), "kv_indices differ"
+
+
+def _oracle_rows(d, tables, gs, sm_scale, rows):
+    """Oracle attention on the sampled (b, h, t) rows only."""
+    w = d["workload"]
+    ref = np.full((w.batch, w.chunk_len, w.num_q_heads, w.head_dim), np.nan)
+    ref_lse = np.full((w.batch, w.num_q_heads, w.chunk_len), np.nan)
+    for (b, h), ts in rows_by_head(rows).items():
+        o, l = oracle.chunk_attention(d["q"], d["k_pool"], d["v_pool"], d["page_table"],
+                                      d["cached_len"], tables, gs, sm_scale,
+                                      heads=[(b, h)], queries=ts)
+        ref[b, ts, h] = o[b, ts, h]
+        ref_lse[b, h, ts] = l[b, h, ts]
+    return ref, ref_lse
+
+
+def _run_attention(p, x, tables, gs, sm_scale, num_splits=0, dense=False):
+    w_lse = torch.empty((p.batch, p.num_q_heads, p.chunk_len), dtype=torch.float32, device="cuda")
+    if dense:
+        out, _ = ca.dense_paged_chunk_attention(p, x["q"], (x["k"], x["v"]), x["pt"], sm_scale,
+                                                num_splits=num_splits, lse=w_lse)
+    else:
+        dt = (i32_dev(tables[0]), i32_dev(tables[1])) if isinstance(tables[0], np.ndarray) else tables
+        out, _ = ca.chunk_attention(p, x["q"], (x["k"], x["v"]), x["pt"], dt, gs, sm_scale,
+                                    num_splits=num_splits, lse=w_lse)
+    torch.cuda.synchronize()
+    return bf16_host_f64(out), w_lse.cpu().numpy().astype(np.float64)
+
+
+# ---------------------------------------------------------------------------
+# tables
+# ---------------------------------------------------------------------------
+def test_tables_tiny_bitexact(workload_inputs):
+    d = workload_inputs("tiny_gqa_1k")
+    w = d["workload"]
+    p = _problem(w)
+    for gs in (1, 2, 4):
+        nkb = [w.n_kv_blocks(0)]
+        ref = oracle.tables_to_csr(oracle.block_tables(d["masks"], gs, nkb))
+        _assert_tables_equal(_gpu_tables(p, d["masks"], gs), ref)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_tables_adversarial(seed):
+    """Ragged batch, garbage bits beyond nKB, word-edge bits, empty and full rows."""
+    rng = np.random.default_rng(100 + seed)
+    cached = [0, 64 * 31, 64 * 64, 64 * 129][: 1 + seed % 4]
+    cached = [int(c) for c in cached]
+    B, Hq, Hkv, C, qb = len(cached), 16, 2, 256, 64
+    maxkb = max(c // 64 for c in cached) + C // 64 + 3
+    W = (maxkb + 63) // 64
+    p = ca.Problem(B, Hq, Hkv, 64, qb, C, maxkb, cached)
+    raw = rng.integers(0, 2**63, size=(B, Hq, C // qb, W), dtype=np.int64).astype(np.uint64)
+    dens = rng.random((B, Hq, C // qb, W * 64)) < [0.0, 0.01, 0.2, 1.0][seed]
+    masks = synth.gen.pack_bits(dens, W) | (raw & np.uint64(1 << (seed * 7)))
+    masks[0, 0, 0, :] = 0                                     # an all-zero row
+    if W > 1:
+        masks[-1, -1, -1, 0] |= np.uint64(1) << np.uint64(63)  # word edge 63/64
+        masks[-1, -1, -1, 1] |= np.uint64(1)
+    for gs in (1, 2, 4, 8):
+        nkb = [c // 64 + C // 64 for c in cached]
+        ref = oracle.tables_to_csr(oracle.block_tables(masks, gs, nkb))
+        _assert_tables_equal(_gpu_tables(p, masks, gs), ref)
+
+
+@pytest.mark.parametrize("name", ["llama8b_32k", "llama8b_128k_final", "batched_ragged_4seq"])
+def test_tables_workloads_bitexact(name, workload_inputs, oracle_estimate):
+    d = workload_inputs(name)
+    w = d["workload"]
+    masks, _ = oracle_estimate(name)
+    p = _problem(w)
+    _, ref = _oracle_tables(masks, w)
+    got = _gpu_tables(p, masks, w.group_size)
+    _assert_tables_equal(got, ref)
+    assert np.array_equal(got[0], _gpu_tables(p, masks, w.group_size)[0])   # deterministic
+    ca.validate_tables(p, w.group_size, (i32_dev(got[0]), i32_dev(got[1])))
+
+
+# ---------------------------------------------------------------------------
+# estimator
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("name", ["tiny_gqa_1k", "llama8b_32k", "batched_ragged_4seq"])
+def test_pooling_and_scores(name, workload_inputs, oracle_estimate):
+    d = workload_inputs(name)
+    w = d["workload"]
+    p = _problem(w)
+    x = device_inputs(d)
+    _, parts = oracle_estimate(name) if w.mask_kind == "estimator" else (None, None)
+    if parts is None:
+        nkb = [w.n_kv_blocks(b) for b in range(w.batch)]
+        qm = oracle.q_block_means(d["q"], w.q_block)
+        km = oracle.k_block_means(d["k_pool"], d["page_table"], nkb)
+        sc = oracle.block_scores(qm, km, [w.n_cached_blocks(b) for b in range(w.batch)])
+    else:
+        qm, km, sc = parts["q_mean"], parts["k_mean"], parts["scores"]
+    g_qm = ca.pool_q_blocks(p, x["q"])
+    g_km = ca.pool_k_blocks(p, x["k"], x["pt"])
+    g_sc = ca.block_scores(p, g_qm, g_km)
+    torch.cuda.synchronize()
+    g_qm, g_km, g_sc = (t.cpu().numpy().astype(np.float64) for t in (g_qm, g_km, g_sc))
+    assert np.abs(g_qm - qm).max() <= 1e-6 * max(1.0, np.abs(qm).max())
+    for b in range(w.batch):
+        nkb = w.n_kv_blocks(b)
+        assert np.abs(g_km[b, :, :nkb] - km[b, :, :nkb]).max() <= 1e-6 * max(1.0, np.abs(km).max())
+        nc = w.n_cached_blocks(b)
+        if nc:
+            err = np.abs(g_sc[b, :, :, :nc] - sc[b]).max()
+            assert err <= 1e-5 * max(1.0, np.abs(sc[b]).max()), err
+
+
+@pytest.mark.parametrize("nc_list,top_frac,sink,local", [
+    ([0], 0.05, 1, 4), ([1], 0.5, 1, 4), ([5], 1.0, 0, 0), ([63], 0.3, 2, 3),
+    ([64], 0.05, 1, 4), ([65, 7, 0], 0.25, 1, 4), ([300], 0.0, 1, 4), ([2016], 0.05, 1, 4),
+    ([2016, 1984, 31], 0.08, 1, 4), ([4000], 0.5, 3, 8),
+])
+def test_select_tied_scores_bitexact(nc_list, top_frac, sink, local):
+    """Selection on generated float32 scores full of exact ties and signed zeros."""
+    B, Hq, Hkv, C, qb = len(nc_list), 4, 1, 256, 128
+    maxkb = max(nc_list) + C // 64
+    p = ca.Problem(B, Hq, Hkv, 64, qb, C, maxkb, [64 * n for n in nc_list])
+    nqb = C // qb
+    scores = np.full((B, Hq, nqb, maxkb), np.nan, dtype=np.float32)
+    per_b = []
+    for b, nc in enumerate(nc_list):
+        s = synth.tied_scores(7 * b + nc, Hq * nqb, max(nc, 1), n_distinct=5)[:, :nc]
+        s = s.reshape(Hq, nqb, nc)
+        scores[b, :, :, :nc] = s
+        per_b.append(s)
+    params = oracle.EstimatorParams(top_frac, sink, local)
+    ref = oracle.masks_from_scores(per_b, nc_list, 64, qb, p.words, params)
+    got = ca.select_blocks(p, torch.from_numpy(scores).cuda(), top_frac, sink, local)
+    torch.cuda.synchronize()
+    assert np.array_equal(u64_host(got), ref)
+
+
+def _near_tie_check(gpu_masks, ref_masks, scores64, w, tol):
+    """Rows may differ only where the fp64 scores of swapped blocks tie within tol."""
+    gb, rb = oracle.unpack_masks(gpu_masks), oracle.unpack_masks(ref_masks)
+    flips = 0
+    for b in range(w.batch):
+        nc = w.n_cached_blocks(b)
+        k = oracle.n_selected(w.top_frac, nc)
+        for h in range(w.num_q_heads):
+            for i in range(w.n_qblocks):
+                if np.array_equal(gb[b, h, i], rb[b, h, i]):
+                    continue
+                flips += 1
+                diff = np.nonzero(gb[b, h, i] != rb[b, h, i])[0]
+                assert diff.max() < nc, "a forced bit differs"
+                s = scores64[b][h, i]
+                kth = np.sort(s)[::-1][k - 1]
+                assert np.all(np.abs(s[diff] - kth) <= tol), (b, h, i, diff, s[diff], kth)
+                assert gb[b, h, i, :nc].sum() == rb[b, h, i, :nc].sum()
+    return flips
+
+
+@pytest.mark.parametrize("name", ["llama8b_32k", "llama8b_128k_final", "batched_ragged_4seq"])
+def test_estimator_end_to_end(name, workload_inputs, oracle_estimate):
+    d = workload_inputs(name)
+    w = d["workload"]
+    p = _problem(w)
+    x = device_inputs(d)
+    ref, parts = oracle_estimate(name)
+    got, _ = ca.estimate_masks(p, x["q"], x["k"], x["pt"], w.top_frac, w.sink_blocks,
+                               w.local_blocks)
+    torch.cuda.synchronize()
+    gm = u64_host(got)
+    flips = _near_tie_check(gm, ref, parts["scores"], w, tol=1e-5)
+    print(f"{name}: {flips} near-tie rows differ")
+    bits = oracle.unpack_masks(gm)
+    assert all(bits[b, h, i, j] for (b, kvh, j, h, i) in d["needles"])
+
+
+# ---------------------------------------------------------------------------
+# attention
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("splits", [1, 3, 0])
+def test_attention_tiny_full(splits, workload_inputs):
+    d = workload_inputs("tiny_gqa_1k")
+    w = d["workload"]
+    p = _problem(w)
+    x = device_inputs(d)
+    T, csr = _oracle_tables(d["masks"], w)
+    ref, ref_lse = oracle.chunk_attention(d["q"], d["k_pool"], d["v_pool"], d["page_table"],
+                                          d["cached_len"], T, w.group_size, w.sm_scale)
+    got, lse = _run_attention(p, x, csr, w.group_size, w.sm_scale, num_splits=splits)
+    print(compare_attention(got, lse, ref, ref_lse))
+
+
+@pytest.mark.parametrize("gs,scale_mult", [(1, 1.0), (2, 1.0), (4, 8.0), (1, 8.0)])
+def test_attention_tiny_groups_and_sharp(gs, scale_mult, workload_inputs):
+    """Sparse random tables per group size; x8 scale makes the softmax peaky (O(1) outputs)."""
+    d = workload_inputs("tiny_gqa_1k")
+    w = d["workload"]
+    p = _problem(w)
+    x = device_inputs(d)
+    nc = w.n_cached_blocks(0)
+    masks = synth.random_masks(5, 1, 4, w.n_qblocks, w.q_block, 64, [nc], w.chunk_len, w.words, 0.05)
+    T = oracle.block_tables(masks, gs, [w.n_kv_blocks(0)])
+    sm = w.sm_scale * scale_mult
+    ref, ref_lse = oracle.chunk_attention(d["q"], d["k_pool"], d["v_pool"], d["page_table"],
+                                          d["cached_len"], T, gs, sm)
+    for splits in (1, 2):
+        got, lse = _run_attention(p, x, oracle.tables_to_csr(T), gs, sm, num_splits=splits)
+        print(compare_attention(got, lse, ref, ref_lse))
+
+
+def test_attention_first_chunk_no_cache():
+    w = synth.get_workload("tiny_gqa_1k", cached_lens=(0,), max_kv_blocks=4)
+    d = synth.make_inputs(w)
+    p = _problem(w)
+    x = device_inputs(d)
+    T, csr = _oracle_tables(d["masks"], w)
+    ref, ref_lse = oracle.chunk_attention(d["q"], d["k_pool"], d["v_pool"], d["page_table"],
+                                          d["cached_len"], T, w.group_size, w.sm_scale)
+    got, lse = _run_attention(p, x, csr, w.group_size, w.sm_scale, num_splits=1)
+    compare_attention(got, lse, ref, ref_lse)
+    got, lse = _run_attention(p, x, None, w.group_size, w.sm_scale, num_splits=1, dense=True)
+    compare_attention(got, lse, ref, ref_lse)
+
+
+@pytest.mark.parametrize("name", ["llama8b_32k", "llama8b_128k_final", "batched_ragged_4seq"])
+def test_attention_workloads_sampled(name, workload_inputs, oracle_estimate):
+    d = workload_inputs(name)
+    w = d["workload"]
+    p = _problem(w)
+    x = device_inputs(d)
+    masks, _ = oracle_estimate(name)
+    T, csr = _oracle_tables(masks, w)
+    got, lse = _run_attention(p, x, csr, w.group_size, w.sm_scale, num_splits=0)
+    rows = sample_rows(w.batch, w.num_q_heads, w.chunk_len, seed=w.seed)
+    ref, ref_lse = _oracle_rows(d, T, w.group_size, w.sm_scale, rows)
+    print(name, compare_attention(got, lse, ref, ref_lse, rows))
+    # sharp softmax on the same tables
+    got, lse = _run_attention(p, x, csr, w.group_size, w.sm_scale * 8, num_splits=0)
+    ref, ref_lse = _oracle_rows(d, T, w.group_size, w.sm_scale * 8, rows[::3])
+    print(name, "sharp", compare_attention(got, lse, ref, ref_lse, rows[::3]))
+
+
+@pytest.mark.parametrize("name", ["llama8b_32k", "batched_ragged_4seq"])
+def test_dense_baseline_sampled(name, workload_inputs):
+    d = workload_inputs(name)
+    w = d["workload"]
+    p = _problem(w)
+    x = device_inputs(d)
+    got, lse = _run_attention(p, x, None, w.group_size, w.sm_scale, dense=True)
+    T = oracle.dense_tables([w.n_kv_blocks(b) for b in range(w.batch)], w.num_groups)
+    rows = sample_rows(w.batch, w.num_q_heads, w.chunk_len, seed=w.seed + 1, heads_per_b=2,
+                       n_random=8)
+    ref, ref_lse = _oracle_rows(d, T, w.group_size, w.sm_scale, rows)
+    print(name, compare_attention(got, lse, ref, ref_lse, rows))
+
+
+def test_attention_page_permutation_invariance(workload_inputs, oracle_estimate):
+    """Moving pages in the pool (and the page table with them) changes no output bit."""
+    name = "llama8b_32k"
+    d = workload_inputs(name)
+    w = d["workload"]
+    p = _problem(w)
+    x = device_inputs(d)
+    masks, _ = oracle_estimate(name)
+    _, csr = _oracle_tables(masks, w)
+    tabs = (i32_dev(csr[0]), i32_dev(csr[1]))
+    out1, _ = ca.chunk_attention(p, x["q"], (x["k"], x["v"]), x["pt"], tabs, w.group_size,
+                                 w.sm_scale)
+    pi = torch.randperm(x["k"].shape[0], generator=torch.Generator().manual_seed(3)).cuda()
+    k2 = torch.empty_like(x["k"]); k2[pi] = x["k"]
+    v2 = torch.empty_like(x["v"]); v2[pi] = x["v"]
+    pt2 = x["pt"].clone()
+    valid = pt2 >= 0
+    pt2[valid] = pi.to(torch.int32)[pt2[valid].long()]
+    out2, _ = ca.chunk_attention(p, x["q"], (k2, v2), pt2, tabs, w.group_size, w.sm_scale)
+    out3, _ = ca.chunk_attention(p, x["q"], (x["k"], x["v"]), x["pt"], tabs, w.group_size,
+                                 w.sm_scale)
+    torch.cuda.synchronize()
+    assert torch.equal(out1.view(torch.int16), out2.view(torch.int16))
+    assert torch.equal(out1.view(torch.int16), out3.view(torch.int16))   # deterministic
+
+
+def test_attention_negative_control(workload_inputs):
+    """Dropping one selected block from a table is visible in the LSE comparison."""
+    d = workload_inputs("tiny_gqa_1k")
+    w = d["workload"]
+    p = _problem(w)
+    x = device_inputs(d)
+    T, csr = _oracle_tables(d["masks"], w)
+    got, lse = _run_attention(p, x, csr, w.group_size, w.sm_scale, num_splits=1)
+    T2 = [[row[:3] + row[4:] for row in per_b] for per_b in T]
+    ref, ref_lse = oracle.chunk_attention(d["q"], d["k_pool"], d["v_pool"], d["page_table"],
+                                          d["cached_len"], T2, w.group_size, w.sm_scale)
+    with pytest.raises(AssertionError):
+        compare_attention(got, lse, ref, ref_lse)
+
+
+# ---------------------------------------------------------------------------
+# the 64-chunk sweep: estimator with incremental block means, tables, attention
+# ---------------------------------------------------------------------------
+@pytest.mark.timeout(900)
+def test_sweep_all_chunks():
+    base = synth.get_workload("sweep_128k_64chunks")
+    seq = synth.make_sweep_sequence(base)
+    params = _params(base)
+    page = base.page_size
+    full_nkb = seq.page_table_full.shape[2]
+    km_all = oracle.k_block_means(seq.k_pool, seq.page_table_full, [full_nkb])
+    k_dev, v_dev = bf16_dev(seq.k_pool), bf16_dev(seq.v_pool)
+    k_mean = torch.zeros((1, base.num_kv_heads, base.max_kv_blocks, base.head_dim),
+                         dtype=torch.float32, device="cuda")
+    attn_chunks = {0, 1, 31, 62, 63}
+    total_flips = 0
+    for c in range(seq.n_chunks):
+        d = seq.inputs(c)
+        w = d["workload"]
+        p = ca.Problem.from_workload(w)
+        q_dev, pt_dev = bf16_dev(d["q"]), i32_dev(d["page_table"])
+        gm, bufs = ca.estimate_masks(p, q_dev, k_dev, pt_dev, w.top_frac, w.sink_blocks,
+                                     w.local_blocks, k_mean=k_mean,
+                                     k_mean_first_block=c * (w.chunk_len // page))
+        tabs = ca.build_block_tables(p, gm, w.group_size)
+        torch.cuda.synchronize()
+        ref, parts = oracle.estimate_masks(d["q"], seq.k_pool, d["page_table"], d["cached_len"],
+                                           page, w.q_block, w.chunk_len, w.words, params,
+                                           return_parts=True, k_mean=km_all)
+        gmn = u64_host(gm)
+        total_flips += _near_tie_check(gmn, ref, parts["scores"], w, tol=1e-5)
+        for (b, kvh, j, h, i) in d["needles"]:
+            assert oracle.unpack_masks(gmn)[b, h, i, j], (c, j, h, i)
+        gip, gix = tabs[0].cpu().numpy(), tabs[1].cpu().numpy()
+        if np.array_equal(gmn, ref):
+            _assert_tables_equal((gip, gix), _oracle_tables(ref, w)[1])
+        if c in attn_chunks:
+            T = [[gix[gip[g]:gip[g + 1]].tolist() for g in range(w.num_groups)]]
+            if np.array_equal(gmn, ref):
+                assert T == _oracle_tables(ref, w)[0]
+            T_ref = _oracle_tables(ref, w)[0]
+            x = dict(q=q_dev, k=k_dev, v=v_dev, pt=pt_dev)
+            got, lse = _run_attention(p, x, _oracle_tables(ref, w)[1], w.group_size, w.sm_scale)
+            rows = sample_rows(1, w.num_q_heads, w.chunk_len, seed=c, heads_per_b=2, n_random=6)
+            dd = dict(d, k_pool=seq.k_pool, v_pool=seq.v_pool)
+            r_out, r_lse = _oracle_rows(dd, T_ref, w.group_size, w.sm_scale, rows)
+            compare_attention(got, lse, r_out, r_lse, rows)
+    print(f"sweep: {total_flips} near-tie rows differ over 64 chunks")
