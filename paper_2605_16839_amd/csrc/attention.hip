@@ -8,19 +8,25 @@
 //     head of the group (group_size heads x 128/group_size chunk queries) and
 //     each KV page staged in LDS feeds all 128 rows;
 //   * wave w owns rows 32w..32w+31, one (head, query) pair per MFMA column;
-//   * per table entry j the workgroup streams page page_table[b,kvh,j] (64
-//     keys) of K and V from HBM into LDS (double buffered, one barrier per
-//     page), then each wave computes S^T = K Q^T (keys x queries) with
-//     v_mfma_f32_32x32x16_bf16, so that every lane holds one query column
-//     and the softmax row statistics stay in-lane, and O^T += V^T P^T;
-//   * V is stored transposed in LDS ([d][key]) with key order permuted
-//     inside each 16-key group so that the P^T fragment produced by the QK
-//     accumulator layout can be fed to the PV MFMA without any shuffle;
-//   * causal masking is applied only to chunk blocks whose keys can be later
-//     than the workgroup's first query, by absolute position 64*j + r versus
-//     cached_len + t (positions from the logical block id, App. B.2);
-//     entries past the workgroup's last visible block end the loop (tables
-//     are ascending).
+//   * the pages of the table are copied from HBM straight into LDS with
+//     16-byte direct-to-LDS loads (no register round trip); each lane picks
+//     its source chunk so that the LDS image is XOR-swizzled and the MFMA
+//     operand reads are bank-conflict free;
+//   * each wave computes S^T = K Q^T (keys x queries) with
+//     v_mfma_f32_32x32x16_bf16, so every lane holds one query column and the
+//     softmax statistics stay in-lane, then O^T += V^T P^T, the V^T
+//     fragments coming straight from the row-major V page through the gfx950
+//     transpose read ds_read_b64_tr_b16;
+//   * software pipeline: while the softmax of page i runs on the VALU, the
+//     MFMAs of S^T for page i+1 are issued and the copies of the K of page
+//     i+2 and the V of page i+1 are in flight; one barrier per page;
+//   * causal masking is applied only to the trailing entries whose keys can
+//     be later than the workgroup's first query, by absolute position
+//     64*j + r versus cached_len + t (positions from the logical block id,
+//     App. B.2); entries past the workgroup's last visible block are dropped
+//     (tables are ascending).
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -46,22 +52,122 @@ struct AttnArgs {
   float scale_log2;
 };
 
-// Position of key k (0..63) of a page inside the transposed V tile: bits 2
-// and 3 of k are swapped, which makes the 8 keys that one lane contributes
-// to a PV MFMA k-step contiguous.
-__device__ __forceinline__ int vperm(int k) {
-  return (k & ~12) | ((k & 4) << 1) | ((k & 8) >> 1);
+// Swizzled position (16-byte chunk) of chunk c of row r in an LDS page tile.
+// K is read 16 bytes per lane by 8 consecutive rows: c ^ (r & 7).
+// V is read 8 bytes per lane by the transpose read, 4 consecutive rows x 2
+// chunks per 16-lane group: c ^ 2*(r & 3).
+__device__ __forceinline__ int k_swz(int r, int c) { return c ^ (r & 7); }
+__device__ __forceinline__ int v_swz(int r, int c) { return c ^ ((r & 3) << 1); }
+
+// 2^x with a single v_exp_f32 (results below the normal range flush to 0,
+// which only affects softmax weights < 2^-126).
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+template <bool DENSE>
+__device__ __forceinline__ int table_entry(const int32_t* __restrict__ idx, int base, int e) {
+  return DENSE ? e : idx[base + e];
+}
+
+typedef __attribute__((address_space(3))) void lds_void;
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+
+// Copy one page (64 rows x D bf16, contiguous in HBM) into an LDS tile with
+// direct-to-LDS loads.  Each wave instruction fills 1 KB of the tile, lane l
+// writing bytes [16l, 16l+16); the lane's source is the chunk that the
+// swizzle maps there (the swizzles are involutions).
+template <int D, bool IS_V>
+__device__ __forceinline__ void page_to_lds(const uint16_t* __restrict__ src, uint16_t* tile,
+                                            int wv, int lane) {
+  constexpr int CPR = D / 8;                             // 16-byte chunks per row
+  constexpr int ROWS_PER_INST = 64 / CPR;                // rows per 1 KB instruction
+  constexpr int INST_PER_WAVE = (64 * D * 2) / 1024 / 4; // 4 waves share a page
+#pragma unroll
+  for (int m = 0; m < INST_PER_WAVE; ++m) {
+    const int inst = wv * INST_PER_WAVE + m;
+    const int r = inst * ROWS_PER_INST + lane / CPR;
+    const int cpos = lane % CPR;
+    const int c = IS_V ? v_swz(r, cpos) : k_swz(r, cpos);
+    __builtin_amdgcn_global_load_lds(src + r * D + c * 8, (lds_void*)(tile + inst * 512), 16,
+                                     0, 0);
+  }
+}
+
+// Wait for this wave's direct-to-LDS copies and tell the compiler that the
+// tiles behind p0/p1 changed (the copies write them outside its view).
+__device__ __forceinline__ void copies_landed(void* p0, void* p1) {
+  __builtin_amdgcn_s_waitcnt(0);
+  __asm__ volatile("" : : "v"(p0), "v"(p1) : "memory");
+}
+
+// max / sum of a value and its partner in the other half of the wave
+// (lanes l and l^32 hold the same query column).
+__device__ __forceinline__ float halves_max(float x) {
+  const uint32_t u = __float_as_uint(x);
+  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float halves_sum(float x) {
+  const uint32_t u = __float_as_uint(x);
+  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// S^T tile of one page: keys 0..31 in .lo, 32..63 in .hi.
+struct STile {
+  f32x16 lo, hi;
+};
+
+// S^T = K Q^T over one page: A = K rows (32 keys x 16 d per k-step), B = Q^T.
+template <int D>
+__device__ __forceinline__ void qk_page(STile& st, const uint16_t* __restrict__ ks,
+                                        const bf16x8 (&qf)[D / 16], int col, int half) {
+#pragma unroll
+  for (int v = 0; v < 16; ++v) { st.lo[v] = 0.f; st.hi[v] = 0.f; }
+#pragma unroll
+  for (int x = 0; x < D / 16; ++x) {
+    const int c = 2 * x + half;
+    const bf16x8 a0 = *reinterpret_cast<const bf16x8*>(ks + col * D + 8 * k_swz(col, c));
+    const bf16x8 a1 =
+        *reinterpret_cast<const bf16x8*>(ks + (32 + col) * D + 8 * k_swz(32 + col, c));
+    st.lo = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, qf[x], st.lo, 0, 0, 0);
+    st.hi = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, qf[x], st.hi, 0, 0, 0);
+  }
+}
+
+// V^T fragment for PV k-step kk and d tile x.  Lane (d row `col`, half) needs
+// the 8 keys 16kk + 4half + {0..3} and 16kk + 8 + 4half + {0..3}, the key
+// order of the P^T fragment taken from the S^T accumulator layout.  In a
+// 16-lane group, source lane 4m + q points at key row base + m, d columns
+// 4q..4q+3 of the group's 16 d; the transpose read then hands lane i the
+// four keys of d = group base + i.
+template <int D>
+__device__ __forceinline__ bf16x8 vt_frag(const uint16_t* __restrict__ vs, int lane, int x,
+                                          int kk) {
+  const int grp = lane >> 4, sl = lane & 15;
+  const int m = sl >> 2, q = sl & 3;
+  const int d = 32 * x + 16 * (grp & 1) + 4 * q;
+  const int c = d >> 3, sub = d & 7;
+  const int r0 = 16 * kk + 4 * (grp >> 1) + m;
+  const int r1 = r0 + 8;
+  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (lds_i16x4*)(vs + r0 * D + 8 * v_swz(r0, c) + sub));
+  const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (lds_i16x4*)(vs + r1 * D + 8 * v_swz(r1, c) + sub));
+  // whole-vector casts only: element-wise bf16 <-> i16 moves are not reliable
+  const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
+  const u32x4 w = {l2[0], l2[1], h2[0], h2[1]};
+  return __builtin_bit_cast(bf16x8, w);
 }
 
 template <int D, bool DENSE>
 __global__ __launch_bounds__(256, 2) void paged_attention_kernel(const AttnArgs a) {
-  constexpr int KS = D + 8;    // bf16 per K row in LDS (16-byte pad)
-  constexpr int VS = 64 + 8;   // bf16 per V^T row in LDS
-  constexpr int NKS = D / 16;  // k-steps of the QK contraction
-  constexpr int NDT = D / 32;  // 32-row d tiles of O^T
-  constexpr int KLD = (64 * D / 8) / 256;  // 16-byte K loads per thread per page
-  __shared__ __attribute__((aligned(16))) uint16_t k_s[2][64 * KS];
-  __shared__ __attribute__((aligned(16))) uint16_t vt_s[2][D * VS];
+  constexpr int NKS = D / 16;   // k-steps of the QK contraction
+  constexpr int NDT = D / 32;   // 32-row d tiles of O^T
+  constexpr int PAGE = 64 * D;  // bf16 per page tile
+  constexpr int COPIES = 2 * (64 * D * 2) / 1024 / 4;   // copy instructions per wave per step
+  __shared__ __attribute__((aligned(1024))) uint16_t k_s[2][PAGE];
+  __shared__ __attribute__((aligned(1024))) uint16_t v_s[2][PAGE];
 
   const int t = threadIdx.x;
   const int wv = t >> 6;
@@ -122,146 +228,131 @@ __global__ __launch_bounds__(256, 2) void paged_attention_kernel(const AttnArgs 
   float m_run = -INFINITY;   // running max, log2-scaled units
   float l_run = 0.f;         // partial row sum over this lane's keys
 
-  uint4 kreg[KLD];
-  uint4 vreg[4];
-  const int vkb = t >> 4;          // V: 4-key block 0..15
-  const int vd0 = (t & 15) * 8;    // V: first of 8 d values
-  const bool v_active = vd0 < D;
-
-  auto entry = [&](int e) -> int { return DENSE ? e : a.kv_indices[tbase + e]; };
-  auto load_page = [&](int j) {
-    const size_t page = (size_t)ptab[j];
-    const uint16_t* kb = a.k_pool + page * (kPage * D);
-    const uint16_t* vb = a.v_pool + page * (kPage * D);
-#pragma unroll
-    for (int x = 0; x < KLD; ++x) {
-      const int c = t + 256 * x;
-      kreg[x] = *reinterpret_cast<const uint4*>(kb + (size_t)c * 8);
-    }
-    if (v_active) {
-#pragma unroll
-      for (int rr = 0; rr < 4; ++rr)
-        vreg[rr] = *reinterpret_cast<const uint4*>(vb + (size_t)(4 * vkb + rr) * D + vd0);
-    }
-  };
-  auto store_page = [&](int st) {
-    uint16_t* ks = k_s[st];
-#pragma unroll
-    for (int x = 0; x < KLD; ++x) {
-      const int c = t + 256 * x;
-      const int row = c / (D / 8), c8 = c % (D / 8);
-      *reinterpret_cast<uint4*>(ks + row * KS + c8 * 8) = kreg[x];
-    }
-    if (v_active) {
-      uint16_t* vt = vt_s[st];
-      const int kpos = vperm(4 * vkb);
-      const uint32_t* w0 = reinterpret_cast<const uint32_t*>(&vreg[0]);
-      const uint32_t* w1 = reinterpret_cast<const uint32_t*>(&vreg[1]);
-      const uint32_t* w2 = reinterpret_cast<const uint32_t*>(&vreg[2]);
-      const uint32_t* w3 = reinterpret_cast<const uint32_t*>(&vreg[3]);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int sh = (e & 1) * 16;
-        const uint32_t x0 = (w0[e >> 1] >> sh) & 0xffffu;
-        const uint32_t x1 = (w1[e >> 1] >> sh) & 0xffffu;
-        const uint32_t x2 = (w2[e >> 1] >> sh) & 0xffffu;
-        const uint32_t x3 = (w3[e >> 1] >> sh) & 0xffffu;
-        uint2 pk;
-        pk.x = x0 | (x1 << 16);
-        pk.y = x2 | (x3 << 16);
-        *reinterpret_cast<uint2*>(vt + (vd0 + e) * VS + kpos) = pk;
-      }
-    }
-  };
-
-  int e = e0;
-  int j = (e < e1) ? entry(e) : 0;
-  bool active = (e < e1) && (j <= j_last);
-  if (active) {
-    load_page(j);
-    store_page(0);
+  // Table entries e0 .. e_end-1 (entries past the last visible block are
+  // dropped; tables are ascending).  Those whose keys can be later than the
+  // first query of the tile need the causal mask and form a suffix.
+  int e_end = e1;
+  if (DENSE) {
+    e_end = e1 < j_last + 1 ? e1 : j_last + 1;
+  } else {
+    while (e_end > e0 && table_entry<DENSE>(a.kv_indices, tbase, e_end - 1) > j_last) --e_end;
   }
-  __syncthreads();
-  int stage = 0;
-  while (active) {
-    int jn = 0;
-    const bool nxt = (e + 1 < e1) && ((jn = entry(e + 1)) <= j_last);
-    if (nxt) load_page(jn);
+  const int n = e_end - e0;
+  int n_main = n;
+  while (n_main > 0 &&
+         kPage * table_entry<DENSE>(a.kv_indices, tbase, e0 + n_main - 1) + kPage - 1 > mask_from)
+    --n_main;
+  auto page_ptr = [&](const uint16_t* pool, int i) -> const uint16_t* {
+    return pool + (size_t)ptab[table_entry<DENSE>(a.kv_indices, tbase, e0 + i)] * (kPage * D);
+  };
 
-    // ---- S^T = K Q^T for the 64 keys of block j (two 32-key tiles) ----
-    const uint16_t* ks = k_s[stage];
-    f32x16 s0, s1;
-#pragma unroll
-    for (int v = 0; v < 16; ++v) { s0[v] = 0.f; s1[v] = 0.f; }
-#pragma unroll
-    for (int x = 0; x < NKS; ++x) {
-      const bf16x8 a0 = *reinterpret_cast<const bf16x8*>(ks + col * KS + 16 * x + 8 * half);
-      const bf16x8 a1 = *reinterpret_cast<const bf16x8*>(ks + (32 + col) * KS + 16 * x + 8 * half);
-      s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, qf[x], s0, 0, 0, 0);
-      s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, qf[x], s1, 0, 0, 0);
-    }
-    // key index inside the page of accumulator slot v: 8*(v/4) + 4*half + v%4
-    if (kPage * j + kPage - 1 > mask_from) {
-      const int kb = kPage * j + 4 * half;
+  // Prologue: K and V of page 0 and K of page 1 in LDS, then S^T of page 0.
+  STile sa, sb;
+  if (n > 0) {
+    page_to_lds<D, false>(page_ptr(a.k_pool, 0), k_s[0], wv, lane);
+    page_to_lds<D, true>(page_ptr(a.v_pool, 0), v_s[0], wv, lane);
+    page_to_lds<D, false>(page_ptr(a.k_pool, n > 1 ? 1 : 0), k_s[1], wv, lane);
+  }
+  copies_landed(k_s, v_s);
+  __syncthreads();
+  if (n > 0) qk_page<D>(sa, k_s[0], qf, col, half);
+  __syncthreads();
+
+  // Pipeline step i (page e0 + i, buffer s = i & 1): copies of K(i+2) -> K[s]
+  // and V(i+1) -> V[s^1] go out first; S^T(i+1) from K[s^1] is interleaved
+  // with the softmax of page i; then O^T += V^T P^T from V[s].
+  auto step = [&](auto masked, int i, STile& cur, STile& nxt) __attribute__((always_inline)) {
+    const int s = i & 1;
+    const int i1 = i + 1 < n ? i + 1 : n - 1;   // clamped: copies stay valid, results unused
+    const int i2 = i + 2 < n ? i + 2 : n - 1;
+    page_to_lds<D, false>(page_ptr(a.k_pool, i2), k_s[s], wv, lane);
+    page_to_lds<D, true>(page_ptr(a.v_pool, i1), v_s[s ^ 1], wv, lane);
+    qk_page<D>(nxt, k_s[s ^ 1], qf, col, half);
+
+    // ---- online softmax of page e0 + i ----
+    if constexpr (decltype(masked)::value) {
+      const int j = table_entry<DENSE>(a.kv_indices, tbase, e0 + i);
+      // key of accumulator slot v: 64*j + 8*(v/4) + 4*half + v%4 (+32 in .hi)
+      const int lim = qpos - kPage * j - 4 * half;
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const int kp = kb + 8 * (v >> 2) + (v & 3);
-        if (kp > qpos) s0[v] = -INFINITY;
-        if (kp + 32 > qpos) s1[v] = -INFINITY;
+        const int kp = 8 * (v >> 2) + (v & 3);
+        if (kp > lim) cur.lo[v] = -INFINITY;
+        if (kp + 32 > lim) cur.hi[v] = -INFINITY;
       }
     }
-    float mx = -INFINITY;
+    float mx = fmaxf(cur.lo[0], cur.hi[0]);
 #pragma unroll
-    for (int v = 0; v < 16; ++v) mx = fmaxf(mx, fmaxf(s0[v], s1[v]));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+    for (int v = 1; v < 16; ++v) mx = fmaxf(mx, fmaxf(cur.lo[v], cur.hi[v]));
+    mx = halves_max(mx);
     const float m_new = fmaxf(m_run, mx * a.scale_log2);
     const float m_base = (m_new == -INFINITY) ? 0.f : m_new;
-    const float alpha = exp2f(m_run - m_base);
+    const float alpha = fast_exp2(m_run - m_base);
+    m_run = m_new;
     float psum = 0.f;
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-      s0[v] = exp2f(fmaf(s0[v], a.scale_log2, -m_base));
-      s1[v] = exp2f(fmaf(s1[v], a.scale_log2, -m_base));
-      psum += s0[v] + s1[v];
+      cur.lo[v] = fast_exp2(fmaf(cur.lo[v], a.scale_log2, -m_base));
+      cur.hi[v] = fast_exp2(fmaf(cur.hi[v], a.scale_log2, -m_base));
+      psum += cur.lo[v] + cur.hi[v];
     }
     l_run = fmaf(l_run, alpha, psum);
-    m_run = m_new;
+    // P^T fragments: k-step kk covers accumulator slots 8*(kk%2)..+7
+    bf16x8 pf[4];
+#pragma unroll
+    for (int x = 0; x < 8; ++x) {
+      pf[0][x] = (__bf16)cur.lo[x];
+      pf[1][x] = (__bf16)cur.lo[8 + x];
+      pf[2][x] = (__bf16)cur.hi[x];
+      pf[3][x] = (__bf16)cur.hi[8 + x];
+    }
+    __builtin_amdgcn_sched_group_barrier(0x020, COPIES, 0);  // page copies first
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);       // first K fragments
+#pragma unroll
+    for (int x = 0; x < 2 * NKS; ++x) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);     // 1 QK MFMA
+      __builtin_amdgcn_sched_group_barrier(0x402, 6, 0);     // 6 VALU / transcendental
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);     // next K fragment
+    }
+
     if (__ballot(alpha != 1.0f)) {
 #pragma unroll
       for (int x = 0; x < NDT; ++x)
 #pragma unroll
         for (int v = 0; v < 16; ++v) o[x][v] *= alpha;
     }
-    // ---- P^T fragments: k-step kk covers accumulator slots 8*(kk%2)..+7 ----
-    bf16x8 pf[4];
-#pragma unroll
-    for (int x = 0; x < 8; ++x) {
-      pf[0][x] = (__bf16)s0[x];
-      pf[1][x] = (__bf16)s0[8 + x];
-      pf[2][x] = (__bf16)s1[x];
-      pf[3][x] = (__bf16)s1[8 + x];
-    }
+
     // ---- O^T += V^T P^T ----
-    const uint16_t* vt = vt_s[stage];
+    const uint16_t* vs = v_s[s];
 #pragma unroll
-    for (int x = 0; x < NDT; ++x) {
+    for (int kk = 0; kk < 4; ++kk) {
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
-        const bf16x8 av =
-            *reinterpret_cast<const bf16x8*>(vt + (32 * x + col) * VS + 16 * kk + 8 * half);
-        o[x] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pf[kk], o[x], 0, 0, 0);
-      }
+      for (int x = 0; x < NDT; ++x)
+        o[x] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vt_frag<D>(vs, lane, x, kk), pf[kk],
+                                                       o[x], 0, 0, 0);
     }
-    if (nxt) store_page(stage ^ 1);
+    copies_landed(k_s, v_s);
     __syncthreads();
-    stage ^= 1;
-    ++e;
-    j = jn;
-    active = nxt;
+  };
+  using Plain = std::integral_constant<bool, false>;
+  using Masked = std::integral_constant<bool, true>;
+  int i = 0;
+  for (; i + 1 < n_main; i += 2) {
+    step(Plain{}, i, sa, sb);
+    step(Plain{}, i + 1, sb, sa);
+  }
+  if (i < n_main) {
+    step(Plain{}, i, sa, sb);
+    ++i;
+    sa = sb;
+  }
+  for (; i < n; ++i) {
+    step(Masked{}, i, sa, sb);
+    sa = sb;
   }
 
   // ---- epilogue ----
-  const float l_tot = l_run + __shfl_xor(l_run, 32, kWave);
+  const float l_tot = halves_sum(l_run);
   const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
   const float lse_val = l_tot > 0.f ? (m_run + log2f(l_tot)) * kLn2 : -INFINITY;
   const size_t qrow_idx = ((size_t)b * a.Hq + head) * a.C + tq;   // [B, Hq, C] order
@@ -295,6 +386,7 @@ __global__ __launch_bounds__(256, 2) void paged_attention_kernel(const AttnArgs 
     if (half == 0) a.part_lse[prow] = lse_val;
   }
 }
+
 
 // Split-KV merge: lse = log sum_i exp(lse_i), out = sum_i exp(lse_i - lse) o_i.
 // One 32-lane half-wave per (b, h, t) row, 4 floats of d per lane (D = 128)
