@@ -17,9 +17,9 @@
 //     softmax statistics stay in-lane, then O^T += V^T P^T, the V^T
 //     fragments coming straight from the row-major V page through the gfx950
 //     transpose read ds_read_b64_tr_b16;
-//   * software pipeline: while the softmax of page i runs on the VALU, the
-//     MFMAs of S^T for page i+1 are issued and the copies of the K of page
-//     i+2 and the V of page i+1 are in flight; one barrier per page;
+//   * the copy of page i+1 is in flight while page i is processed (double
+//     buffered tiles, one barrier per page); the MFMA and softmax phases of
+//     the two workgroups resident on a CU overlap on each SIMD;
 //   * causal masking is applied only to the trailing entries whose keys can
 //     be later than the workgroup's first query, by absolute position
 //     64*j + r versus cached_len + t (positions from the logical block id,
@@ -53,11 +53,22 @@ struct AttnArgs {
 };
 
 // Swizzled position (16-byte chunk) of chunk c of row r in an LDS page tile.
-// K is read 16 bytes per lane by 8 consecutive rows: c ^ (r & 7).
-// V is read 8 bytes per lane by the transpose read, 4 consecutive rows x 2
-// chunks per 16-lane group: c ^ 2*(r & 3).
-__device__ __forceinline__ int k_swz(int r, int c) { return c ^ (r & 7); }
-__device__ __forceinline__ int v_swz(int r, int c) { return c ^ ((r & 3) << 1); }
+// gfx950 LDS has 64 banks of 4 bytes; a 16-byte read is served 16 lanes per
+// cycle and an 8-byte read 32 lanes per cycle.
+// K is read 16 bytes per lane by 16 consecutive rows at one chunk: the 16
+// rows must land on 16 different 16-byte bank slots of the 256-byte bank
+// window (a D = 64 row is half a window, so rows pair up).
+// V is read 8 bytes per lane by the transpose read, 32 lanes covering 4
+// consecutive rows x 4 chunks: each row's aligned group of 4 chunks must
+// move to a different aligned group of the window.
+template <int D>
+__device__ __forceinline__ int k_swz(int r, int c) {
+  return D == 128 ? (c ^ (r & 15)) : (c ^ ((r >> 1) & 7));
+}
+template <int D>
+__device__ __forceinline__ int v_swz(int r, int c) {
+  return D == 128 ? (c ^ ((r & 3) << 2)) : (c ^ (((r >> 1) & 1) << 2));
+}
 
 // 2^x with a single v_exp_f32 (results below the normal range flush to 0,
 // which only affects softmax weights < 2^-126).
@@ -87,9 +98,9 @@ __device__ __forceinline__ void page_to_lds(const uint16_t* __restrict__ src, ui
     const int inst = wv * INST_PER_WAVE + m;
     const int r = inst * ROWS_PER_INST + lane / CPR;
     const int cpos = lane % CPR;
-    const int c = IS_V ? v_swz(r, cpos) : k_swz(r, cpos);
-    __builtin_amdgcn_global_load_lds(src + r * D + c * 8, (lds_void*)(tile + inst * 512), 16,
-                                     0, 0);
+    const int c = IS_V ? v_swz<D>(r, cpos) : k_swz<D>(r, cpos);
+    const uint32_t off = (uint32_t)(r * D + c * 8);   // unsigned: scalar base + 32-bit offset
+    __builtin_amdgcn_global_load_lds(src + off, (lds_void*)(tile + inst * 512), 16, 0, 0);
   }
 }
 
@@ -127,9 +138,9 @@ __device__ __forceinline__ void qk_page(STile& st, const uint16_t* __restrict__ 
 #pragma unroll
   for (int x = 0; x < D / 16; ++x) {
     const int c = 2 * x + half;
-    const bf16x8 a0 = *reinterpret_cast<const bf16x8*>(ks + col * D + 8 * k_swz(col, c));
+    const bf16x8 a0 = *reinterpret_cast<const bf16x8*>(ks + col * D + 8 * k_swz<D>(col, c));
     const bf16x8 a1 =
-        *reinterpret_cast<const bf16x8*>(ks + (32 + col) * D + 8 * k_swz(32 + col, c));
+        *reinterpret_cast<const bf16x8*>(ks + (32 + col) * D + 8 * k_swz<D>(32 + col, c));
     st.lo = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, qf[x], st.lo, 0, 0, 0);
     st.hi = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, qf[x], st.hi, 0, 0, 0);
   }
@@ -151,9 +162,9 @@ __device__ __forceinline__ bf16x8 vt_frag(const uint16_t* __restrict__ vs, int l
   const int r0 = 16 * kk + 4 * (grp >> 1) + m;
   const int r1 = r0 + 8;
   const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-      (lds_i16x4*)(vs + r0 * D + 8 * v_swz(r0, c) + sub));
+      (lds_i16x4*)(vs + r0 * D + 8 * v_swz<D>(r0, c) + sub));
   const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-      (lds_i16x4*)(vs + r1 * D + 8 * v_swz(r1, c) + sub));
+      (lds_i16x4*)(vs + r1 * D + 8 * v_swz<D>(r1, c) + sub));
   // whole-vector casts only: element-wise bf16 <-> i16 moves are not reliable
   const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
   const u32x4 w = {l2[0], l2[1], h2[0], h2[1]};
@@ -166,8 +177,12 @@ __global__ __launch_bounds__(256, 2) void paged_attention_kernel(const AttnArgs 
   constexpr int NDT = D / 32;   // 32-row d tiles of O^T
   constexpr int PAGE = 64 * D;  // bf16 per page tile
   constexpr int COPIES = 2 * (64 * D * 2) / 1024 / 4;   // copy instructions per wave per step
-  __shared__ __attribute__((aligned(1024))) uint16_t k_s[2][PAGE];
-  __shared__ __attribute__((aligned(1024))) uint16_t v_s[2][PAGE];
+  // Separate buffers (not one array) so that the compiler can tell the copy
+  // target of a step from the tiles that step reads.
+  __shared__ __attribute__((aligned(1024))) uint16_t k_s0[PAGE];
+  __shared__ __attribute__((aligned(1024))) uint16_t k_s1[PAGE];
+  __shared__ __attribute__((aligned(1024))) uint16_t v_s0[PAGE];
+  __shared__ __attribute__((aligned(1024))) uint16_t v_s1[PAGE];
 
   const int t = threadIdx.x;
   const int wv = t >> 6;
@@ -242,48 +257,74 @@ __global__ __launch_bounds__(256, 2) void paged_attention_kernel(const AttnArgs 
   while (n_main > 0 &&
          kPage * table_entry<DENSE>(a.kv_indices, tbase, e0 + n_main - 1) + kPage - 1 > mask_from)
     --n_main;
+  // Block and page ids of the entries, 64 at a time: lane l of blk_cur /
+  // pg_cur holds entry e0 + base + l (clamped to the last entry), the *_nxt
+  // pair the following 64; a step picks its ids with a scalar readlane.
+  int base = 0, blk_cur = 0, pg_cur = 0, blk_nxt = 0, pg_nxt = 0;
+  auto fetch = [&](int b0, int& blk, int& pg) {
+    int idx = b0 + lane;
+    idx = idx < n ? idx : n - 1;
+    idx = idx < 0 ? 0 : idx;
+    blk = (n > 0) ? table_entry<DENSE>(a.kv_indices, tbase, e0 + idx) : 0;
+    pg = (n > 0) ? ptab[blk] : 0;
+  };
+  fetch(0, blk_cur, pg_cur);
+  fetch(64, blk_nxt, pg_nxt);
+  auto advance = [&](int i) {   // make i - base < 64
+    while (i - base >= 64) {
+      base += 64;
+      blk_cur = blk_nxt;
+      pg_cur = pg_nxt;
+      fetch(base + 64, blk_nxt, pg_nxt);
+    }
+  };
+  auto id_of = [&](int cur, int nxt, int i) -> int {   // i - base in [0, 128)
+    const int d = i - base;
+    return d < 64 ? __builtin_amdgcn_readlane(cur, d) : __builtin_amdgcn_readlane(nxt, d - 64);
+  };
   auto page_ptr = [&](const uint16_t* pool, int i) -> const uint16_t* {
-    return pool + (size_t)ptab[table_entry<DENSE>(a.kv_indices, tbase, e0 + i)] * (kPage * D);
+    return pool + (size_t)id_of(pg_cur, pg_nxt, i) * (kPage * D);
   };
 
-  // Prologue: K and V of page 0 and K of page 1 in LDS, then S^T of page 0.
-  STile sa, sb;
+  // Prologue: K and V of page 0 in LDS.
   if (n > 0) {
-    page_to_lds<D, false>(page_ptr(a.k_pool, 0), k_s[0], wv, lane);
-    page_to_lds<D, true>(page_ptr(a.v_pool, 0), v_s[0], wv, lane);
-    page_to_lds<D, false>(page_ptr(a.k_pool, n > 1 ? 1 : 0), k_s[1], wv, lane);
+    page_to_lds<D, false>(page_ptr(a.k_pool, 0), k_s0, wv, lane);
+    page_to_lds<D, true>(page_ptr(a.v_pool, 0), v_s0, wv, lane);
   }
-  copies_landed(k_s, v_s);
-  __syncthreads();
-  if (n > 0) qk_page<D>(sa, k_s[0], qf, col, half);
+  copies_landed(k_s0, v_s0);
   __syncthreads();
 
-  // Pipeline step i (page e0 + i, buffer s = i & 1): copies of K(i+2) -> K[s]
-  // and V(i+1) -> V[s^1] go out first; S^T(i+1) from K[s^1] is interleaved
-  // with the softmax of page i; then O^T += V^T P^T from V[s].
-  auto step = [&](auto masked, int i, STile& cur, STile& nxt) __attribute__((always_inline)) {
-    const int s = i & 1;
-    const int i1 = i + 1 < n ? i + 1 : n - 1;   // clamped: copies stay valid, results unused
-    const int i2 = i + 2 < n ? i + 2 : n - 1;
-    page_to_lds<D, false>(page_ptr(a.k_pool, i2), k_s[s], wv, lane);
-    page_to_lds<D, true>(page_ptr(a.v_pool, i1), v_s[s ^ 1], wv, lane);
-    qk_page<D>(nxt, k_s[s ^ 1], qf, col, half);
+  // Step i (page e0 + i, buffer parity S = i & 1 as a compile-time constant so
+  // that the copy targets and the tiles read are distinct objects): the copy
+  // of page i+1 into buffers S^1 goes out first and lands while page i is
+  // processed from buffers S: S^T = K Q^T, online softmax, O^T += V^T P^T.
+  auto step = [&](auto masked, auto stage, int i) __attribute__((always_inline)) {
+    constexpr int S = decltype(stage)::value;
+    uint16_t* const k_here = S ? k_s1 : k_s0;
+    uint16_t* const k_next = S ? k_s0 : k_s1;
+    uint16_t* const v_here = S ? v_s1 : v_s0;
+    uint16_t* const v_next = S ? v_s0 : v_s1;
+    const int i1 = i + 1 < n ? i + 1 : n - 1;   // clamped: the copy stays valid, unused
+    page_to_lds<D, false>(page_ptr(a.k_pool, i1), k_next, wv, lane);
+    page_to_lds<D, true>(page_ptr(a.v_pool, i1), v_next, wv, lane);
+    STile st;
+    qk_page<D>(st, k_here, qf, col, half);
 
     // ---- online softmax of page e0 + i ----
     if constexpr (decltype(masked)::value) {
-      const int j = table_entry<DENSE>(a.kv_indices, tbase, e0 + i);
+      const int j = id_of(blk_cur, blk_nxt, i);
       // key of accumulator slot v: 64*j + 8*(v/4) + 4*half + v%4 (+32 in .hi)
       const int lim = qpos - kPage * j - 4 * half;
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int kp = 8 * (v >> 2) + (v & 3);
-        if (kp > lim) cur.lo[v] = -INFINITY;
-        if (kp + 32 > lim) cur.hi[v] = -INFINITY;
+        if (kp > lim) st.lo[v] = -INFINITY;
+        if (kp + 32 > lim) st.hi[v] = -INFINITY;
       }
     }
-    float mx = fmaxf(cur.lo[0], cur.hi[0]);
+    float mx = fmaxf(st.lo[0], st.hi[0]);
 #pragma unroll
-    for (int v = 1; v < 16; ++v) mx = fmaxf(mx, fmaxf(cur.lo[v], cur.hi[v]));
+    for (int v = 1; v < 16; ++v) mx = fmaxf(mx, fmaxf(st.lo[v], st.hi[v]));
     mx = halves_max(mx);
     const float m_new = fmaxf(m_run, mx * a.scale_log2);
     const float m_base = (m_new == -INFINITY) ? 0.f : m_new;
@@ -292,29 +333,20 @@ __global__ __launch_bounds__(256, 2) void paged_attention_kernel(const AttnArgs 
     float psum = 0.f;
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-      cur.lo[v] = fast_exp2(fmaf(cur.lo[v], a.scale_log2, -m_base));
-      cur.hi[v] = fast_exp2(fmaf(cur.hi[v], a.scale_log2, -m_base));
-      psum += cur.lo[v] + cur.hi[v];
+      st.lo[v] = fast_exp2(fmaf(st.lo[v], a.scale_log2, -m_base));
+      st.hi[v] = fast_exp2(fmaf(st.hi[v], a.scale_log2, -m_base));
+      psum += st.lo[v] + st.hi[v];
     }
     l_run = fmaf(l_run, alpha, psum);
     // P^T fragments: k-step kk covers accumulator slots 8*(kk%2)..+7
     bf16x8 pf[4];
 #pragma unroll
     for (int x = 0; x < 8; ++x) {
-      pf[0][x] = (__bf16)cur.lo[x];
-      pf[1][x] = (__bf16)cur.lo[8 + x];
-      pf[2][x] = (__bf16)cur.hi[x];
-      pf[3][x] = (__bf16)cur.hi[8 + x];
+      pf[0][x] = (__bf16)st.lo[x];
+      pf[1][x] = (__bf16)st.lo[8 + x];
+      pf[2][x] = (__bf16)st.hi[x];
+      pf[3][x] = (__bf16)st.hi[8 + x];
     }
-    __builtin_amdgcn_sched_group_barrier(0x020, COPIES, 0);  // page copies first
-    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);       // first K fragments
-#pragma unroll
-    for (int x = 0; x < 2 * NKS; ++x) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);     // 1 QK MFMA
-      __builtin_amdgcn_sched_group_barrier(0x402, 6, 0);     // 6 VALU / transcendental
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);     // next K fragment
-    }
-
     if (__ballot(alpha != 1.0f)) {
 #pragma unroll
       for (int x = 0; x < NDT; ++x)
@@ -323,32 +355,35 @@ __global__ __launch_bounds__(256, 2) void paged_attention_kernel(const AttnArgs 
     }
 
     // ---- O^T += V^T P^T ----
-    const uint16_t* vs = v_s[s];
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
 #pragma unroll
       for (int x = 0; x < NDT; ++x)
-        o[x] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vt_frag<D>(vs, lane, x, kk), pf[kk],
-                                                       o[x], 0, 0, 0);
+        o[x] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vt_frag<D>(v_here, lane, x, kk),
+                                                       pf[kk], o[x], 0, 0, 0);
     }
-    copies_landed(k_s, v_s);
+    copies_landed(k_next, v_next);
     __syncthreads();
   };
   using Plain = std::integral_constant<bool, false>;
   using Masked = std::integral_constant<bool, true>;
+  using S0 = std::integral_constant<int, 0>;
+  using S1 = std::integral_constant<int, 1>;
   int i = 0;
   for (; i + 1 < n_main; i += 2) {
-    step(Plain{}, i, sa, sb);
-    step(Plain{}, i + 1, sb, sa);
+    advance(i);
+    step(Plain{}, S0{}, i);
+    step(Plain{}, S1{}, i + 1);
   }
-  if (i < n_main) {
-    step(Plain{}, i, sa, sb);
+  if (i < n_main) {             // i is even here
+    advance(i);
+    step(Plain{}, S0{}, i);
     ++i;
-    sa = sb;
   }
   for (; i < n; ++i) {
-    step(Masked{}, i, sa, sb);
-    sa = sb;
+    advance(i);
+    if (i & 1) step(Masked{}, S1{}, i);
+    else step(Masked{}, S0{}, i);
   }
 
   // ---- epilogue ----
