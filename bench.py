@@ -39,8 +39,51 @@ def parse():
     ap.add_argument("--rho", type=float, default=None,
                     help="override the query-direction weight (0 = literal iid inputs)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-queries", type=int, default=512)
+    ap.add_argument("--cpu-sample-queries", type=int, default=1024)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain device copy of 256 MiB (to scale HBM counters)")
     return ap.parse_args()
+
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attention_llama8b_128k_final_traffic.md")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2605_16839_amd", "csrc", "attention.hip")
+
+
+def kernel_source_hash() -> str:
+    import hashlib
+    return hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per attention launch from the committed counter summary, or
+    None when that summary was taken on a different kernel source."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    vals = {}
+    for line in open(TRAFFIC_FILE):
+        if ":" in line and line.strip().startswith("- "):
+            k, v = line.strip()[2:].split(":", 1)
+            vals[k.strip()] = v.strip().strip("`")
+    if vals.get("kernel_source_sha256_16") != kernel_source_hash():
+        return None
+    try:
+        return int(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def copy_calibration():
+    """A plain copy of known size, profiled with the same counters as the
+    attention kernel: FETCH_SIZE / WRITE_SIZE of it give the KiB the
+    counters report per byte actually moved."""
+    import torch
+    n = 256 << 20
+    x = torch.ones(n // 2, dtype=torch.bfloat16, device="cuda")
+    y = torch.empty_like(x)
+    for _ in range(3):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": n}), flush=True)
 
 
 def selected_flops(w, ip: np.ndarray, ix: np.ndarray) -> float:
@@ -99,6 +142,9 @@ def cpu_baseline(w, d, tables_T, sample_queries: int):
 
 def main():
     args = parse()
+    if args.copy_calibration:
+        copy_calibration()
+        return
     if args.gpus != 1:
         print("bench.py measures one GPU: the path shards by (sequence, KV group) with no "
               "exchange, and multi-GPU runs are not part of this build; use --gpus 1.",
@@ -175,6 +221,18 @@ def main():
         stage["attention"].append(m[2].elapsed_time(m[3]))
     st_ms = {k: float(np.median(v)) for k, v in stage.items()}
 
+    # ---- the attention kernel alone, K launches (roofline timing) ----
+    ca.build_block_tables(p, bufs["masks"], gs, out=tables, ws=tws)
+    torch.cuda.synchronize()
+    a0, a1 = ev(), ev()
+    a0.record(stream)
+    for _ in range(args.steps):
+        ca.chunk_attention(p, q, (kp, vp), pt, tables, gs, w.sm_scale, num_splits=0, out=out,
+                           lse=lse, ws=aws)
+    a1.record(stream)
+    torch.cuda.synchronize()
+    attn_ms = a0.elapsed_time(a1) / args.steps
+
     # ---- dense paged baseline ----
     dargs = dict(num_splits=0, out=out_dense, ws=dws)
     for _ in range(args.warmup):
@@ -192,7 +250,7 @@ def main():
     ix = tables[1].cpu().numpy()
     f_sel = selected_flops(w, ip, ix)
     f_dense = w.dense_flops()
-    attn_tflops = f_sel / (st_ms["attention"] * 1e-3) / 1e12
+    attn_tflops = f_sel / (attn_ms * 1e-3) / 1e12
     dense_tflops = f_dense / (dense_ms * 1e-3) / 1e12
     ncached = sum(w.n_cached_blocks(b) for b in range(w.batch)) * G
     sel_cached = sum(int(np.count_nonzero(ix[ip[r]:ip[r + 1]] <
@@ -219,18 +277,19 @@ def main():
         "stage_ms": {k: round(v, 4) for k, v in st_ms.items()},
         "dense_ms": round(dense_ms, 4),
         "speedup_vs_dense": round(dense_ms / ms_per_step, 3),
-        "speedup_vs_dense_kernel_only": round(dense_ms / st_ms["attention"], 3),
+        "speedup_vs_dense_kernel_only": round(dense_ms / attn_ms, 3),
+        "attention_kernel_ms": round(attn_ms, 4),
         "executed_cached_density": round(density, 4),
         "attention_tflops_selected": round(attn_tflops, 1),
         "dense_tflops": round(dense_tflops, 1),
         "mfma_util_time_based": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
         "roofline": {"bound": "mfma", "achieved": round(attn_tflops, 1),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None},
+                     "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
+                   "traffic": measured_traffic()},
+        "kernel_source_sha256_16": kernel_source_hash(),
     }
     if not args.no_cpu_baseline:
-        import oracle
-        nkb = [w.n_kv_blocks(b) for b in range(w.batch)]
         res["cpu_baseline"] = cpu_baseline(w, d, None, args.cpu_sample_queries)
     print(json.dumps(res), flush=True)
 
