@@ -74,6 +74,39 @@ __device__ __forceinline__ int v_swz(int r, int c) {
 // which only affects softmax weights < 2^-126).
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// o[x] *= alpha for every tile when `any` is non-zero.  The branch lives
+// inside the asm so that the accumulators keep their registers on both paths
+// (a compiler-level branch makes the register allocator copy all of them
+// every step).  Only taken when the exponent base moves (lazy rescaling);
+// the leading nops cover the MFMA-to-VALU and the trailing ones the
+// VALU-to-MFMA dependency distances of the accumulators.
+template <int NDT>
+__device__ __forceinline__ void rescale_tiles(f32x16 (&o)[NDT], float alpha, uint64_t any) {
+#pragma unroll
+  for (int x = 0; x < NDT; ++x) {
+    __asm__ volatile(
+        "s_cmp_eq_u64 %16, 0\n"
+        "s_cbranch_scc1 1f\n"
+        "s_nop 7\n s_nop 7\n s_nop 7\n"
+        "v_mul_f32 %0, %17, %0\n v_mul_f32 %1, %17, %1\n"
+        "v_mul_f32 %2, %17, %2\n v_mul_f32 %3, %17, %3\n"
+        "v_mul_f32 %4, %17, %4\n v_mul_f32 %5, %17, %5\n"
+        "v_mul_f32 %6, %17, %6\n v_mul_f32 %7, %17, %7\n"
+        "v_mul_f32 %8, %17, %8\n v_mul_f32 %9, %17, %9\n"
+        "v_mul_f32 %10, %17, %10\n v_mul_f32 %11, %17, %11\n"
+        "v_mul_f32 %12, %17, %12\n v_mul_f32 %13, %17, %13\n"
+        "v_mul_f32 %14, %17, %14\n v_mul_f32 %15, %17, %15\n"
+        "s_nop 7\n"
+        "1:"
+        : "+v"(o[x][0]), "+v"(o[x][1]), "+v"(o[x][2]), "+v"(o[x][3]), "+v"(o[x][4]),
+          "+v"(o[x][5]), "+v"(o[x][6]), "+v"(o[x][7]), "+v"(o[x][8]), "+v"(o[x][9]),
+          "+v"(o[x][10]), "+v"(o[x][11]), "+v"(o[x][12]), "+v"(o[x][13]), "+v"(o[x][14]),
+          "+v"(o[x][15])
+        : "s"(any), "v"(alpha)
+        : "scc");
+  }
+}
+
 template <bool DENSE>
 __device__ __forceinline__ int table_entry(const int32_t* __restrict__ idx, int base, int e) {
   return DENSE ? e : idx[base + e];
@@ -110,6 +143,18 @@ __device__ __forceinline__ void copies_landed(void* p0, void* p1) {
   __builtin_amdgcn_s_waitcnt(0);
   __asm__ volatile("" : : "v"(p0), "v"(p1) : "memory");
 }
+
+// NaN-propagating maximum (v_maximum3_f32 on gfx950).  fmaxf would quiet
+// each MFMA result with an extra v_max first (IEEE mode); the scores are
+// never NaN, so the two agree.
+__device__ __forceinline__ float max3(float a, float b, float c) {
+  return __builtin_elementwise_maximum(__builtin_elementwise_maximum(a, b), c);
+}
+
+// Lazy rescaling threshold (log2 units): the running max used as the
+// exponent base is only moved when a new score exceeds it by more than this,
+// so the weights stay <= 2^kRescaleSlack and most pages skip the O rescale.
+constexpr float kRescaleSlack = 8.0f;
 
 // max / sum of a value and its partner in the other half of the wave
 // (lanes l and l^32 hold the same query column).
@@ -322,22 +367,29 @@ __global__ __launch_bounds__(256, 2) void paged_attention_kernel(const AttnArgs 
         if (kp + 32 > lim) st.hi[v] = -INFINITY;
       }
     }
-    float mx = fmaxf(st.lo[0], st.hi[0]);
+    float mx = max3(st.lo[0], st.hi[0], st.lo[1]);
+    mx = max3(mx, st.hi[1], st.lo[2]);
 #pragma unroll
-    for (int v = 1; v < 16; ++v) mx = fmaxf(mx, fmaxf(st.lo[v], st.hi[v]));
-    mx = halves_max(mx);
-    const float m_new = fmaxf(m_run, mx * a.scale_log2);
-    const float m_base = (m_new == -INFINITY) ? 0.f : m_new;
-    const float alpha = fast_exp2(m_run - m_base);
-    m_run = m_new;
-    float psum = 0.f;
+    for (int v = 2; v < 15; ++v) mx = max3(mx, st.hi[v], st.lo[v + 1]);
+    mx = max3(mx, st.hi[15], st.hi[15]);
+    mx = halves_max(mx) * a.scale_log2;
+    // move the base only when the page's max exceeds it by the slack
+    // (-inf > -inf + slack is false: a fully masked row keeps its base)
+    const bool rebase = mx > m_run + kRescaleSlack;
+    const float alpha = rebase ? fast_exp2(m_run - mx) : 1.0f;
+    m_run = rebase ? mx : m_run;
+    l_run *= alpha;
+    rescale_tiles<NDT>(o, alpha, __ballot(rebase));
+    const float m_base = (m_run == -INFINITY) ? 0.f : m_run;
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
       st.lo[v] = fast_exp2(fmaf(st.lo[v], a.scale_log2, -m_base));
       st.hi[v] = fast_exp2(fmaf(st.hi[v], a.scale_log2, -m_base));
-      psum += st.lo[v] + st.hi[v];
     }
-    l_run = fmaf(l_run, alpha, psum);
+    float ps0 = st.lo[0], ps1 = st.hi[0];
+#pragma unroll
+    for (int v = 1; v < 16; ++v) { ps0 += st.lo[v]; ps1 += st.hi[v]; }
+    l_run += ps0 + ps1;
     // P^T fragments: k-step kk covers accumulator slots 8*(kk%2)..+7
     bf16x8 pf[4];
 #pragma unroll
@@ -346,12 +398,6 @@ __global__ __launch_bounds__(256, 2) void paged_attention_kernel(const AttnArgs 
       pf[1][x] = (__bf16)st.lo[8 + x];
       pf[2][x] = (__bf16)st.hi[x];
       pf[3][x] = (__bf16)st.hi[8 + x];
-    }
-    if (__ballot(alpha != 1.0f)) {
-#pragma unroll
-      for (int x = 0; x < NDT; ++x)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) o[x][v] *= alpha;
     }
 
     // ---- O^T += V^T P^T ----
