@@ -39,6 +39,8 @@ def parse():
     ap.add_argument("--rho", type=float, default=None,
                     help="override the query-direction weight (0 = literal iid inputs)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-arms", action="store_true",
+                    help="skip the copy and block-sparse execution arms")
     ap.add_argument("--cpu-sample-queries", type=int, default=1024)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of 256 MiB (to scale HBM counters)")
@@ -140,6 +142,93 @@ def cpu_baseline(w, d, tables_T, sample_queries: int):
     }
 
 
+def block_sparse_flops(w, bits: np.ndarray) -> float:
+    """4*D per unmasked (query, key) pair of every (head, Q-block) mask row."""
+    qb, pg = w.q_block, w.page_size
+    total = 0
+    for b in range(w.batch):
+        nc = w.n_cached_blocks(b)
+        c_sel = bits[b, :, :, :nc].sum(axis=2)              # [Hq, nQB] selected cached blocks
+        total += int(c_sel.sum()) * qb * pg
+        for i in range(w.n_qblocks):                        # chunk keys 0..t for t in Q-block i
+            t0 = i * qb
+            total += w.num_q_heads * (qb * t0 + qb * (qb + 1) // 2)
+    return 4.0 * w.head_dim * total
+
+
+def strategy_arms(ca, p, w, q, kp, vp, pt, masks, tables, ip, args, stream, ev):
+    """Copy and block-sparse arms at the same masks (Sec. 4.4 execution ablation).
+
+    copy: gather the selected pages of every group table into contiguous pools,
+    then the same attention kernel on them; block-sparse: one table per
+    (head, Q-block) mask row, no union.  Each is timed over K back-to-back
+    launches of its kernels, like the zero-copy attention."""
+    import torch
+
+    def timed(fn):
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        a0, a1 = ev(), ev()
+        a0.record(stream)
+        for _ in range(args.steps):
+            fn()
+        a1.record(stream)
+        torch.cuda.synchronize()
+        return a0.elapsed_time(a1) / args.steps
+
+    gs = w.group_size
+    nnz = int(ip[-1])
+    page_bytes = w.page_size * w.head_dim * 2
+    packed = ca.gather_selected_pages(p, (kp, vp), pt, tables, gs, capacity_pages=nnz)
+    out = torch.empty_like(q)
+    aws_n = ca.attention_workspace_bytes(p, gs, 0)
+    aws = torch.empty(aws_n, dtype=torch.uint8, device=q.device) if aws_n else None
+    g_ms = timed(lambda: ca.gather_selected_pages(p, (kp, vp), pt, tables, gs,
+                                                  capacity_pages=nnz, out=packed))
+    pa_ms = timed(lambda: ca.packed_chunk_attention(p, q, packed, tables, gs, w.sm_scale,
+                                                    num_splits=0, out=out, ws=aws))
+    copy_total = timed(lambda: (ca.gather_selected_pages(p, (kp, vp), pt, tables, gs,
+                                                         capacity_pages=nnz, out=packed),
+                                ca.packed_chunk_attention(p, q, packed, tables, gs, w.sm_scale,
+                                                          num_splits=0, out=out, ws=aws)))
+    zc_ms = timed(lambda: ca.chunk_attention(p, q, (kp, vp), pt, tables, gs, w.sm_scale,
+                                             num_splits=0, out=out, ws=aws))
+    del packed
+    res = {"zero_copy_attention_ms": round(zc_ms, 4),
+           "copy": {"gather_ms": round(g_ms, 4), "attention_ms": round(pa_ms, 4),
+                    "total_ms": round(copy_total, 4), "pages_copied": nnz,
+                    "gather_GBps": round(4 * nnz * page_bytes / (g_ms * 1e-3) / 1e9, 1)}}
+    if w.q_block == 128:          # the block-sparse arm runs one head x one 128-query Q-block
+        R = w.batch * w.num_q_heads * w.n_qblocks
+        bt = (torch.empty(R + 1, dtype=torch.int32, device=q.device),
+              torch.empty(R * w.max_kv_blocks, dtype=torch.int32, device=q.device))
+        bsw_n = ca.attention_workspace_bytes(p, 1, 0)
+        bsw = torch.empty(bsw_n, dtype=torch.uint8, device=q.device) if bsw_n else None
+        words = masks.cpu().numpy().view(np.uint8)
+        bits = np.unpackbits(words, axis=-1, bitorder="little").astype(bool)
+        # matched tables: every (head, Q-block) tile runs its group's union (what zero-copy
+        # executes); raw masks: every tile runs its own mask row (the selector's sparsity)
+        for key, group in (("block_sparse", gs), ("block_sparse_raw_mask", 0)):
+            bws = torch.empty(max(ca.block_sparse_tables_workspace_bytes(p, group), 1),
+                              dtype=torch.uint8, device=q.device)
+            t_ms = timed(lambda: ca.build_block_sparse_tables(p, masks, group, out=bt, ws=bws))
+            b_ms = timed(lambda: ca.block_sparse_chunk_attention(p, q, (kp, vp), pt, bt,
+                                                                 w.sm_scale, num_splits=0,
+                                                                 out=out, ws=bsw))
+            entry = {"tables_ms": round(t_ms, 4), "attention_ms": round(b_ms, 4),
+                     "total_ms": round(t_ms + b_ms, 4), "pages_read": int(bt[0][-1].item())}
+            if group == 0:
+                entry["tflops_unmasked"] = round(block_sparse_flops(w, bits) / (b_ms * 1e-3) / 1e12, 1)
+            res[key] = entry
+    # zero-copy again after the arms: the two readings bracket them (clock drift)
+    zc2 = timed(lambda: ca.chunk_attention(p, q, (kp, vp), pt, tables, gs, w.sm_scale,
+                                           num_splits=0, out=out, ws=aws))
+    res["zero_copy_attention_ms"] = round(0.5 * (zc_ms + zc2), 4)
+    res["zero_copy_attention_ms_before_after"] = [round(zc_ms, 4), round(zc2, 4)]
+    return res
+
+
 def main():
     args = parse()
     if args.copy_calibration:
@@ -223,6 +312,9 @@ def main():
 
     # ---- the attention kernel alone, K launches (roofline timing) ----
     ca.build_block_tables(p, bufs["masks"], gs, out=tables, ws=tws)
+    for _ in range(args.warmup):
+        ca.chunk_attention(p, q, (kp, vp), pt, tables, gs, w.sm_scale, num_splits=0, out=out,
+                           lse=lse, ws=aws)
     torch.cuda.synchronize()
     a0, a1 = ev(), ev()
     a0.record(stream)
@@ -289,6 +381,9 @@ def main():
                    "traffic": measured_traffic()},
         "kernel_source_sha256_16": kernel_source_hash(),
     }
+    if not args.no_arms:
+        res["arms"] = strategy_arms(ca, p, w, q, kp, vp, pt, bufs["masks"], tables, ip,
+                                    args, stream, ev)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(w, d, None, args.cpu_sample_queries)
     print(json.dumps(res), flush=True)

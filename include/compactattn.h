@@ -61,7 +61,7 @@
 extern "C" {
 #endif
 
-#define CA_ABI_VERSION 1
+#define CA_ABI_VERSION 2
 
 typedef enum ca_status {
   CA_OK = 0,
@@ -189,6 +189,73 @@ ca_status ca_dense_paged_chunk_attention(const ca_problem* p, const uint16_t* q,
                                          const int32_t* page_table, float sm_scale,
                                          int32_t num_splits, uint16_t* out, float* lse,
                                          void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * 4. Execution-strategy arms at matched masks (Sec. 4.4, Fig. 7c; App. C
+ *    Table 9).  They compute what the paper compares the zero-copy path
+ *    against, with the same attention kernel, so that only the strategy
+ *    differs.
+ *
+ * 4a. Block-sparse: every (sequence b, query head h, Q-block i) is its own
+ *    tile with its own block list (no packing of the heads of a group; each
+ *    tile reads its pages separately).
+ *    ca_build_block_sparse_tables: CSR over rows (b*Hq + h)*nQB + i,
+ *    kv_indptr int32 [B*Hq*nQB + 1], kv_indices capacity
+ *    B*Hq*nQB*max_kv_blocks, entries ascending.  group_size = 0: row
+ *    (b,h,i) = the set bits j < nKB_b of its own mask row M[b,h,i,:]
+ *    (the raw mask executed directly); group_size > 0: row (b,h,i) = the
+ *    union table T[b, h/group_size] of section 2, limited to the blocks
+ *    Q-block i can see (j < nC_b + (i+1)*q_block/page_size), which is the
+ *    same unioned mask the zero-copy path executes (the matched-table
+ *    ablation of Sec. 4.4).
+ *    Workspace: ca_block_sparse_tables_workspace_bytes(p, group_size).
+ *    ca_block_sparse_chunk_attention: for query t of Q-block i of head h,
+ *    out = softmax over the keys of the blocks of row (b,h,i) with position
+ *    <= cached_len[b] + t (as in section 3).  A query tile is one head x 128
+ *    queries, so q_block must be 128 (else CA_ERR_UNSUPPORTED).  num_splits
+ *    and workspace as in section 3 with group_size = 1
+ *    (ca_attention_workspace_bytes(p, 1, num_splits)).
+ * ---------------------------------------------------------------------- */
+size_t ca_block_sparse_tables_workspace_bytes(const ca_problem* p, int32_t group_size);
+
+ca_status ca_build_block_sparse_tables(const ca_problem* p, const uint64_t* masks,
+                                       int32_t group_size, int32_t* kv_indptr,
+                                       int32_t* kv_indices, void* ws, size_t ws_bytes,
+                                       void* stream);
+
+ca_status ca_block_sparse_chunk_attention(const ca_problem* p, const uint16_t* q,
+                                          const uint16_t* k_pool, const uint16_t* v_pool,
+                                          const int32_t* page_table,
+                                          const int32_t* kv_indptr,
+                                          const int32_t* kv_indices, float sm_scale,
+                                          int32_t num_splits, uint16_t* out, float* lse,
+                                          void* ws, size_t ws_bytes, void* stream);
+
+/* 4b. Copy: the selected pages of every group table are first gathered into
+ *    contiguous pools, then attention runs on them.
+ *    ca_gather_selected_pages: packed page p (0 <= p < kv_indptr[B*G]) gets
+ *    K_pool / V_pool page page_table[b, kvh, kv_indices[p]] of the row that
+ *    owns entry p; k_packed and v_packed are bf16 [capacity_pages, page, D]
+ *    and capacity_pages must be >= kv_indptr[B*G] (B*G*max_kv_blocks always
+ *    is; entries beyond the capacity are not copied).  Invalid entries
+ *    (kv_indices outside [0, max_kv_blocks)) are skipped.
+ *    ca_packed_chunk_attention: the section 3 result for the same tables,
+ *    reading table entry p from packed page p (no page_table); the same
+ *    kernel, so the output is bit-identical to ca_chunk_attention.
+ * ---------------------------------------------------------------------- */
+ca_status ca_gather_selected_pages(const ca_problem* p, const uint16_t* k_pool,
+                                   const uint16_t* v_pool, const int32_t* page_table,
+                                   const int32_t* kv_indptr, const int32_t* kv_indices,
+                                   int32_t group_size, uint16_t* k_packed,
+                                   uint16_t* v_packed, int64_t capacity_pages,
+                                   void* stream);
+
+ca_status ca_packed_chunk_attention(const ca_problem* p, const uint16_t* q,
+                                    const uint16_t* k_packed, const uint16_t* v_packed,
+                                    const int32_t* kv_indptr, const int32_t* kv_indices,
+                                    int32_t group_size, float sm_scale, int32_t num_splits,
+                                    int64_t capacity_pages, uint16_t* out, float* lse,
+                                    void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
  * Debug helper: synchronises `stream`, copies the tables to the host and

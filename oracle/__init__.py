@@ -16,7 +16,9 @@ It is a plain, slow, float64 restatement of what the paper defines:
 * ``attention``  -- attention of every chunk query over exactly the blocks of
   its group's table, after an explicit gather of those pages (the copy the
   zero-copy design avoids, Sec. 3.3), with causal masking in absolute
-  positions (App. B.2, last paragraph).
+  positions (App. B.2, last paragraph); ``block_sparse_attention`` runs the
+  same softmax per (head, Q-block) mask row without any union, the block-
+  sparse execution the paper compares against (Sec. 4.4).
 
 Parity status of each function is stated in its docstring; every function is
 pinned by ``tests/test_oracle.py`` against properties that the paper or the
@@ -29,5 +31,5 @@ from .estimator import (  # noqa: F401
 )
 from .tables import unpack_masks, block_tables, tables_to_csr, union_densities  # noqa: F401
 from .attention import (  # noqa: F401
-    gather_selected, attention_rows, chunk_attention, dense_tables,
+    gather_selected, attention_rows, chunk_attention, dense_tables, block_sparse_attention,
 )

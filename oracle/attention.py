@@ -118,3 +118,41 @@ def chunk_attention(q_bits: np.ndarray, k_pool_bits: np.ndarray,
             out[b, t_idx, h, :] = o
             lse[b, h, t_idx] = l
     return out, lse
+
+
+def block_sparse_attention(q_bits: np.ndarray, k_pool_bits: np.ndarray,
+                           v_pool_bits: np.ndarray, page_table: np.ndarray,
+                           cached_len: Sequence[int], mask_bits: np.ndarray, q_block: int,
+                           sm_scale: float,
+                           heads: Optional[Iterable[Tuple[int, int]]] = None,
+                           queries: Optional[Sequence[int]] = None):
+    """Block-sparse execution of the 2D mask (the ablation arm of Sec. 4.4).
+
+    Query t of Q-block i = t // q_block of head h attends to the blocks of its
+    own mask row, T = {j < nKB_b : M[b, h, i, j]} (no union over Q-blocks or
+    heads), through the same gather and softmax as ``chunk_attention``.
+    ``mask_bits`` is the unpacked mask, bool [B, Hq, nQB, >= nKB_b].  Returns
+    (out [B, C, Hq, D], lse [B, Hq, C]); rows not computed are NaN.
+    """
+    B, C, Hq, D = q_bits.shape
+    Hkv = page_table.shape[1]
+    ratio = Hq // Hkv
+    chunk_blocks = C // k_pool_bits.shape[1]
+    if heads is None:
+        heads = [(b, h) for b in range(B) for h in range(Hq)]
+    t_all = np.arange(C) if queries is None else np.asarray(queries)
+    out = np.full((B, C, Hq, D), np.nan)
+    lse = np.full((B, Hq, C), np.nan)
+    for (b, h) in heads:
+        nkb = int(cached_len[b]) // k_pool_bits.shape[1] + chunk_blocks
+        kvh = h // ratio
+        for i in sorted(set((t_all // q_block).tolist())):
+            t_idx = t_all[t_all // q_block == i]
+            table = [j for j in range(nkb) if mask_bits[b, h, i, j]]
+            ksel, vsel, kpos = gather_selected(k_pool_bits, v_pool_bits, page_table,
+                                               b, kvh, table)
+            q = bf16_to_f64(q_bits[b, t_idx, h, :])
+            o, l = attention_rows(q, int(cached_len[b]) + t_idx, ksel, vsel, kpos, sm_scale)
+            out[b, t_idx, h, :] = o
+            lse[b, h, t_idx] = l
+    return out, lse

@@ -7,5 +7,7 @@ from .binding import (  # noqa: F401
     CAError, Problem, load, abi_version, check_problem, pool_q_blocks, pool_k_blocks,
     block_scores, select_blocks, estimate_masks, tables_workspace_bytes,
     build_block_tables, attention_workspace_bytes, chunk_attention,
-    dense_paged_chunk_attention, validate_tables, EXPORTED, LIB_PATH,
+    dense_paged_chunk_attention, validate_tables, block_sparse_tables_workspace_bytes,
+    build_block_sparse_tables, block_sparse_chunk_attention, gather_selected_pages,
+    packed_chunk_attention, EXPORTED, LIB_PATH,
 )

@@ -25,6 +25,8 @@ EXPORTED = (
     "ca_estimate_masks", "ca_tables_workspace_bytes", "ca_build_block_tables",
     "ca_attention_workspace_bytes", "ca_chunk_attention",
     "ca_dense_paged_chunk_attention", "ca_validate_tables",
+    "ca_block_sparse_tables_workspace_bytes", "ca_build_block_sparse_tables",
+    "ca_block_sparse_chunk_attention", "ca_gather_selected_pages", "ca_packed_chunk_attention",
 )
 
 
@@ -66,6 +68,7 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib = ctypes.CDLL(p)
     P = ctypes.POINTER(CAProblem)
     vp, i32, f32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_float, ctypes.c_size_t
+    i64 = ctypes.c_int64
     sig = {
         "ca_abi_version": ([], ctypes.c_int),
         "ca_status_string": ([ctypes.c_int], ctypes.c_char_p),
@@ -84,6 +87,14 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
         "ca_dense_paged_chunk_attention": ([P, vp, vp, vp, vp, f32, i32, vp, vp, vp, sz, vp],
                                            ctypes.c_int),
         "ca_validate_tables": ([P, i32, vp, vp, i32, vp], ctypes.c_int),
+        "ca_block_sparse_tables_workspace_bytes": ([P, i32], sz),
+        "ca_build_block_sparse_tables": ([P, vp, i32, vp, vp, vp, sz, vp], ctypes.c_int),
+        "ca_block_sparse_chunk_attention": ([P, vp, vp, vp, vp, vp, vp, f32, i32, vp, vp, vp,
+                                             sz, vp], ctypes.c_int),
+        "ca_gather_selected_pages": ([P, vp, vp, vp, vp, vp, i32, vp, vp, i64, vp],
+                                     ctypes.c_int),
+        "ca_packed_chunk_attention": ([P, vp, vp, vp, vp, vp, i32, f32, i32, i64, vp, vp, vp,
+                                       sz, vp], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -308,6 +319,87 @@ def dense_paged_chunk_attention(p: Problem, q_chunk: torch.Tensor,
                                                  _ptr(v_pool), _ptr(page_table), sm_scale,
                                                  num_splits, _ptr(out), _ptr(lse), _ptr(ws),
                                                  _nbytes(ws), _stream(stream)))
+    return out, lse
+
+
+def block_sparse_tables_workspace_bytes(p: Problem, group_size: int = 0) -> int:
+    return load().ca_block_sparse_tables_workspace_bytes(p.ref, group_size)
+
+
+def build_block_sparse_tables(p: Problem, masks: torch.Tensor, group_size: int = 0,
+                              out: Optional[Tuple[torch.Tensor, torch.Tensor]] = None,
+                              ws: Optional[torch.Tensor] = None, stream=None):
+    """One table per (b, h, Q-block) row: its own mask row (group_size = 0) or the
+    causally limited union of its execution group (group_size > 0)."""
+    dev = masks.device
+    R = p.batch * p.num_q_heads * p.n_qblocks
+    if out is None:
+        out = (torch.empty(R + 1, dtype=torch.int32, device=dev),
+               torch.empty(R * p.max_kv_blocks, dtype=torch.int32, device=dev))
+    nbytes = block_sparse_tables_workspace_bytes(p, group_size)
+    if ws is None:
+        ws = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+    _check(load().ca_build_block_sparse_tables(p.ref, _ptr(masks), group_size, _ptr(out[0]),
+                                               _ptr(out[1]), _ptr(ws), _nbytes(ws),
+                                               _stream(stream)))
+    return out
+
+
+def block_sparse_chunk_attention(p: Problem, q_chunk: torch.Tensor,
+                                 kv_pool: Tuple[torch.Tensor, torch.Tensor],
+                                 page_table: torch.Tensor, tables: Tuple[torch.Tensor, torch.Tensor],
+                                 sm_scale: float, num_splits: int = 0,
+                                 out: Optional[torch.Tensor] = None,
+                                 lse: Optional[torch.Tensor] = None,
+                                 ws: Optional[torch.Tensor] = None, stream=None):
+    """Attention of every (head, Q-block) over its own mask row's blocks."""
+    k_pool, v_pool = kv_pool
+    if out is None:
+        out = torch.empty_like(q_chunk)
+    ws = _attn_ws(p, 1, num_splits, ws, q_chunk.device)
+    _check(load().ca_block_sparse_chunk_attention(p.ref, _ptr(q_chunk), _ptr(k_pool),
+                                                  _ptr(v_pool), _ptr(page_table),
+                                                  _ptr(tables[0]), _ptr(tables[1]), sm_scale,
+                                                  num_splits, _ptr(out), _ptr(lse), _ptr(ws),
+                                                  _nbytes(ws), _stream(stream)))
+    return out, lse
+
+
+def gather_selected_pages(p: Problem, kv_pool: Tuple[torch.Tensor, torch.Tensor],
+                          page_table: torch.Tensor, tables: Tuple[torch.Tensor, torch.Tensor],
+                          group_size: int, capacity_pages: Optional[int] = None,
+                          out: Optional[Tuple[torch.Tensor, torch.Tensor]] = None, stream=None):
+    """Copy arm: pack every group's selected K/V pages contiguously in table order."""
+    k_pool, v_pool = kv_pool
+    if capacity_pages is None:
+        capacity_pages = p.batch * p.n_groups(group_size) * p.max_kv_blocks
+    if out is None:
+        shape = (capacity_pages,) + tuple(k_pool.shape[1:])
+        out = (torch.empty(shape, dtype=k_pool.dtype, device=k_pool.device),
+               torch.empty(shape, dtype=v_pool.dtype, device=v_pool.device))
+    _check(load().ca_gather_selected_pages(p.ref, _ptr(k_pool), _ptr(v_pool), _ptr(page_table),
+                                           _ptr(tables[0]), _ptr(tables[1]), group_size,
+                                           _ptr(out[0]), _ptr(out[1]), capacity_pages,
+                                           _stream(stream)))
+    return out
+
+
+def packed_chunk_attention(p: Problem, q_chunk: torch.Tensor,
+                           packed: Tuple[torch.Tensor, torch.Tensor],
+                           tables: Tuple[torch.Tensor, torch.Tensor], group_size: int,
+                           sm_scale: float, num_splits: int = 0,
+                           out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
+                           ws: Optional[torch.Tensor] = None, stream=None):
+    """Copy arm: attention over the packed pools (table entry p = packed page p)."""
+    k_packed, v_packed = packed
+    if out is None:
+        out = torch.empty_like(q_chunk)
+    ws = _attn_ws(p, group_size, num_splits, ws, q_chunk.device)
+    _check(load().ca_packed_chunk_attention(p.ref, _ptr(q_chunk), _ptr(k_packed),
+                                            _ptr(v_packed), _ptr(tables[0]), _ptr(tables[1]),
+                                            group_size, sm_scale, num_splits,
+                                            k_packed.shape[0], _ptr(out), _ptr(lse), _ptr(ws),
+                                            _nbytes(ws), _stream(stream)))
     return out, lse
 
 

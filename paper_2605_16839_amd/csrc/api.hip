@@ -126,13 +126,20 @@ ca_status run_attention(const ca_problem* p, const uint16_t* q, const uint16_t* 
                         const uint16_t* v_pool, const int32_t* page_table,
                         const int32_t* kv_indptr, const int32_t* kv_indices, int32_t group_size,
                         float sm_scale, int32_t num_splits, uint16_t* out, float* lse, void* ws,
-                        size_t ws_bytes, void* stream, bool dense) {
+                        size_t ws_bytes, void* stream, bool dense,
+                        int table_mode = ca::kTablesPerGroup, long long packed_pages = 0) {
   ca::Dims d;
   ca_status s = check(p, group_size, &d);
   if (s != CA_OK) return s;
   if ((s = need_device(p)) != CA_OK) return s;
-  if (!q || !k_pool || !v_pool || !page_table || !out)
+  if (!q || !k_pool || !v_pool || !out || (!page_table && table_mode != ca::kTablesPacked))
     return fail(CA_ERR_NULL, "q, k_pool, v_pool, page_table and out are required");
+  if (table_mode == ca::kTablesPerQTile && ca::attn_query_tile(group_size) != d.q_block)
+    return fail(CA_ERR_UNSUPPORTED,
+                "block-sparse attention runs one head x one Q-block per tile: q_block must be "
+                "%d, got %d", ca::attn_query_tile(group_size), d.q_block);
+  if (table_mode == ca::kTablesPacked && packed_pages < 1)
+    return fail(CA_ERR_SHAPE, "capacity_pages must be >= 1");
   if (!dense && (!kv_indptr || !kv_indices))
     return fail(CA_ERR_NULL, "kv_indptr and kv_indices are required");
   if ((s = attention_tile_ok(d, group_size)) != CA_OK) return s;
@@ -161,6 +168,8 @@ ca_status run_attention(const ca_problem* p, const uint16_t* q, const uint16_t* 
   L.splits = splits;
   L.ws = ws;
   L.dense = dense;
+  L.table_mode = table_mode;
+  L.packed_pages = packed_pages;
   return hip_status(ca::launch_attention(d, L, static_cast<hipStream_t>(stream)),
                     dense ? "dense paged attention launch" : "chunk attention launch");
 }
@@ -322,6 +331,86 @@ ca_status ca_dense_paged_chunk_attention(const ca_problem* p, const uint16_t* q,
   while (gs > 1 && 128 % gs != 0) --gs;
   return run_attention(p, q, k_pool, v_pool, page_table, nullptr, nullptr, gs, sm_scale,
                        num_splits, out, lse, ws, ws_bytes, stream, true);
+}
+
+size_t ca_block_sparse_tables_workspace_bytes(const ca_problem* p, int32_t group_size) {
+  ca::Dims d;
+  if (group_size < 0 || check(p, group_size, &d) != CA_OK) return 0;
+  if (group_size > 0) return ca::union_rows_ws_bytes(d, group_size);
+  ca::Dims r = d;   // one table row per (b, h, Q-block): heads x Q-blocks, one Q-block each
+  r.Hq = d.Hq * d.nqb;
+  r.nqb = 1;
+  return ca::tables_ws_bytes(r, 1);
+}
+
+ca_status ca_build_block_sparse_tables(const ca_problem* p, const uint64_t* masks,
+                                       int32_t group_size, int32_t* kv_indptr,
+                                       int32_t* kv_indices, void* ws, size_t ws_bytes,
+                                       void* stream) {
+  ca::Dims d;
+  if (group_size < 0) return fail(CA_ERR_GROUP, "group_size must be >= 0");
+  ca_status s = check(p, group_size, &d);
+  if (s != CA_OK) return s;
+  if ((s = need_device(p)) != CA_OK) return s;
+  if (!masks || !kv_indptr || !kv_indices)
+    return fail(CA_ERR_NULL, "masks, kv_indptr and kv_indices are required");
+  const size_t need = ca_block_sparse_tables_workspace_bytes(p, group_size);
+  if (ws == nullptr || ws_bytes < need)
+    return fail(CA_ERR_WORKSPACE, "block-sparse tables need %zu workspace bytes, got %zu", need,
+                ws == nullptr ? (size_t)0 : ws_bytes);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (group_size > 0)
+    return hip_status(ca::launch_union_rows(d, masks, p->cached_len, group_size, kv_indptr,
+                                            kv_indices, ws, st),
+                      "block-sparse union rows launch");
+  ca::Dims r = d;
+  r.Hq = d.Hq * d.nqb;
+  r.nqb = 1;
+  return hip_status(ca::launch_tables(r, masks, p->cached_len, 1, kv_indptr, kv_indices, ws, st),
+                    "block-sparse tables launch");
+}
+
+ca_status ca_block_sparse_chunk_attention(const ca_problem* p, const uint16_t* q,
+                                          const uint16_t* k_pool, const uint16_t* v_pool,
+                                          const int32_t* page_table, const int32_t* kv_indptr,
+                                          const int32_t* kv_indices, float sm_scale,
+                                          int32_t num_splits, uint16_t* out, float* lse,
+                                          void* ws, size_t ws_bytes, void* stream) {
+  return run_attention(p, q, k_pool, v_pool, page_table, kv_indptr, kv_indices, 1, sm_scale,
+                       num_splits, out, lse, ws, ws_bytes, stream, false, ca::kTablesPerQTile);
+}
+
+ca_status ca_gather_selected_pages(const ca_problem* p, const uint16_t* k_pool,
+                                   const uint16_t* v_pool, const int32_t* page_table,
+                                   const int32_t* kv_indptr, const int32_t* kv_indices,
+                                   int32_t group_size, uint16_t* k_packed, uint16_t* v_packed,
+                                   int64_t capacity_pages, void* stream) {
+  ca::Dims d;
+  if (group_size < 1) return fail(CA_ERR_GROUP, "group_size must be >= 1");
+  ca_status s = check(p, group_size, &d);
+  if (s != CA_OK) return s;
+  if (!k_pool || !v_pool || !page_table || !kv_indptr || !kv_indices || !k_packed || !v_packed)
+    return fail(CA_ERR_NULL, "pools, page_table, tables and packed pools are required");
+  const long long cap_max = (long long)d.B * (d.Hq / group_size) * d.max_kv_blocks;
+  if (capacity_pages < 1 || capacity_pages > cap_max)
+    return fail(CA_ERR_SHAPE, "capacity_pages %lld out of range [1, %lld]",
+                (long long)capacity_pages, cap_max);
+  return hip_status(ca::launch_gather(d, k_pool, v_pool, page_table, kv_indptr, kv_indices,
+                                      group_size, capacity_pages, k_packed, v_packed,
+                                      static_cast<hipStream_t>(stream)),
+                    "gather launch");
+}
+
+ca_status ca_packed_chunk_attention(const ca_problem* p, const uint16_t* q,
+                                    const uint16_t* k_packed, const uint16_t* v_packed,
+                                    const int32_t* kv_indptr, const int32_t* kv_indices,
+                                    int32_t group_size, float sm_scale, int32_t num_splits,
+                                    int64_t capacity_pages, uint16_t* out, float* lse, void* ws,
+                                    size_t ws_bytes, void* stream) {
+  if (group_size < 1) return fail(CA_ERR_GROUP, "group_size must be >= 1");
+  return run_attention(p, q, k_packed, v_packed, nullptr, kv_indptr, kv_indices, group_size,
+                       sm_scale, num_splits, out, lse, ws, ws_bytes, stream, false,
+                       ca::kTablesPacked, capacity_pages);
 }
 
 ca_status ca_validate_tables(const ca_problem* p, int32_t group_size, const int32_t* kv_indptr,

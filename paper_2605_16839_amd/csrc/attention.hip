@@ -49,6 +49,8 @@ struct AttnArgs {
   float* part_o;     // [splits, B*Hq*C, D] when splits > 1
   float* part_lse;   // [splits, B*Hq*C]
   int B, Hq, Hkv, C, max_kv_blocks, group_size, G, n_qtiles, splits;
+  int table_mode;          // kTablesPerGroup / kTablesPerQTile / kTablesPacked
+  long long packed_pages;  // capacity of the packed pools (kTablesPacked)
   float scale_log2;
 };
 
@@ -264,8 +266,10 @@ __global__ __launch_bounds__(256, 2) void paged_attention_kernel(const AttnArgs 
   if (DENSE) {
     len = nkb;
   } else {
-    tbase = a.kv_indptr[rowid];
-    len = a.kv_indptr[rowid + 1] - tbase;
+    // per-group rows, or one row per (head, query tile) for the block-sparse arm
+    const int trow = a.table_mode == kTablesPerQTile ? rowid * a.n_qtiles + qt : rowid;
+    tbase = a.kv_indptr[trow];
+    len = a.kv_indptr[trow + 1] - tbase;
   }
   const int e0 = (int)(((long long)len * sp) / a.splits);
   const int e1 = (int)(((long long)len * (sp + 1)) / a.splits);
@@ -311,7 +315,13 @@ __global__ __launch_bounds__(256, 2) void paged_attention_kernel(const AttnArgs 
     idx = idx < n ? idx : n - 1;
     idx = idx < 0 ? 0 : idx;
     blk = (n > 0) ? table_entry<DENSE>(a.kv_indices, tbase, e0 + idx) : 0;
-    pg = (n > 0) ? ptab[blk] : 0;
+    if (!DENSE && a.table_mode == kTablesPacked) {
+      // packed pools hold the selected pages in table order (copy arm)
+      const long long pp = (long long)tbase + e0 + idx;
+      pg = (n > 0) ? (int)(pp < a.packed_pages ? pp : a.packed_pages - 1) : 0;
+    } else {
+      pg = (n > 0) ? ptab[blk] : 0;
+    }
   };
   fetch(0, blk_cur, pg_cur);
   fetch(64, blk_nxt, pg_nxt);
@@ -469,6 +479,61 @@ __global__ __launch_bounds__(256, 2) void paged_attention_kernel(const AttnArgs 
 }
 
 
+// Copy arm (Sec. 4.4): pack the selected K and V pages of every table row into
+// contiguous pools in table order (packed page p = table entry p of the CSR),
+// so that attention can run on contiguous KV.  One workgroup per packed page;
+// the row of entry p is found by binary search in kv_indptr.
+template <int D>
+__global__ __launch_bounds__(256) void gather_kernel(
+    const uint16_t* __restrict__ k_pool, const uint16_t* __restrict__ v_pool,
+    const int32_t* __restrict__ page_table, const int32_t* __restrict__ kv_indptr,
+    const int32_t* __restrict__ kv_indices, int R, int G, int group_size, int Hq, int Hkv,
+    int max_kv_blocks, uint16_t* __restrict__ k_packed, uint16_t* __restrict__ v_packed) {
+  const int p = blockIdx.x;
+  if (p >= kv_indptr[R]) return;
+  int lo = 0, hi = R;   // kv_indptr[lo] <= p < kv_indptr[hi]
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (kv_indptr[mid] <= p) lo = mid;
+    else hi = mid;
+  }
+  const int b = lo / G, g = lo % G;
+  const int kvh = (g * group_size) / (Hq / Hkv);
+  const int j = kv_indices[p];
+  if (j < 0 || j >= max_kv_blocks) return;
+  const int pg = page_table[((size_t)b * Hkv + kvh) * max_kv_blocks + j];
+  constexpr int N16 = kPage * D * 2 / 16;   // 16-byte pieces per page
+  const uint4* ks = reinterpret_cast<const uint4*>(k_pool + (size_t)pg * kPage * D);
+  const uint4* vs = reinterpret_cast<const uint4*>(v_pool + (size_t)pg * kPage * D);
+  uint4* kd = reinterpret_cast<uint4*>(k_packed + (size_t)p * kPage * D);
+  uint4* vd = reinterpret_cast<uint4*>(v_packed + (size_t)p * kPage * D);
+#pragma unroll
+  for (int i = threadIdx.x; i < N16; i += 256) {
+    const uint4 kv = ks[i], vv = vs[i];
+    kd[i] = kv;
+    vd[i] = vv;
+  }
+}
+
+hipError_t launch_gather(const Dims& d, const uint16_t* k_pool, const uint16_t* v_pool,
+                         const int32_t* page_table, const int32_t* kv_indptr,
+                         const int32_t* kv_indices, int group_size, long long capacity_pages,
+                         uint16_t* k_packed, uint16_t* v_packed, hipStream_t st) {
+  const int G = d.Hq / group_size;
+  const int R = d.B * G;
+  if (capacity_pages <= 0) return hipSuccess;
+  const int grid = (int)capacity_pages;
+  if (d.D == 128)
+    gather_kernel<128><<<grid, 256, 0, st>>>(k_pool, v_pool, page_table, kv_indptr, kv_indices,
+                                             R, G, group_size, d.Hq, d.Hkv, d.max_kv_blocks,
+                                             k_packed, v_packed);
+  else
+    gather_kernel<64><<<grid, 256, 0, st>>>(k_pool, v_pool, page_table, kv_indptr, kv_indices,
+                                            R, G, group_size, d.Hq, d.Hkv, d.max_kv_blocks,
+                                            k_packed, v_packed);
+  return hipGetLastError();
+}
+
 // Split-KV merge: lse = log sum_i exp(lse_i), out = sum_i exp(lse_i - lse) o_i.
 // One 32-lane half-wave per (b, h, t) row, 4 floats of d per lane (D = 128)
 // or 2 (D = 64).
@@ -546,6 +611,8 @@ hipError_t launch_attention(const Dims& d, const AttnLaunch& L, hipStream_t st) 
   a.G = d.Hq / L.group_size;
   a.n_qtiles = d.C / attn_query_tile(L.group_size);
   a.splits = L.splits;
+  a.table_mode = L.table_mode;
+  a.packed_pages = L.packed_pages;
   a.scale_log2 = L.sm_scale * kLog2e;
   const int nwg = attn_base_workgroups(d, L.group_size) * L.splits;
   if (d.D == 128) {

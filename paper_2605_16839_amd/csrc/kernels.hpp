@@ -30,6 +30,17 @@ size_t tables_ws_bytes(const Dims& d, int group_size);
 hipError_t launch_tables(const Dims& d, const uint64_t* masks, const int32_t* cached_len,
                          int group_size, int32_t* kv_indptr, int32_t* kv_indices, void* ws,
                          hipStream_t st);
+// Block-sparse rows (b, h, Q-block i) holding the union of the group of h,
+// causally limited to Q-block i (the block-sparse arm at matched tables).
+size_t union_rows_ws_bytes(const Dims& d, int group_size);
+hipError_t launch_union_rows(const Dims& d, const uint64_t* masks, const int32_t* cached_len,
+                             int group_size, int32_t* kv_indptr, int32_t* kv_indices, void* ws,
+                             hipStream_t st);
+
+// Table layouts the attention kernel understands.
+constexpr int kTablesPerGroup = 0;   // row b*G + g, entries translated by page_table
+constexpr int kTablesPerQTile = 1;   // row (b*Hq + h)*n_qtiles + tile (block-sparse arm)
+constexpr int kTablesPacked = 2;     // per-group rows; page of entry p is p (copy arm)
 
 // Attention over per-group tables (dense = identity tables, no table read).
 struct AttnLaunch {
@@ -47,10 +58,16 @@ struct AttnLaunch {
   int splits;        // >= 1
   void* ws;          // partials when splits > 1
   bool dense;
+  int table_mode = kTablesPerGroup;
+  long long packed_pages = 0;
 };
 int attn_query_tile(int group_size);                    // chunk queries per workgroup
 int attn_base_workgroups(const Dims& d, int group_size);
 size_t attn_ws_bytes(const Dims& d, int splits);
 hipError_t launch_attention(const Dims& d, const AttnLaunch& a, hipStream_t st);
+hipError_t launch_gather(const Dims& d, const uint16_t* k_pool, const uint16_t* v_pool,
+                         const int32_t* page_table, const int32_t* kv_indptr,
+                         const int32_t* kv_indices, int group_size, long long capacity_pages,
+                         uint16_t* k_packed, uint16_t* v_packed, hipStream_t st);
 
 }  // namespace ca

@@ -101,6 +101,68 @@ __global__ __launch_bounds__(256) void compact_kernel(const uint64_t* __restrict
   }
 }
 
+// Block-sparse arm at matched tables (Sec. 4.4): the union of execution group
+// g(h) as the mask row of every (b, h, Q-block i), limited to the blocks that
+// Q-block i can see causally (j < nC_b + (i+1)*q_block/page).  One workgroup
+// per (b, h, i) row; words from the group rows written by union_kernel.
+__global__ __launch_bounds__(256) void expand_union_kernel(const uint64_t* __restrict__ gwords,
+                                                           const int32_t* __restrict__ cached_len,
+                                                           uint64_t* __restrict__ rwords,
+                                                           int32_t* __restrict__ counts, int Hq,
+                                                           int nqb, int W, int group_size,
+                                                           int q_block, int page) {
+  __shared__ int red[4];
+  const int r = blockIdx.x;                 // (b*Hq + h)*nqb + i
+  const int i = r % nqb;
+  const int h = (r / nqb) % Hq;
+  const int b = r / (nqb * Hq);
+  const int G = Hq / group_size;
+  const int t = threadIdx.x;
+  const int lim = cached_len[b] / page + (i + 1) * q_block / page;
+  const uint64_t* src = gwords + ((size_t)b * G + h / group_size) * W;
+  int cnt = 0;
+  for (int w = t; w < W; w += 256) {
+    unsigned long long v = src[w];
+    const int lo = w * 64;
+    if (lo >= lim) v = 0ull;
+    else if (lim - lo < 64) v &= (~0ull >> (64 - (lim - lo)));
+    rwords[(size_t)r * W + w] = v;
+    cnt += __popcll(v);
+  }
+  cnt = wave_sum(cnt);
+  if (lane_id() == 0) red[t >> 6] = cnt;
+  __syncthreads();
+  if (t == 0) counts[r] = red[0] + red[1] + red[2] + red[3];
+}
+
+size_t union_rows_ws_bytes(const Dims& d, int group_size) {
+  const size_t R = (size_t)d.B * d.Hq * d.nqb;
+  return tables_ws_bytes(d, group_size) + R * d.W * sizeof(uint64_t) + R * sizeof(int32_t);
+}
+
+hipError_t launch_union_rows(const Dims& d, const uint64_t* masks, const int32_t* cached_len,
+                             int group_size, int32_t* kv_indptr, int32_t* kv_indices, void* ws,
+                             hipStream_t st) {
+  const int G = d.Hq / group_size;
+  const int RG = d.B * G;
+  const int R = d.B * d.Hq * d.nqb;
+  uint64_t* gwords = static_cast<uint64_t*>(ws);
+  int32_t* gcounts = reinterpret_cast<int32_t*>(gwords + (size_t)RG * d.W);
+  uint64_t* rwords = reinterpret_cast<uint64_t*>(
+      static_cast<char*>(ws) + tables_ws_bytes(d, group_size));
+  int32_t* rcounts = reinterpret_cast<int32_t*>(rwords + (size_t)R * d.W);
+  union_kernel<<<RG, 256, 0, st>>>(masks, cached_len, gwords, gcounts, d.Hq, d.nqb, d.W,
+                                   group_size, G, d.chunk_blocks);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  expand_union_kernel<<<R, 256, 0, st>>>(gwords, cached_len, rwords, rcounts, d.Hq, d.nqb, d.W,
+                                         group_size, d.q_block, d.page);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  compact_kernel<<<R, 256, 0, st>>>(rwords, rcounts, kv_indptr, kv_indices, d.W);
+  return hipGetLastError();
+}
+
 size_t tables_ws_bytes(const Dims& d, int group_size) {
   const size_t R = (size_t)d.B * (d.Hq / group_size);
   return R * d.W * sizeof(uint64_t) + R * sizeof(int32_t);

@@ -33,7 +33,8 @@ def test_exports_every_declared_symbol(lib):
     assert declared == set(ca.EXPORTED)
     for name in declared:
         assert hasattr(lib, name), name
-    assert lib.ca_abi_version() == 1
+    m = re.search(r"#define CA_ABI_VERSION (\d+)", open(HEADER).read())
+    assert lib.ca_abi_version() == int(m.group(1))
 
 
 def _prob(**kw):
@@ -97,3 +98,29 @@ def test_workspace_sizes(lib):
                  max_kv_blocks=20, cached_len=[1024])
     assert ca.attention_workspace_bytes(tiny, 4, 0) > 0
     assert ca.tables_workspace_bytes(p, 3) == 0        # invalid group -> 0
+    # block-sparse tables: one row per (b, h, Q-block) = 512 rows of 32 words + counts
+    assert ca.block_sparse_tables_workspace_bytes(p) == 512 * 32 * 8 + 512 * 4
+    assert ca.block_sparse_tables_workspace_bytes(p, 4) == (8 * 32 * 8 + 8 * 4) + (512 * 32 * 8 + 512 * 4)
+    assert ca.block_sparse_tables_workspace_bytes(p, 3) == 0
+
+
+def test_arm_validation(lib):
+    """Host-side checks of the copy and block-sparse arms (nothing is launched)."""
+    fake = ctypes.c_void_p(0x1000)    # never dereferenced: validation fails first
+    tiny = _prob(num_q_heads=4, num_kv_heads=1, head_dim=64, q_block=64, chunk_len=256,
+                 max_kv_blocks=20, cached_len=[1024])
+    tiny.c.cached_len = fake.value
+    # a 128-query tile of one head cannot follow 64-query Q-blocks
+    s = lib.ca_block_sparse_chunk_attention(tiny.ref, fake, fake, fake, fake, fake, fake, 0.1, 1,
+                                            fake, None, None, 0, None)
+    assert lib.ca_status_string(s).decode() == "CA_ERR_UNSUPPORTED"
+    p = _prob()
+    p.c.cached_len = fake.value
+    s = lib.ca_packed_chunk_attention(p.ref, fake, fake, fake, fake, fake, 4, 0.1, 1, 0,
+                                      fake, None, None, 0, None)
+    assert lib.ca_status_string(s).decode() == "CA_ERR_SHAPE"     # capacity 0
+    s = lib.ca_gather_selected_pages(p.ref, fake, fake, fake, fake, fake, 4, fake, fake,
+                                     8 * 2048 + 1, None)
+    assert lib.ca_status_string(s).decode() == "CA_ERR_SHAPE"     # beyond B*G*max_kv_blocks
+    s = lib.ca_gather_selected_pages(p.ref, fake, fake, fake, fake, fake, 3, fake, fake, 10, None)
+    assert lib.ca_status_string(s).decode() == "CA_ERR_GROUP"

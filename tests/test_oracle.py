@@ -250,6 +250,53 @@ def test_page_permutation_invariance(workload_inputs):
     assert np.array_equal(out, base) and np.array_equal(lse, lb)
 
 
+def test_block_sparse_rows_equal_masked_sdpa(workload_inputs):
+    """Block-sparse arm: each (head, Q-block) row == torch fp64 SDPA with only
+    that row's mask blocks open (independent of the gather/table code)."""
+    d = workload_inputs("tiny_gqa_1k")
+    w = d["workload"]
+    nc = w.n_cached_blocks(0)
+    masks = synth.random_masks(13, 1, 4, w.n_qblocks, w.q_block, w.page_size, [nc],
+                               w.chunk_len, w.words, 0.1)
+    bits = oracle.unpack_masks(masks)
+    out, lse = oracle.block_sparse_attention(d["q"], d["k_pool"], d["v_pool"], d["page_table"],
+                                             d["cached_len"], bits, w.q_block, w.sm_scale)
+    assert np.isfinite(lse).all()
+    distinct = 0
+    for h in range(4):
+        for i in range(w.n_qblocks):
+            keep = [j for j in range(w.n_kv_blocks(0)) if bits[0, h, i, j]]
+            qs = np.arange(i * w.q_block, (i + 1) * w.q_block)
+            ref = _sdpa_ref(d, 0, h, qs, keep_blocks=keep)
+            np.testing.assert_allclose(out[0, qs, h, :], ref, atol=1e-12, rtol=0)
+            distinct += keep != [j for j in range(w.n_kv_blocks(0)) if bits[0, 0, 0, j]]
+    assert distinct > 0      # rows really differ from each other
+
+
+def test_block_sparse_group_uniform_rows_equal_union(workload_inputs):
+    """When every (head, Q-block) row of a group selects the same cached blocks,
+    per-row execution and the group-union table give the same attention (the
+    extra chunk blocks of the union are causally invisible)."""
+    d = workload_inputs("tiny_gqa_1k")
+    w = d["workload"]
+    nc = w.n_cached_blocks(0)
+    one = synth.random_masks(17, 1, 1, 1, w.q_block, w.page_size, [nc], w.chunk_len, w.words, 0.2)
+    sel = oracle.unpack_masks(one)[0, 0, 0, :nc]
+    nkb = w.n_kv_blocks(0)
+    bits = np.zeros((1, 4, w.n_qblocks, 64 * w.words), dtype=bool)
+    for i in range(w.n_qblocks):
+        bits[0, :, i, :nc] = sel
+        last = nc + (i + 1) * w.q_block // w.page_size       # chunk-causal bits of Q-block i
+        bits[0, :, i, nc:last] = True
+    T = [[sorted(set(np.nonzero(sel)[0].tolist()) | set(range(nc, nkb)))]]
+    bs, bl = oracle.block_sparse_attention(d["q"], d["k_pool"], d["v_pool"], d["page_table"],
+                                           d["cached_len"], bits, w.q_block, w.sm_scale)
+    un, ul = oracle.chunk_attention(d["q"], d["k_pool"], d["v_pool"], d["page_table"],
+                                    d["cached_len"], T, 4, w.sm_scale)
+    np.testing.assert_allclose(bs, un, atol=1e-12, rtol=0)
+    np.testing.assert_allclose(bl, ul, atol=1e-12, rtol=0)
+
+
 # ---------------------------------------------------------------------------
 # estimator (the selector reading; see oracle/estimator.py)
 # ---------------------------------------------------------------------------
