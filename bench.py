@@ -39,6 +39,11 @@ def parse():
     ap.add_argument("--rho", type=float, default=None,
                     help="override the query-direction weight (0 = literal iid inputs)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--group-size", type=int, default=None,
+                    help="execution-group size (default: the workload's; a divisor of Hq/Hkv)")
+    ap.add_argument("--chunk-sweep", action="store_true",
+                    help="also prefill one 128K sequence chunk by chunk at chunk sizes "
+                         "512/1024/2048 (Table 5) and report cumulative stage times")
     ap.add_argument("--no-arms", action="store_true",
                     help="skip the copy and block-sparse execution arms")
     ap.add_argument("--cpu-sample-queries", type=int, default=1024)
@@ -142,6 +147,23 @@ def cpu_baseline(w, d, tables_T, sample_queries: int):
     }
 
 
+def stage_densities(w, bits: np.ndarray) -> dict:
+    """Cached-block density after each aggregation step (Table 2's quantities):
+    per (head, Q-block) row, after the Q-block union, after the group union."""
+    pre, qu, gu = [], [], []
+    for b in range(w.batch):
+        nc = w.n_cached_blocks(b)
+        if nc == 0:
+            continue
+        cb = bits[b, :, :, :nc]
+        pre.append(cb.mean())
+        per_head = cb.any(axis=1)
+        qu.append(per_head.mean())
+        gu.append(per_head.reshape(-1, w.group_size, nc).any(axis=1).mean())
+    f = lambda v: round(float(np.mean(v)), 4) if v else 0.0
+    return {"pre_union": f(pre), "q_union": f(qu), "group_union": f(gu)}
+
+
 def block_sparse_flops(w, bits: np.ndarray) -> float:
     """4*D per unmasked (query, key) pair of every (head, Q-block) mask row."""
     qb, pg = w.q_block, w.page_size
@@ -229,6 +251,71 @@ def strategy_arms(ca, p, w, q, kp, vp, pt, masks, tables, ip, args, stream, ev):
     return res
 
 
+def chunk_sweep(ca, stream, ev):
+    """Chunked prefill of one 131072-token sequence at chunk sizes 512, 1024 and
+    2048 (Sec. 4.3 / Table 5 sizes): per chunk the incremental estimator (only
+    the newly cached blocks are pooled), the tables and the attention, against
+    the dense paged attention of the same chunk.  One layer, one timed pass per
+    chunk; the sums are the cumulative attention-side prefill cost."""
+    import torch
+    from dataclasses import replace
+
+    import synth
+
+    base = synth.get_workload("sweep_128k_64chunks")
+    total = base.chunk_len * synth.configs.SWEEP_CHUNKS
+    dev = "cuda"
+    bf = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
+    res = {}
+    for C in (512, 1024, 2048):
+        n = total // C
+        seq = synth.make_sweep_sequence(replace(base, chunk_len=C), n_chunks=n)
+        kd, vd = bf(seq.k_pool), bf(seq.v_pool)
+        k_mean = torch.zeros((1, base.num_kv_heads, base.max_kv_blocks, base.head_dim),
+                             dtype=torch.float32, device=dev)
+        cb = C // base.page_size
+        sums = {"estimate": 0.0, "tables": 0.0, "attention": 0.0, "dense": 0.0}
+        final = {}
+        for c in range(-1, n):          # c = -1: untimed warm-up on chunk 0
+            d = seq.inputs(max(c, 0))
+            w = d["workload"]
+            p = ca.Problem.from_workload(w, device=dev)
+            q, pt = bf(d["q"]), torch.from_numpy(d["page_table"]).to(dev)
+            m = [ev() for _ in range(6)]
+            torch.cuda.synchronize()
+            m[0].record(stream)
+            masks, _ = ca.estimate_masks(p, q, kd, pt, w.top_frac, w.sink_blocks,
+                                         w.local_blocks, k_mean=k_mean,
+                                         k_mean_first_block=max(c, 0) * cb)
+            m[1].record(stream)
+            tabs = ca.build_block_tables(p, masks, w.group_size)
+            m[2].record(stream)
+            ca.chunk_attention(p, q, (kd, vd), pt, tabs, w.group_size, w.sm_scale)
+            m[3].record(stream)
+            m[4].record(stream)
+            ca.dense_paged_chunk_attention(p, q, (kd, vd), pt, w.sm_scale)
+            m[5].record(stream)
+            torch.cuda.synchronize()
+            if c < 0:
+                continue
+            t = {"estimate": m[0].elapsed_time(m[1]), "tables": m[1].elapsed_time(m[2]),
+                 "attention": m[2].elapsed_time(m[3]), "dense": m[4].elapsed_time(m[5])}
+            for k in sums:
+                sums[k] += t[k]
+            if c == n - 1:
+                final = {k: round(v, 4) for k, v in t.items()}
+        sel = sums["estimate"] + sums["tables"] + sums["attention"]
+        res[str(C)] = {"chunks": n, "cumulative_ms": {k: round(v, 3) for k, v in sums.items()},
+                       "cumulative_speedup_vs_dense": round(sums["dense"] / sel, 3),
+                       "final_chunk_ms": final,
+                       "final_chunk_speedup_vs_dense": round(
+                           final["dense"] / (final["estimate"] + final["tables"]
+                                             + final["attention"]), 3)}
+        del kd, vd, seq
+        torch.cuda.empty_cache()
+    return res
+
+
 def main():
     args = parse()
     if args.copy_calibration:
@@ -244,9 +331,12 @@ def main():
     import paper_2605_16839_amd as ca
     import synth
 
-    w = synth.get_workload(args.workload)
+    over = {}
     if args.rho is not None:
-        w = synth.get_workload(args.workload, rho=args.rho)
+        over["rho"] = args.rho
+    if args.group_size is not None:
+        over["group_size"] = args.group_size
+    w = synth.get_workload(args.workload, **over)
     d = synth.make_inputs(w)
     dev = "cuda"
     bf = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
@@ -372,6 +462,8 @@ def main():
         "speedup_vs_dense_kernel_only": round(dense_ms / attn_ms, 3),
         "attention_kernel_ms": round(attn_ms, 4),
         "executed_cached_density": round(density, 4),
+        "densities": stage_densities(w, np.unpackbits(bufs["masks"].cpu().numpy().view(np.uint8),
+                                                      axis=-1, bitorder="little").astype(bool)),
         "attention_tflops_selected": round(attn_tflops, 1),
         "dense_tflops": round(dense_tflops, 1),
         "mfma_util_time_based": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
@@ -384,6 +476,8 @@ def main():
     if not args.no_arms:
         res["arms"] = strategy_arms(ca, p, w, q, kp, vp, pt, bufs["masks"], tables, ip,
                                     args, stream, ev)
+    if args.chunk_sweep:
+        res["chunk_sweep"] = chunk_sweep(ca, stream, ev)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(w, d, None, args.cpu_sample_queries)
     print(json.dumps(res), flush=True)

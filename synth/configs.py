@@ -1,4 +1,4 @@
-"""The five synthetic workloads, written as data.
+"""The synthetic workloads, written as data.
 
 Shapes follow the LLaMA-3.1-8B attention layer the paper measures on
 (Sec. 4.1: 32 query heads, 8 KV heads, head_dim 128) with a 2048-token
@@ -92,7 +92,7 @@ def _llama(name, seed, cached_lens, top_frac, needles, description, **kw):
     nkb_max = max((c + 2048) // PAGE for c in cached_lens)
     return Workload(
         name=name, seed=seed, batch=len(cached_lens), num_q_heads=32,
-        num_kv_heads=8, head_dim=128, q_block=128, chunk_len=2048,
+        num_kv_heads=kw.pop("num_kv_heads", 8), head_dim=128, q_block=128, chunk_len=2048,
         cached_lens=tuple(cached_lens), max_kv_blocks=kw.pop("max_kv_blocks", nkb_max),
         sm_scale=1.0 / math.sqrt(128.0), mask_kind="estimator",
         top_frac=top_frac, needles_per_kv_head=needles, rho=RHO_CALIBRATED,
@@ -117,6 +117,13 @@ WORKLOADS = {
     "batched_ragged_4seq": _llama(
         "batched_ragged_4seq", 4, (16384, 32768, 65536, 126976), 0.08, 0,
         "4 sequences sharing one page pool, top 8%, ragged tables"),
+    # Qwen3-30B-A3B-like attention layer (32 query heads on 4 KV heads, GQA 8:1):
+    # execution groups of 4 heads are sub-groups of a KV group, so every KV
+    # head has two tables (App. B.1).
+    "qwen3_30b_128k_final": _llama(
+        "qwen3_30b_128k_final", 6, (129024,), 0.05, 32,
+        "Qwen3-30B-A3B-like layer (32/4 heads), 128K final chunk, top 5%, sub-groups of 4",
+        num_kv_heads=4),
     "sweep_128k_64chunks": _llama(
         "sweep_128k_64chunks", 5, (129024,), 0.05, 64,
         "131072-token sequence prefilled in 64 chunks of 2048, top 5%",

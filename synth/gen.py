@@ -245,10 +245,7 @@ class SweepSequence:
     page_table_full: np.ndarray       # [1, Hkv, 2048]
     needles: List[Tuple[int, int, int, int, int, int]]  # (b, kvh, j, h, target chunk, i)
     mu: Optional[np.ndarray]
-
-    @property
-    def n_chunks(self) -> int:
-        return SWEEP_CHUNKS
+    n_chunks: int = SWEEP_CHUNKS
 
     def q_chunk(self, c: int) -> np.ndarray:
         return _gen_q(self.base, 0, c, self.mu)[None]
@@ -264,8 +261,8 @@ class SweepSequence:
                     needles=[(b, kvh, j, h, i) for (b, kvh, j, h, tc, i) in self.needles if tc == c])
 
 
-def make_sweep_sequence(w: Workload) -> SweepSequence:
-    """Whole-sequence K/V pool for the chunked sweep.
+def make_sweep_sequence(w: Workload, n_chunks: int = SWEEP_CHUNKS) -> SweepSequence:
+    """Whole-sequence K/V pool for a chunked prefill of ``n_chunks`` chunks.
 
     Needles: ``needles_per_kv_head`` blocks per KV head drawn without
     replacement from blocks [1, chunk_blocks * (n_chunks - 1)); each targets a
@@ -273,18 +270,18 @@ def make_sweep_sequence(w: Workload) -> SweepSequence:
     """
     assert w.batch == 1
     cb = w.chunk_len // w.page_size
-    nkb_total = cb * SWEEP_CHUNKS
+    nkb_total = cb * n_chunks
     full = replace(w, cached_lens=(nkb_total * w.page_size - w.chunk_len,))
     pt, total = _page_assignment(full, [nkb_total])
     mu = _mu(w, 0) if w.rho else None
     rng = _rng(w.seed, _T_NEEDLE)
     needles = []
     for kvh in range(w.num_kv_heads):
-        js = np.sort(rng.choice(np.arange(1, cb * (SWEEP_CHUNKS - 1)),
+        js = np.sort(rng.choice(np.arange(1, cb * (n_chunks - 1)),
                                 size=w.needles_per_kv_head, replace=False))
         for j in js:
             own = int(j) // cb
-            tc = int(rng.integers(own + 1, SWEEP_CHUNKS))
+            tc = int(rng.integers(own + 1, n_chunks))
             h = kvh * w.ratio + int(rng.integers(w.ratio))
             i = int(rng.integers(w.n_qblocks))
             needles.append((0, kvh, int(j), h, tc, i))
@@ -304,4 +301,4 @@ def make_sweep_sequence(w: Workload) -> SweepSequence:
 
     k_pool, v_pool = _fill_kv(full, pt, total, [nkb_total], needle_fn)
     return SweepSequence(base=w, k_pool=k_pool, v_pool=v_pool, page_table_full=pt,
-                         needles=needles, mu=mu)
+                         needles=needles, mu=mu, n_chunks=n_chunks)

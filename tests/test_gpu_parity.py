@@ -117,7 +117,8 @@ def test_tables_adversarial(seed):
         _assert_tables_equal(_gpu_tables(p, masks, gs), ref)
 
 
-@pytest.mark.parametrize("name", ["llama8b_32k", "llama8b_128k_final", "batched_ragged_4seq"])
+@pytest.mark.parametrize("name", ["llama8b_32k", "llama8b_128k_final", "batched_ragged_4seq",
+                                  "qwen3_30b_128k_final"])
 def test_tables_workloads_bitexact(name, workload_inputs, oracle_estimate):
     d = workload_inputs(name)
     w = d["workload"]
@@ -128,6 +129,11 @@ def test_tables_workloads_bitexact(name, workload_inputs, oracle_estimate):
     _assert_tables_equal(got, ref)
     assert np.array_equal(got[0], _gpu_tables(p, masks, w.group_size)[0])   # deterministic
     ca.validate_tables(p, w.group_size, (i32_dev(got[0]), i32_dev(got[1])))
+    if w.ratio > w.group_size:
+        # sub-groups (App. B.1): the full KV group's tables as well
+        nkb = [w.n_kv_blocks(b) for b in range(w.batch)]
+        ref_full = oracle.tables_to_csr(oracle.block_tables(masks, w.ratio, nkb))
+        _assert_tables_equal(_gpu_tables(p, masks, w.ratio), ref_full)
 
 
 # ---------------------------------------------------------------------------
@@ -208,7 +214,8 @@ def _near_tie_check(gpu_masks, ref_masks, scores64, w, tol):
     return flips
 
 
-@pytest.mark.parametrize("name", ["llama8b_32k", "llama8b_128k_final", "batched_ragged_4seq"])
+@pytest.mark.parametrize("name", ["llama8b_32k", "llama8b_128k_final", "batched_ragged_4seq",
+                                  "qwen3_30b_128k_final"])
 def test_estimator_end_to_end(name, workload_inputs, oracle_estimate):
     d = workload_inputs(name)
     w = d["workload"]
@@ -273,7 +280,8 @@ def test_attention_first_chunk_no_cache():
     compare_attention(got, lse, ref, ref_lse)
 
 
-@pytest.mark.parametrize("name", ["llama8b_32k", "llama8b_128k_final", "batched_ragged_4seq"])
+@pytest.mark.parametrize("name", ["llama8b_32k", "llama8b_128k_final", "batched_ragged_4seq",
+                                  "qwen3_30b_128k_final"])
 def test_attention_workloads_sampled(name, workload_inputs, oracle_estimate):
     d = workload_inputs(name)
     w = d["workload"]

@@ -100,3 +100,21 @@ def test_calibrated_density_and_needles(oracle_estimate, workload_inputs):
     assert all(bits[b, h, i, j] for (b, kvh, j, h, i) in d["needles"])
     q = synth.bf16_bits_to_f32(d["q"])
     assert abs(q.std() - 1.0) < 0.02                                  # still N(0,1) marginally
+
+
+def test_subgroup_densities_qwen_shape(oracle_estimate, workload_inputs):
+    """GQA 8:1 with execution groups of 4 (two tables per KV head, App. B.1):
+    density grows at every aggregation step and the sub-group union keeps
+    more sparsity than the full KV group (the pattern of Table 2)."""
+    name = "qwen3_30b_128k_final"
+    d = workload_inputs(name)
+    w = d["workload"]
+    assert w.ratio == 8 and w.group_size == 4
+    masks, _ = oracle_estimate(name)
+    nc = [w.n_cached_blocks(0)]
+    sub = oracle.union_densities(masks, 4, nc)
+    full = oracle.union_densities(masks, 8, nc)
+    assert sub["pre_union"] < sub["q_union"] < sub["group_union"] < full["group_union"] < 1.0
+    bits = oracle.unpack_masks(masks)
+    assert all(bits[b, h, i, j] for (b, kvh, j, h, i) in d["needles"])
+
