@@ -274,6 +274,7 @@ def chunk_sweep(ca, stream, ev):
         k_mean = torch.zeros((1, base.num_kv_heads, base.max_kv_blocks, base.head_dim),
                              dtype=torch.float32, device=dev)
         cb = C // base.page_size
+        ebufs = {}                      # estimator buffers reused across the chunks
         sums = {"estimate": 0.0, "tables": 0.0, "attention": 0.0, "dense": 0.0}
         final = {}
         for c in range(-1, n):          # c = -1: untimed warm-up on chunk 0
@@ -286,7 +287,7 @@ def chunk_sweep(ca, stream, ev):
             m[0].record(stream)
             masks, _ = ca.estimate_masks(p, q, kd, pt, w.top_frac, w.sink_blocks,
                                          w.local_blocks, k_mean=k_mean,
-                                         k_mean_first_block=max(c, 0) * cb)
+                                         k_mean_first_block=max(c, 0) * cb, bufs=ebufs)
             m[1].record(stream)
             tabs = ca.build_block_tables(p, masks, w.group_size)
             m[2].record(stream)

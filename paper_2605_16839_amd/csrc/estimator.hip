@@ -18,7 +18,7 @@ namespace ca {
 // ---------------------------------------------------------------------------
 template <int D>
 __device__ __forceinline__ void pool_rows(const uint16_t* __restrict__ base, size_t stride,
-                                          int rows, float* __restrict__ out) {
+                                          int rows, float* __restrict__ out, float scale) {
   constexpr int CPR = D / 8;           // 16-byte chunks per row
   constexpr int RPI = kWave / CPR;     // rows per load instruction
   const int l = lane_id();
@@ -39,25 +39,32 @@ __device__ __forceinline__ void pool_rows(const uint16_t* __restrict__ base, siz
     for (int e = 0; e < 8; ++e) acc[e] += __shfl_xor(acc[e], o, kWave);
   }
   if (l < CPR) {
-    const float inv = 1.0f / (float)rows;
     float4* dst = reinterpret_cast<float4*>(out + chunk * 8);
-    dst[0] = make_float4(acc[0] * inv, acc[1] * inv, acc[2] * inv, acc[3] * inv);
-    dst[1] = make_float4(acc[4] * inv, acc[5] * inv, acc[6] * inv, acc[7] * inv);
+    dst[0] = make_float4(acc[0] * scale, acc[1] * scale, acc[2] * scale, acc[3] * scale);
+    dst[1] = make_float4(acc[4] * scale, acc[5] * scale, acc[6] * scale, acc[7] * scale);
   }
 }
 
-// One wave per (b, h, i).
+// One workgroup per (b, h, i): each wave sums a quarter of the Q-block's rows,
+// the four partial sums meet in LDS.
 template <int D>
 __global__ __launch_bounds__(256) void pool_q_kernel(const uint16_t* __restrict__ q,
                                                      float* __restrict__ q_mean, int B, int C,
                                                      int Hq, int q_block, int nqb) {
-  const int w = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (w >= B * Hq * nqb) return;
+  __shared__ __attribute__((aligned(16))) float part[4][D];
+  const int w = blockIdx.x;
   const int i = w % nqb;
   const int h = (w / nqb) % Hq;
   const int b = w / (nqb * Hq);
-  const uint16_t* base = q + (((size_t)b * C + (size_t)i * q_block) * Hq + h) * D;
-  pool_rows<D>(base, (size_t)Hq * D, q_block, q_mean + (size_t)w * D);
+  const int wv = threadIdx.x >> 6;
+  const int rows = q_block / 4;
+  const uint16_t* base = q + (((size_t)b * C + (size_t)i * q_block + (size_t)wv * rows) * Hq + h) * D;
+  pool_rows<D>(base, (size_t)Hq * D, rows, part[wv], 1.0f);
+  __syncthreads();
+  const int t = threadIdx.x;
+  if (t < D)
+    q_mean[(size_t)w * D + t] = ((part[0][t] + part[1][t]) + (part[2][t] + part[3][t])) *
+                                (1.0f / (float)q_block);
 }
 
 // One wave per (b, kvh, j), j in [first_block, nKB_b).
@@ -75,14 +82,15 @@ __global__ __launch_bounds__(256) void pool_k_kernel(const uint16_t* __restrict_
   if (j >= nkb) return;
   const int page = page_table[(size_t)bk * max_kv_blocks + j];
   pool_rows<D>(k_pool + (size_t)page * kPage * D, D, kPage,
-               k_mean + ((size_t)bk * max_kv_blocks + j) * D);
+               k_mean + ((size_t)bk * max_kv_blocks + j) * D, 1.0f / (float)kPage);
 }
 
 // ---------------------------------------------------------------------------
 // Scores: for one (b, kvh), the ratio*nQB pooled query rows are contiguous in
 // q_mean and the matching score rows are contiguous too.  A workgroup
-// computes a 64-row x 64-block tile with fp32 FMAs (d ascending), staging
-// 32-wide slices of both operands in LDS.
+// computes a 64-row x 32-block tile with fp32 FMAs (d ascending) from whole
+// rows of both operands staged in LDS; lanes 0..15 of a row group own 16
+// consecutive blocks, so the score stores are contiguous.
 // ---------------------------------------------------------------------------
 template <int D>
 __global__ __launch_bounds__(256) void scores_kernel(const float* __restrict__ q_mean,
@@ -90,54 +98,58 @@ __global__ __launch_bounds__(256) void scores_kernel(const float* __restrict__ q
                                                      const int32_t* __restrict__ cached_len,
                                                      float* __restrict__ scores, int Hq, int Hkv,
                                                      int nqb, int max_kv_blocks) {
-  constexpr int DS = 32;
-  __shared__ float qs[64][DS + 1];
-  __shared__ float ks[64][DS + 1];
+  constexpr int TR = 64, TB = 32;
+  __shared__ float qs[TR][D + 1];
+  __shared__ float ks[TB][D + 1];
   const int bk = blockIdx.z;
   const int b = bk / Hkv, kvh = bk % Hkv;
   const int ratio = Hq / Hkv;
   const int nrows = ratio * nqb;
   const int nc = cached_len[b] / kPage;
-  const int j0 = blockIdx.x * 64, r0 = blockIdx.y * 64;
+  const int j0 = blockIdx.x * TB, r0 = blockIdx.y * TR;
   if (j0 >= nc) return;
   const size_t row_base = ((size_t)b * Hq + (size_t)kvh * ratio) * nqb;
   const float* qrow = q_mean + row_base * D;
   const float* krow = k_mean + ((size_t)bk * max_kv_blocks) * D;
   const int t = threadIdx.x;
-  const int tr = t >> 4, tc = t & 15;
-  float acc[4][4];
+  for (int x = t; x < TR * D / 4; x += 256) {
+    const int r = x / (D / 4), d4 = x % (D / 4);
+    const float4 v = (r0 + r < nrows)
+                         ? *reinterpret_cast<const float4*>(qrow + (size_t)(r0 + r) * D + 4 * d4)
+                         : make_float4(0.f, 0.f, 0.f, 0.f);
+    qs[r][4 * d4 + 0] = v.x; qs[r][4 * d4 + 1] = v.y;
+    qs[r][4 * d4 + 2] = v.z; qs[r][4 * d4 + 3] = v.w;
+  }
+  for (int x = t; x < TB * D / 4; x += 256) {
+    const int r = x / (D / 4), d4 = x % (D / 4);
+    const float4 v = (j0 + r < nc)
+                         ? *reinterpret_cast<const float4*>(krow + (size_t)(j0 + r) * D + 4 * d4)
+                         : make_float4(0.f, 0.f, 0.f, 0.f);
+    ks[r][4 * d4 + 0] = v.x; ks[r][4 * d4 + 1] = v.y;
+    ks[r][4 * d4 + 2] = v.z; ks[r][4 * d4 + 3] = v.w;
+  }
+  __syncthreads();
+  const int bc = t & 15, rg = t >> 4;   // blocks bc, bc+16; rows rg + 16a
+  float acc[4][2];
 #pragma unroll
-  for (int a = 0; a < 4; ++a)
+  for (int a = 0; a < 4; ++a) { acc[a][0] = 0.f; acc[a][1] = 0.f; }
+#pragma unroll 8
+  for (int d = 0; d < D; ++d) {
+    const float k0 = ks[bc][d], k1 = ks[bc + 16][d];
 #pragma unroll
-    for (int c = 0; c < 4; ++c) acc[a][c] = 0.f;
-  for (int d0 = 0; d0 < D; d0 += DS) {
-    for (int x = t; x < 64 * DS; x += 256) {
-      const int r = x / DS, d = x % DS;
-      qs[r][d] = (r0 + r < nrows) ? qrow[(size_t)(r0 + r) * D + d0 + d] : 0.f;
-      ks[r][d] = (j0 + r < nc) ? krow[(size_t)(j0 + r) * D + d0 + d] : 0.f;
+    for (int a = 0; a < 4; ++a) {
+      const float qv = qs[rg + 16 * a][d];
+      acc[a][0] = fmaf(qv, k0, acc[a][0]);
+      acc[a][1] = fmaf(qv, k1, acc[a][1]);
     }
-    __syncthreads();
-#pragma unroll 4
-    for (int d = 0; d < DS; ++d) {
-      float qv[4], kv[4];
-#pragma unroll
-      for (int a = 0; a < 4; ++a) qv[a] = qs[tr + 16 * a][d];
-#pragma unroll
-      for (int c = 0; c < 4; ++c) kv[c] = ks[tc + 16 * c][d];
-#pragma unroll
-      for (int a = 0; a < 4; ++a)
-#pragma unroll
-        for (int c = 0; c < 4; ++c) acc[a][c] = fmaf(qv[a], kv[c], acc[a][c]);
-    }
-    __syncthreads();
   }
 #pragma unroll
   for (int a = 0; a < 4; ++a) {
-    const int r = r0 + tr + 16 * a;
+    const int r = r0 + rg + 16 * a;
     if (r >= nrows) continue;
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const int j = j0 + tc + 16 * c;
+    for (int c = 0; c < 2; ++c) {
+      const int j = j0 + bc + 16 * c;
       if (j < nc) scores[(row_base + r) * max_kv_blocks + j] = acc[a][c];
     }
   }
@@ -261,8 +273,7 @@ __global__ __launch_bounds__(256) void select_kernel(const float* __restrict__ s
 // launchers
 // ---------------------------------------------------------------------------
 hipError_t launch_pool_q(const Dims& d, const uint16_t* q, float* q_mean, hipStream_t st) {
-  const int waves = d.B * d.Hq * d.nqb;
-  dim3 grid((waves + 3) / 4);
+  dim3 grid(d.B * d.Hq * d.nqb);
   if (d.D == 128)
     pool_q_kernel<128><<<grid, 256, 0, st>>>(q, q_mean, d.B, d.C, d.Hq, d.q_block, d.nqb);
   else
@@ -289,7 +300,7 @@ hipError_t launch_scores(const Dims& d, const float* q_mean, const float* k_mean
                          const int32_t* cached_len, float* scores, hipStream_t st) {
   if (d.max_nc <= 0) return hipSuccess;
   const int nrows = (d.Hq / d.Hkv) * d.nqb;
-  dim3 grid((d.max_nc + 63) / 64, (nrows + 63) / 64, d.B * d.Hkv);
+  dim3 grid((d.max_nc + 31) / 32, (nrows + 63) / 64, d.B * d.Hkv);
   if (d.D == 128)
     scores_kernel<128><<<grid, 256, 0, st>>>(q_mean, k_mean, cached_len, scores, d.Hq, d.Hkv,
                                              d.nqb, d.max_kv_blocks);
