@@ -44,6 +44,8 @@ def parse():
     ap.add_argument("--chunk-sweep", action="store_true",
                     help="also prefill one 128K sequence chunk by chunk at chunk sizes "
                          "512/1024/2048 (Table 5) and report cumulative stage times")
+    ap.add_argument("--threshold-sweep", action="store_true",
+                    help="also run the alpha-threshold selector at several (alpha, temperature)")
     ap.add_argument("--no-arms", action="store_true",
                     help="skip the copy and block-sparse execution arms")
     ap.add_argument("--cpu-sample-queries", type=int, default=1024)
@@ -317,6 +319,57 @@ def chunk_sweep(ca, stream, ev):
     return res
 
 
+THRESHOLD_POINTS = ((16.0, 0.01), (16.0, 0.03), (16.0, 0.06), (16.0, 0.1), (8.0, 0.06))
+
+
+def threshold_sweep(ca, p, w, q, kp, vp, pt, dense_ms, args, stream, ev):
+    """The alpha-threshold selector (the FlashPrefill-style reading of Sec. 4.1)
+    in place of top-k, at several (temperature, alpha): per point the whole
+    step (estimate + tables + attention) timed over `steps` launches, and the
+    cached density it executes."""
+    import torch
+
+    gs = w.group_size
+    G = w.num_q_heads // gs
+    R = w.batch * G
+    ebufs = {}
+    tables = (torch.empty(R + 1, dtype=torch.int32, device="cuda"),
+              torch.empty(R * w.max_kv_blocks, dtype=torch.int32, device="cuda"))
+    tws = torch.empty(max(ca.tables_workspace_bytes(p, gs), 1), dtype=torch.uint8, device="cuda")
+    out = torch.empty_like(q)
+
+    def step(tau, alpha):
+        masks, _ = ca.estimate_masks_threshold(p, q, kp, pt, alpha, tau, w.sm_scale,
+                                               w.sink_blocks, w.local_blocks, bufs=ebufs)
+        ca.build_block_tables(p, masks, gs, out=tables, ws=tws)
+        ca.chunk_attention(p, q, (kp, vp), pt, tables, gs, w.sm_scale, num_splits=0, out=out)
+
+    res = []
+    for tau, alpha in THRESHOLD_POINTS:
+        for _ in range(args.warmup):
+            step(tau, alpha)
+        torch.cuda.synchronize()
+        t0, t1 = ev(), ev()
+        t0.record(stream)
+        for _ in range(args.steps):
+            step(tau, alpha)
+        t1.record(stream)
+        torch.cuda.synchronize()
+        ms = t0.elapsed_time(t1) / args.steps
+        ip, ix = tables[0].cpu().numpy(), tables[1].cpu().numpy()
+        ncached = sum(w.n_cached_blocks(b) for b in range(w.batch)) * G
+        sel = sum(int(np.count_nonzero(ix[ip[r]:ip[r + 1]] < w.n_cached_blocks(r // G)))
+                  for r in range(R))
+        bits = np.unpackbits(ebufs["masks"].cpu().numpy().view(np.uint8), axis=-1,
+                             bitorder="little").astype(bool)
+        row = np.mean([bits[b, :, :, :w.n_cached_blocks(b)].mean() for b in range(w.batch)])
+        res.append({"temperature": tau, "alpha": alpha, "ms_per_step": round(ms, 4),
+                    "speedup_vs_dense": round(dense_ms / ms, 3),
+                    "row_density": round(float(row), 4),
+                    "executed_cached_density": round(sel / max(ncached, 1), 4)})
+    return res
+
+
 def main():
     args = parse()
     if args.copy_calibration:
@@ -477,6 +530,9 @@ def main():
     if not args.no_arms:
         res["arms"] = strategy_arms(ca, p, w, q, kp, vp, pt, bufs["masks"], tables, ip,
                                     args, stream, ev)
+    if args.threshold_sweep:
+        res["threshold_sweep"] = threshold_sweep(ca, p, w, q, kp, vp, pt, dense_ms, args,
+                                                 stream, ev)
     if args.chunk_sweep:
         res["chunk_sweep"] = chunk_sweep(ca, stream, ev)
     if not args.no_cpu_baseline:

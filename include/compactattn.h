@@ -139,6 +139,30 @@ ca_status ca_estimate_masks(const ca_problem* p, const uint16_t* q,
                             int32_t k_mean_first_block, float* q_mean, float* k_mean,
                             float* scores, uint64_t* masks, void* stream);
 
+/* 1b. Alpha-threshold selection (the FlashPrefill-style "max-threshold"
+ *    selector the paper pairs with the union, Sec. 4.1; the paper gives no
+ *    formula, so this is a reading).  Per mask row (b,h,i), a cached block j
+ *    is kept when its estimated attention weight relative to the row's best,
+ *    exp(temperature * sm_scale * (s_j - s_max)), is at least alpha:
+ *        s_j >= s_max + margin,  margin = ln(alpha) / (temperature * sm_scale)
+ *    with s = the block scores (ca_block_scores), margin computed in double from the
+ *    single-precision parameters and rounded once to float, and the sum
+ *    s_max + margin taken in float.  Sink, local and chunk-causal bits as in
+ *    ca_select_blocks.  alpha in (0, 1], temperature > 0, sm_scale > 0 (else
+ *    CA_ERR_SHAPE).  ca_estimate_masks_threshold = pooling + scores + this.
+ * ---------------------------------------------------------------------- */
+ca_status ca_select_blocks_threshold(const ca_problem* p, const float* scores, float alpha,
+                                    float temperature, float sm_scale, int32_t sink_blocks,
+                                    int32_t local_blocks, uint64_t* masks, void* stream);
+
+ca_status ca_estimate_masks_threshold(const ca_problem* p, const uint16_t* q,
+                                      const uint16_t* k_pool, const int32_t* page_table,
+                                      float alpha, float temperature, float sm_scale,
+                                      int32_t sink_blocks, int32_t local_blocks,
+                                      int32_t k_mean_first_block, float* q_mean,
+                                      float* k_mean, float* scores, uint64_t* masks,
+                                      void* stream);
+
 /* ------------------------------------------------------------------------
  * 2. Block tables (Sec. 3.2): bitwise OR over the nQB mask rows of every
  *    head of each group, compaction of the set bits j < nKB_b into the CSR

@@ -22,8 +22,14 @@ particular selector; the reading implemented here is:
 When nC_b = 0 there is neither top-k nor local window.  The unscaled dot
 product is used because a positive softmax scale does not change a ranking.
 
+A second selection rule, the alpha-threshold ("max-threshold") reading of
+the FlashPrefill-style selector the paper pairs with the union, keeps every
+cached block whose score is within a margin of the row's best (see
+``select_threshold_blocks``).
+
 Parity: pinned (closed-form pooling, brute-force top-k with ties, needle
-recall, popcount bounds) in tests/test_oracle.py.
+recall, popcount bounds; the threshold rule against top-k prefixes and its
+limit cases) in tests/test_oracle.py.
 """
 from __future__ import annotations
 
@@ -125,6 +131,48 @@ def masks_from_scores(scores32: Sequence[np.ndarray], n_cached: Sequence[int],
                 sel = set(select_top_blocks(scores32[b][h, i], k).tolist()) if k else set()
                 sel |= set(range(min(params.sink_blocks, nc)))
                 sel |= set(range(max(0, nc - params.local_blocks), nc))
+                sel |= set(range(nc, nc + ((i + 1) * q_block) // page))
+                for j in sel:
+                    masks[b, h, i, j >> 6] |= np.uint64(1) << np.uint64(j & 63)
+    return masks
+
+
+def threshold_margin(alpha: float, temperature: float, sm_scale: float) -> np.float32:
+    """The score margin of the alpha-threshold selector (a reading, below):
+    ln(alpha) / (temperature * sm_scale) from the single-precision values of
+    the three parameters, evaluated in double and rounded once to float32."""
+    a, t, s = (float(np.float32(x)) for x in (alpha, temperature, sm_scale))
+    return np.float32(math.log(a) / (t * s))
+
+
+def select_threshold_blocks(scores_row: np.ndarray, margin: np.float32) -> np.ndarray:
+    """Max-threshold selection (FlashPrefill-style, Sec. 4.1; the paper gives no
+    formula, so this is a reading): keep block j when its estimated attention
+    weight exp(temperature * sm_scale * (s_j - s_max)) is at least alpha, i.e.
+    s_j >= s_max + margin with margin = ln(alpha) / (temperature * sm_scale).
+    The sum s_max + margin is taken in float32, the precision the GPU scores
+    are produced in, so both sides take the same decision."""
+    s = np.asarray(scores_row, dtype=np.float32)
+    if s.shape[0] == 0:
+        return np.zeros(0, dtype=np.int64)
+    thr = np.float32(s.max() + np.float32(margin))
+    return np.nonzero(s >= thr)[0]
+
+
+def masks_from_threshold(scores32: Sequence[np.ndarray], n_cached: Sequence[int],
+                         page: int, q_block: int, words: int, margin: np.float32,
+                         sink_blocks: int = 1, local_blocks: int = 4) -> np.ndarray:
+    """Like masks_from_scores, with the threshold selection of the cached blocks."""
+    B = len(scores32)
+    Hq, nqb = scores32[0].shape[:2]
+    masks = np.zeros((B, Hq, nqb, words), dtype=np.uint64)
+    for b in range(B):
+        nc = int(n_cached[b])
+        for h in range(Hq):
+            for i in range(nqb):
+                sel = set(select_threshold_blocks(scores32[b][h, i][:nc], margin).tolist())
+                sel |= set(range(min(sink_blocks, nc)))
+                sel |= set(range(max(0, nc - local_blocks), nc))
                 sel |= set(range(nc, nc + ((i + 1) * q_block) // page))
                 for j in sel:
                     masks[b, h, i, j >> 6] |= np.uint64(1) << np.uint64(j & 63)

@@ -27,6 +27,7 @@ EXPORTED = (
     "ca_dense_paged_chunk_attention", "ca_validate_tables",
     "ca_block_sparse_tables_workspace_bytes", "ca_build_block_sparse_tables",
     "ca_block_sparse_chunk_attention", "ca_gather_selected_pages", "ca_packed_chunk_attention",
+    "ca_select_blocks_threshold", "ca_estimate_masks_threshold",
 )
 
 
@@ -87,6 +88,9 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
         "ca_dense_paged_chunk_attention": ([P, vp, vp, vp, vp, f32, i32, vp, vp, vp, sz, vp],
                                            ctypes.c_int),
         "ca_validate_tables": ([P, i32, vp, vp, i32, vp], ctypes.c_int),
+        "ca_select_blocks_threshold": ([P, vp, f32, f32, f32, i32, i32, vp, vp], ctypes.c_int),
+        "ca_estimate_masks_threshold": ([P, vp, vp, vp, f32, f32, f32, i32, i32, i32, vp, vp, vp,
+                                         vp, vp], ctypes.c_int),
         "ca_block_sparse_tables_workspace_bytes": ([P, i32], sz),
         "ca_build_block_sparse_tables": ([P, vp, i32, vp, vp, vp, sz, vp], ctypes.c_int),
         "ca_block_sparse_chunk_attention": ([P, vp, vp, vp, vp, vp, vp, f32, i32, vp, vp, vp,
@@ -248,6 +252,49 @@ def estimate_masks(p: Problem, q: torch.Tensor, k_pool: torch.Tensor, page_table
                                     _ptr(b["q_mean"]), _ptr(b["k_mean"]), _ptr(b["scores"]),
                                     _ptr(b["masks"]), _stream(stream)))
     return b["masks"], b
+
+
+def estimate_masks_threshold(p: Problem, q: torch.Tensor, k_pool: torch.Tensor,
+                             page_table: torch.Tensor, alpha: float, temperature: float,
+                             sm_scale: float, sink_blocks: int = 1, local_blocks: int = 4,
+                             k_mean: Optional[torch.Tensor] = None, k_mean_first_block: int = 0,
+                             bufs: Optional[dict] = None, stream=None):
+    """Alpha-threshold selector: (masks, buffers) like estimate_masks."""
+    dev = q.device
+    b = bufs if bufs is not None else {}
+    if "q_mean" not in b:
+        b["q_mean"] = torch.empty((p.batch, p.num_q_heads, p.n_qblocks, p.head_dim),
+                                  dtype=torch.float32, device=dev)
+    if k_mean is not None:
+        b["k_mean"] = k_mean
+    elif "k_mean" not in b:
+        b["k_mean"] = torch.zeros((p.batch, p.num_kv_heads, p.max_kv_blocks, p.head_dim),
+                                  dtype=torch.float32, device=dev)
+    if "scores" not in b:
+        b["scores"] = torch.empty((p.batch, p.num_q_heads, p.n_qblocks, p.max_kv_blocks),
+                                  dtype=torch.float32, device=dev)
+    if "masks" not in b:
+        b["masks"] = torch.empty((p.batch, p.num_q_heads, p.n_qblocks, p.words),
+                                 dtype=torch.int64, device=dev)
+    _check(load().ca_estimate_masks_threshold(p.ref, _ptr(q), _ptr(k_pool), _ptr(page_table),
+                                              alpha, temperature, sm_scale, sink_blocks,
+                                              local_blocks, k_mean_first_block,
+                                              _ptr(b["q_mean"]), _ptr(b["k_mean"]),
+                                              _ptr(b["scores"]), _ptr(b["masks"]),
+                                              _stream(stream)))
+    return b["masks"], b
+
+
+def select_blocks_threshold(p: Problem, scores: torch.Tensor, alpha: float, temperature: float,
+                            sm_scale: float, sink_blocks: int = 1, local_blocks: int = 4,
+                            masks: Optional[torch.Tensor] = None, stream=None):
+    if masks is None:
+        masks = torch.empty((p.batch, p.num_q_heads, p.n_qblocks, p.words), dtype=torch.int64,
+                            device=scores.device)
+    _check(load().ca_select_blocks_threshold(p.ref, _ptr(scores), alpha, temperature, sm_scale,
+                                             sink_blocks, local_blocks, _ptr(masks),
+                                             _stream(stream)))
+    return masks
 
 
 def tables_workspace_bytes(p: Problem, group_size: int) -> int:

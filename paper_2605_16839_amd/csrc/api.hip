@@ -2,6 +2,7 @@
 // The meaning of every entry point is documented in include/compactattn.h.
 #include <hip/hip_runtime.h>
 
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <string>
@@ -265,12 +266,66 @@ ca_status ca_estimate_masks(const ca_problem* p, const uint16_t* q, const uint16
                             const int32_t* page_table, float top_frac, int32_t sink_blocks,
                             int32_t local_blocks, int32_t k_mean_first_block, float* q_mean,
                             float* k_mean, float* scores, uint64_t* masks, void* stream) {
+  // the selection parameters are checked before the first stage is enqueued
+  if (!(top_frac >= 0.f && top_frac <= 1.f))
+    return fail(CA_ERR_SHAPE, "top_frac must be in [0, 1]");
+  if (sink_blocks < 0 || local_blocks < 0)
+    return fail(CA_ERR_SHAPE, "sink_blocks and local_blocks must be >= 0");
+  if (!masks) return fail(CA_ERR_NULL, "masks is required");
   ca_status s = ca_pool_q_blocks(p, q, q_mean, stream);
   if (s != CA_OK) return s;
   if ((s = ca_pool_k_blocks(p, k_pool, page_table, k_mean_first_block, k_mean, stream)) != CA_OK)
     return s;
   if ((s = ca_block_scores(p, q_mean, k_mean, scores, stream)) != CA_OK) return s;
   return ca_select_blocks(p, scores, top_frac, sink_blocks, local_blocks, masks, stream);
+}
+
+static ca_status check_threshold(float alpha, float temperature, float sm_scale,
+                                 int32_t sink_blocks, int32_t local_blocks) {
+  if (!(alpha > 0.f && alpha <= 1.f))
+    return fail(CA_ERR_SHAPE, "alpha must be in (0, 1], got %g", (double)alpha);
+  if (!(temperature > 0.f) || !(sm_scale > 0.f))
+    return fail(CA_ERR_SHAPE, "temperature and sm_scale must be > 0");
+  if (sink_blocks < 0 || local_blocks < 0)
+    return fail(CA_ERR_SHAPE, "sink_blocks and local_blocks must be >= 0");
+  return CA_OK;
+}
+
+ca_status ca_select_blocks_threshold(const ca_problem* p, const float* scores, float alpha,
+                                    float temperature, float sm_scale, int32_t sink_blocks,
+                                    int32_t local_blocks, uint64_t* masks, void* stream) {
+  ca::Dims d;
+  ca_status s = check(p, 0, &d);
+  if (s != CA_OK) return s;
+  if ((s = need_device(p)) != CA_OK) return s;
+  if (!scores || !masks) return fail(CA_ERR_NULL, "scores and masks are required");
+  if ((s = check_threshold(alpha, temperature, sm_scale, sink_blocks, local_blocks)) != CA_OK)
+    return s;
+  // margin = ln(alpha) / (temperature * sm_scale), rounded once to fp32
+  const float margin = (float)(std::log((double)alpha) / ((double)temperature * sm_scale));
+  return hip_status(ca::launch_threshold_select(d, scores, p->cached_len, margin, sink_blocks,
+                                                local_blocks, masks,
+                                                static_cast<hipStream_t>(stream)),
+                    "threshold select launch");
+}
+
+ca_status ca_estimate_masks_threshold(const ca_problem* p, const uint16_t* q,
+                                      const uint16_t* k_pool, const int32_t* page_table,
+                                      float alpha, float temperature, float sm_scale,
+                                      int32_t sink_blocks, int32_t local_blocks,
+                                      int32_t k_mean_first_block, float* q_mean, float* k_mean,
+                                      float* scores, uint64_t* masks, void* stream) {
+  // the selection parameters are checked before the first stage is enqueued
+  ca_status s = check_threshold(alpha, temperature, sm_scale, sink_blocks, local_blocks);
+  if (s != CA_OK) return s;
+  if (!masks) return fail(CA_ERR_NULL, "masks is required");
+  s = ca_pool_q_blocks(p, q, q_mean, stream);
+  if (s != CA_OK) return s;
+  if ((s = ca_pool_k_blocks(p, k_pool, page_table, k_mean_first_block, k_mean, stream)) != CA_OK)
+    return s;
+  if ((s = ca_block_scores(p, q_mean, k_mean, scores, stream)) != CA_OK) return s;
+  return ca_select_blocks_threshold(p, scores, alpha, temperature, sm_scale, sink_blocks,
+                                    local_blocks, masks, stream);
 }
 
 size_t ca_tables_workspace_bytes(const ca_problem* p, int32_t group_size) {

@@ -270,6 +270,47 @@ __global__ __launch_bounds__(256) void select_kernel(const float* __restrict__ s
 }
 
 // ---------------------------------------------------------------------------
+// Threshold selection (the alpha / max-threshold reading): one workgroup per
+// mask row keeps every cached block with s_j >= s_max + margin (the sum in
+// fp32), plus the same sink, local and chunk-causal bits as select_kernel.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void threshold_select_kernel(
+    const float* __restrict__ scores, const int32_t* __restrict__ cached_len,
+    uint64_t* __restrict__ masks, int Hq, int nqb, int max_kv_blocks, int W, int chunk_blocks,
+    int qblock_blocks, float margin, int sink_blocks, int local_blocks) {
+  __shared__ float red[4];
+  const int row = blockIdx.x;
+  const int t = threadIdx.x;
+  const int wv = t >> 6;
+  const int i = row % nqb;
+  const int b = row / (nqb * Hq);
+  const int nc = cached_len[b] / kPage;
+  const int nkb = nc + chunk_blocks;
+  const float* s = scores + (size_t)row * max_kv_blocks;
+  float mx = -INFINITY;
+  for (int j = t; j < nc; j += 256) mx = fmaxf(mx, s[j]);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, kWave));
+  if (lane_id() == 0) red[wv] = mx;
+  __syncthreads();
+  mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  const float thr = mx + margin;
+  const int causal_end = nc + (i + 1) * qblock_blocks;
+  const int sink_end = sink_blocks < nc ? sink_blocks : nc;
+  const int local_begin = nc - local_blocks;
+  uint64_t* mrow = masks + (size_t)row * W;
+  for (int base = 0; base < W * 64; base += 256) {
+    const int j = base + t;
+    const bool sel = j < nc && s[j] >= thr;
+    const bool forced = j < nkb && ((j < sink_end) || (j >= local_begin && j < nc) ||
+                                    (j >= nc && j < causal_end));
+    const uint64_t word = __ballot(sel || forced);
+    const int widx = j >> 6;
+    if (lane_id() == 0 && widx < W) mrow[widx] = word;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // launchers
 // ---------------------------------------------------------------------------
 hipError_t launch_pool_q(const Dims& d, const uint16_t* q, float* q_mean, hipStream_t st) {
@@ -323,6 +364,18 @@ hipError_t launch_select(const Dims& d, const float* scores, const int32_t* cach
   select_kernel<<<grid, 256, lds, st>>>(scores, cached_len, masks, d.Hq, d.nqb,
                                         d.max_kv_blocks, d.W, d.chunk_blocks,
                                         d.q_block / kPage, top_frac, sink_blocks, local_blocks);
+  return hipGetLastError();
+}
+
+
+hipError_t launch_threshold_select(const Dims& d, const float* scores, const int32_t* cached_len,
+                                   float margin, int sink_blocks, int local_blocks,
+                                   uint64_t* masks, hipStream_t st) {
+  dim3 grid(d.B * d.Hq * d.nqb);
+  threshold_select_kernel<<<grid, 256, 0, st>>>(scores, cached_len, masks, d.Hq, d.nqb,
+                                                d.max_kv_blocks, d.W, d.chunk_blocks,
+                                                d.q_block / kPage, margin, sink_blocks,
+                                                local_blocks);
   return hipGetLastError();
 }
 

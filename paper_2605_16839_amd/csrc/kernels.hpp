@@ -25,6 +25,9 @@ hipError_t launch_select(const Dims& d, const float* scores, const int32_t* cach
                          float top_frac, int sink_blocks, int local_blocks, uint64_t* masks,
                          hipStream_t st);
 hipError_t raise_select_lds(int bytes);
+hipError_t launch_threshold_select(const Dims& d, const float* scores, const int32_t* cached_len,
+                                   float margin, int sink_blocks, int local_blocks,
+                                   uint64_t* masks, hipStream_t st);
 
 size_t tables_ws_bytes(const Dims& d, int group_size);
 hipError_t launch_tables(const Dims& d, const uint64_t* masks, const int32_t* cached_len,

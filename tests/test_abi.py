@@ -124,3 +124,22 @@ def test_arm_validation(lib):
     assert lib.ca_status_string(s).decode() == "CA_ERR_SHAPE"     # beyond B*G*max_kv_blocks
     s = lib.ca_gather_selected_pages(p.ref, fake, fake, fake, fake, fake, 3, fake, fake, 10, None)
     assert lib.ca_status_string(s).decode() == "CA_ERR_GROUP"
+
+
+def test_threshold_validation(lib):
+    """Threshold parameters are rejected on the host before any stage is enqueued
+    (fake device pointers, never dereferenced)."""
+    fake = ctypes.c_void_p(0x1000)
+    p = _prob()
+    p.c.cached_len = fake.value
+    cases = [(0.0, 16.0, 0.1, 1, 4), (1.5, 16.0, 0.1, 1, 4), (float("nan"), 16.0, 0.1, 1, 4),
+             (0.1, 0.0, 0.1, 1, 4), (0.1, 16.0, -0.1, 1, 4), (0.1, 16.0, 0.1, -1, 4)]
+    for a, t, sm, sink, local in cases:
+        s = lib.ca_select_blocks_threshold(p.ref, fake, a, t, sm, sink, local, fake, None)
+        assert lib.ca_status_string(s).decode() == "CA_ERR_SHAPE", (a, t, sm, sink, local)
+        s = lib.ca_estimate_masks_threshold(p.ref, fake, fake, fake, a, t, sm, sink, local, 0,
+                                            fake, fake, fake, fake, None)
+        assert lib.ca_status_string(s).decode() == "CA_ERR_SHAPE", (a, t, sm, sink, local)
+    s = lib.ca_estimate_masks(p.ref, fake, fake, fake, 1.5, 1, 4, 0, fake, fake, fake, fake,
+                              None)
+    assert lib.ca_status_string(s).decode() == "CA_ERR_SHAPE"

@@ -193,6 +193,68 @@ def test_select_tied_scores_bitexact(nc_list, top_frac, sink, local):
     assert np.array_equal(u64_host(got), ref)
 
 
+@pytest.mark.parametrize("nc_list,alpha,tau", [
+    ([16], 0.06, 16.0), ([0, 33, 130], 0.5, 1.0), ([2016], 1.0, 1.0), ([480, 64], 0.01, 4.0),
+])
+def test_threshold_select_bitexact(nc_list, alpha, tau):
+    """Alpha-threshold selection on generated float32 scores (ties, signed zeros)."""
+    B, Hq, Hkv, C, qb = len(nc_list), 4, 1, 256, 128
+    maxkb = max(nc_list) + C // 64
+    p = ca.Problem(B, Hq, Hkv, 64, qb, C, maxkb, [64 * n for n in nc_list])
+    nqb = C // qb
+    sm = 0.125
+    scores = np.full((B, Hq, nqb, maxkb), np.nan, dtype=np.float32)
+    per_b = []
+    for b, nc in enumerate(nc_list):
+        s = synth.tied_scores(11 * b + nc, Hq * nqb, max(nc, 1), n_distinct=7)[:, :nc]
+        s = s.reshape(Hq, nqb, nc)
+        scores[b, :, :, :nc] = s
+        per_b.append(s)
+    margin = oracle.threshold_margin(alpha, tau, sm)
+    ref = oracle.masks_from_threshold(per_b, nc_list, 64, qb, p.words, margin, 1, 4)
+    got = ca.select_blocks_threshold(p, torch.from_numpy(scores).cuda(), alpha, tau, sm)
+    torch.cuda.synchronize()
+    assert np.array_equal(u64_host(got), ref)
+
+
+@pytest.mark.parametrize("name,alpha,tau", [("llama8b_32k", 0.03, 16.0),
+                                            ("llama8b_128k_final", 0.06, 16.0)])
+def test_threshold_estimator_end_to_end(name, alpha, tau, workload_inputs, oracle_estimate):
+    """GPU threshold masks vs the oracle's on fp64 scores: only blocks whose fp64
+    score lies within 1e-5 of the row's threshold may differ; needles are kept."""
+    d = workload_inputs(name)
+    w = d["workload"]
+    p = _problem(w)
+    x = device_inputs(d)
+    _, parts = oracle_estimate(name)
+    got, _ = ca.estimate_masks_threshold(p, x["q"], x["k"], x["pt"], alpha, tau, w.sm_scale,
+                                         w.sink_blocks, w.local_blocks)
+    torch.cuda.synchronize()
+    margin = oracle.threshold_margin(alpha, tau, w.sm_scale)
+    s32 = [np.asarray(sb, dtype=np.float32) for sb in parts["scores"]]
+    ref = oracle.masks_from_threshold(s32, [w.n_cached_blocks(b) for b in range(w.batch)],
+                                      w.page_size, w.q_block, w.words, margin, w.sink_blocks,
+                                      w.local_blocks)
+    gb, rb = oracle.unpack_masks(u64_host(got)), oracle.unpack_masks(ref)
+    flips = 0
+    for b in range(w.batch):
+        nc = w.n_cached_blocks(b)
+        for h in range(w.num_q_heads):
+            for i in range(w.n_qblocks):
+                diff = np.nonzero(gb[b, h, i] != rb[b, h, i])[0]
+                if diff.size == 0:
+                    continue
+                flips += 1
+                assert diff.max() < nc, "a forced bit differs"
+                s64 = parts["scores"][b][h, i][:nc]
+                thr = s64.max() + float(margin)
+                assert np.all(np.abs(s64[diff] - thr) <= 1e-5), (b, h, i, diff)
+    bits = gb
+    assert all(bits[b, h, i, j] for (b, kvh, j, h, i) in d["needles"])
+    print(f"{name}: {flips} near-threshold rows differ, density "
+          f"{gb[..., :w.n_cached_blocks(0)].mean():.4f}")
+
+
 def _near_tie_check(gpu_masks, ref_masks, scores64, w, tol):
     """Rows may differ only where the fp64 scores of swapped blocks tie within tol."""
     gb, rb = oracle.unpack_masks(gpu_masks), oracle.unpack_masks(ref_masks)

@@ -397,3 +397,59 @@ def test_estimator_recall_and_popcount(oracle_estimate, workload_inputs):
             assert not stair[:, (i + 1) * w.q_block // w.page_size:].any()
         dens = oracle.union_densities(masks, w.group_size, [nc])
         assert dens["pre_union"] <= dens["q_union"] <= dens["group_union"]
+
+
+# ---------------------------------------------------------------------------
+# alpha-threshold selector (a reading; see oracle/estimator.py)
+# ---------------------------------------------------------------------------
+def test_threshold_selection_is_a_topk_prefix():
+    """With distinct scores the kept set is the top-m set for m = its size, so it
+    must equal the independent top-k selection at that k; it grows as the
+    margin falls, keeps the maximum, and the limits are argmax / everything."""
+    rng = np.random.default_rng(21)
+    for n in (1, 2, 17, 64, 300):
+        s = rng.standard_normal(n).astype(np.float32)
+        s[rng.integers(n)] = s.max() + np.float32(1.0)         # a clear maximum
+        prev = None
+        for margin in (0.0, -0.01, -0.3, -1.0, -3.0, -np.inf):
+            kept = oracle.select_threshold_blocks(s, np.float32(margin))
+            assert s.argmax() in kept
+            assert np.array_equal(kept, oracle.select_top_blocks(s, len(kept)))
+            if prev is not None:
+                assert set(prev) <= set(kept.tolist())
+            prev = kept.tolist()
+        assert prev == list(range(n))                          # -inf keeps every block
+        assert oracle.select_threshold_blocks(s, np.float32(0.0)).tolist() == [int(s.argmax())]
+    ties = np.array([1.0, 3.0, 3.0, -0.0, 0.0], dtype=np.float32)
+    assert oracle.select_threshold_blocks(ties, np.float32(0.0)).tolist() == [1, 2]
+    assert oracle.select_threshold_blocks(ties, np.float32(-3.0)).tolist() == [0, 1, 2, 3, 4]
+
+
+def test_threshold_margin_matches_alpha_weight():
+    """exp(temperature * sm_scale * margin) recovers alpha (the reading's definition)."""
+    for alpha in (0.01, 0.06, 0.5):
+        for tau in (1.0, 16.0):
+            m = oracle.threshold_margin(alpha, tau, 1.0 / math.sqrt(128.0))
+            assert m <= 0
+            assert abs(math.exp(tau * float(m) / math.sqrt(128.0)) - alpha) < 1e-5 * alpha
+
+
+
+def test_threshold_kept_blocks_are_the_alpha_heavy_softmax_blocks():
+    """Through the softmax of the sharpened block scores (scipy), a block passes
+    when its probability is at least alpha times the largest one; checked on
+    every block not within 1e-4 (relative) of the cut."""
+    from scipy.special import softmax
+    rng = np.random.default_rng(23)
+    sm = 1.0 / math.sqrt(128.0)
+    for alpha, tau in ((0.01, 16.0), (0.06, 16.0), (0.3, 4.0), (0.9, 1.0)):
+        s = (rng.standard_normal(500) * 3.0).astype(np.float32)
+        kept = set(oracle.select_threshold_blocks(
+            s, oracle.threshold_margin(alpha, tau, sm)).tolist())
+        prob = softmax(tau * sm * s.astype(np.float64))
+        ratio = prob / prob.max()
+        clear = np.abs(ratio - alpha) > 1e-4 * alpha
+        assert clear.sum() > 450
+        want = set(np.nonzero((ratio >= alpha) & clear)[0].tolist())
+        assert {j for j in kept if clear[j]} == want
+        assert 0 < len(want) < 500
