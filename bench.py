@@ -277,15 +277,18 @@ def chunk_sweep(ca, stream, ev):
                              dtype=torch.float32, device=dev)
         cb = C // base.page_size
         ebufs = {}                      # estimator buffers reused across the chunks
-        sums = {"estimate": 0.0, "tables": 0.0, "attention": 0.0, "dense": 0.0}
+        sums = {"estimate": 0.0, "tables": 0.0, "attention": 0.0, "dense": 0.0,
+                "fused_estimate_tables": 0.0}
+        fbufs = {}
         final = {}
         for c in range(-1, n):          # c = -1: untimed warm-up on chunk 0
             d = seq.inputs(max(c, 0))
             w = d["workload"]
             p = ca.Problem.from_workload(w, device=dev)
             q, pt = bf(d["q"]), torch.from_numpy(d["page_table"]).to(dev)
-            m = [ev() for _ in range(6)]
+            m = [ev() for _ in range(8)]
             torch.cuda.synchronize()
+            host_ahead(torch)
             m[0].record(stream)
             masks, _ = ca.estimate_masks(p, q, kd, pt, w.top_frac, w.sink_blocks,
                                          w.local_blocks, k_mean=k_mean,
@@ -298,18 +301,26 @@ def chunk_sweep(ca, stream, ev):
             m[4].record(stream)
             ca.dense_paged_chunk_attention(p, q, (kd, vd), pt, w.sm_scale)
             m[5].record(stream)
+            m[6].record(stream)
+            ca.estimate_tables(p, q, kd, pt, w.top_frac, w.group_size, w.sink_blocks,
+                               w.local_blocks, k_mean=k_mean,
+                               k_mean_first_block=max(c, 0) * cb, bufs=fbufs)
+            m[7].record(stream)
             torch.cuda.synchronize()
             if c < 0:
                 continue
             t = {"estimate": m[0].elapsed_time(m[1]), "tables": m[1].elapsed_time(m[2]),
-                 "attention": m[2].elapsed_time(m[3]), "dense": m[4].elapsed_time(m[5])}
+                 "attention": m[2].elapsed_time(m[3]), "dense": m[4].elapsed_time(m[5]),
+                 "fused_estimate_tables": m[6].elapsed_time(m[7])}
             for k in sums:
                 sums[k] += t[k]
             if c == n - 1:
                 final = {k: round(v, 4) for k, v in t.items()}
         sel = sums["estimate"] + sums["tables"] + sums["attention"]
+        sel_fused = sums["fused_estimate_tables"] + sums["attention"]
         res[str(C)] = {"chunks": n, "cumulative_ms": {k: round(v, 3) for k, v in sums.items()},
                        "cumulative_speedup_vs_dense": round(sums["dense"] / sel, 3),
+                       "cumulative_speedup_vs_dense_fused": round(sums["dense"] / sel_fused, 3),
                        "final_chunk_ms": final,
                        "final_chunk_speedup_vs_dense": round(
                            final["dense"] / (final["estimate"] + final["tables"]
@@ -317,6 +328,13 @@ def chunk_sweep(ca, stream, ev):
         del kd, vd, seq
         torch.cuda.empty_cache()
     return res
+
+
+def host_ahead(torch):
+    """Queue a short GPU spin so that the launches recorded after it are all
+    enqueued before the GPU reaches them: stage timings between events then
+    measure GPU time, not the host's launch overhead."""
+    torch.cuda._sleep(1_000_000)
 
 
 THRESHOLD_POINTS = ((16.0, 0.01), (16.0, 0.03), (16.0, 0.06), (16.0, 0.1), (8.0, 0.06))
@@ -443,10 +461,47 @@ def main():
     torch.cuda.synchronize()
     ms_per_step = start.elapsed_time(stop) / args.steps
 
+    # ---- fused estimator -> union path (no per-row masks), whole step ----
+    fbufs = {}
+    ftables = (torch.empty(R + 1, dtype=torch.int32, device=dev),
+               torch.empty(R * w.max_kv_blocks, dtype=torch.int32, device=dev))
+
+    def step_fused(marks=None):
+        if marks:
+            marks[0].record(stream)
+        ca.estimate_tables(p, q, kp, pt, w.top_frac, gs, w.sink_blocks, w.local_blocks,
+                           bufs=fbufs, out=ftables, ws=tws)
+        if marks:
+            marks[1].record(stream)
+        ca.chunk_attention(p, q, (kp, vp), pt, ftables, gs, w.sm_scale, num_splits=0, out=out,
+                           lse=lse, ws=aws)
+        if marks:
+            marks[2].record(stream)
+
+    for _ in range(args.warmup):
+        step_fused()
+    torch.cuda.synchronize()
+    f0, f1 = ev(), ev()
+    f0.record(stream)
+    for _ in range(args.steps):
+        step_fused()
+    f1.record(stream)
+    torch.cuda.synchronize()
+    fused_ms = f0.elapsed_time(f1) / args.steps
+    fst = []
+    for _ in range(args.steps):
+        m = [ev() for _ in range(3)]
+        host_ahead(torch)
+        step_fused(m)
+        torch.cuda.synchronize()
+        fst.append(m[0].elapsed_time(m[1]))
+    fused_est_ms = float(np.median(fst))
+
     # ---- per-stage split (separate pass with events between stages) ----
     stage = {"estimate": [], "tables": [], "attention": []}
     for _ in range(args.steps):
         m = [ev() for _ in range(4)]
+        host_ahead(torch)
         step(m)
         torch.cuda.synchronize()
         stage["estimate"].append(m[0].elapsed_time(m[1]))
@@ -511,6 +566,8 @@ def main():
                    "cached_tokens": list(w.cached_lens), "chunk_len": w.chunk_len,
                    "top_frac": w.top_frac, "rho": w.rho, "group_size": gs},
         "stage_ms": {k: round(v, 4) for k, v in st_ms.items()},
+        "fused_step_ms": round(fused_ms, 4),
+        "fused_estimate_tables_ms": round(fused_est_ms, 4),
         "dense_ms": round(dense_ms, 4),
         "speedup_vs_dense": round(dense_ms / ms_per_step, 3),
         "speedup_vs_dense_kernel_only": round(dense_ms / attn_ms, 3),

@@ -177,6 +177,27 @@ ca_status ca_build_block_tables(const ca_problem* p, const uint64_t* masks,
                                 int32_t* kv_indices, void* ws, size_t ws_bytes,
                                 void* stream);
 
+/* 2b. Fused estimator-to-union (Sec. 3.2: the selected blocks of every head
+ *    and Q-block of a group only matter through their union): the four
+ *    estimator stages of ca_estimate_masks, except that each selection row
+ *    is ORed straight into the words of its (b, group) table row instead of
+ *    being stored as a mask, then the words are compacted into the CSR pair.
+ *    The tables are bit-identical to ca_build_block_tables(group_size) of
+ *    the masks ca_estimate_masks produces from the same inputs; no per-row
+ *    mask is written.  q_mean, k_mean and scores are written as by
+ *    ca_estimate_masks (k_mean_first_block likewise).
+ *    Workspace: at least B * (Hq / group_size) * W * 8 bytes of device memory,
+ *    8-byte aligned (ca_tables_workspace_bytes(p, group_size) is enough);
+ *    its contents on entry are irrelevant (it is cleared by the first
+ *    stage).  Errors: CA_ERR_GROUP, CA_ERR_NULL, CA_ERR_SHAPE (top_frac,
+ *    sink/local, first_block), CA_ERR_WORKSPACE, all before any launch. */
+ca_status ca_estimate_tables(const ca_problem* p, const uint16_t* q, const uint16_t* k_pool,
+                             const int32_t* page_table, float top_frac, int32_t sink_blocks,
+                             int32_t local_blocks, int32_t k_mean_first_block,
+                             int32_t group_size, float* q_mean, float* k_mean, float* scores,
+                             int32_t* kv_indptr, int32_t* kv_indices, void* ws,
+                             size_t ws_bytes, void* stream);
+
 /* ------------------------------------------------------------------------
  * 3. Chunk attention over the tables (Sec. 3.3, App. B.2).
  *    q bf16 [B, C, Hq, D]; out bf16 [B, C, Hq, D]; lse fp32 [B, Hq, C]

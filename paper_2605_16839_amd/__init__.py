@@ -9,6 +9,7 @@ from .binding import (  # noqa: F401
     build_block_tables, attention_workspace_bytes, chunk_attention,
     dense_paged_chunk_attention, validate_tables, block_sparse_tables_workspace_bytes,
     build_block_sparse_tables, block_sparse_chunk_attention, gather_selected_pages,
-    packed_chunk_attention, estimate_masks_threshold, select_blocks_threshold, EXPORTED,
+    packed_chunk_attention, estimate_masks_threshold, select_blocks_threshold, estimate_tables,
+    EXPORTED,
     LIB_PATH,
 )

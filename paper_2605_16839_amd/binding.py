@@ -27,7 +27,7 @@ EXPORTED = (
     "ca_dense_paged_chunk_attention", "ca_validate_tables",
     "ca_block_sparse_tables_workspace_bytes", "ca_build_block_sparse_tables",
     "ca_block_sparse_chunk_attention", "ca_gather_selected_pages", "ca_packed_chunk_attention",
-    "ca_select_blocks_threshold", "ca_estimate_masks_threshold",
+    "ca_select_blocks_threshold", "ca_estimate_masks_threshold", "ca_estimate_tables",
 )
 
 
@@ -91,6 +91,8 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
         "ca_select_blocks_threshold": ([P, vp, f32, f32, f32, i32, i32, vp, vp], ctypes.c_int),
         "ca_estimate_masks_threshold": ([P, vp, vp, vp, f32, f32, f32, i32, i32, i32, vp, vp, vp,
                                          vp, vp], ctypes.c_int),
+        "ca_estimate_tables": ([P, vp, vp, vp, f32, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp,
+                                sz, vp], ctypes.c_int),
         "ca_block_sparse_tables_workspace_bytes": ([P, i32], sz),
         "ca_build_block_sparse_tables": ([P, vp, i32, vp, vp, vp, sz, vp], ctypes.c_int),
         "ca_block_sparse_chunk_attention": ([P, vp, vp, vp, vp, vp, vp, f32, i32, vp, vp, vp,
@@ -317,6 +319,41 @@ def build_block_tables(p: Problem, masks: torch.Tensor, group_size: int,
                                         _ptr(out[1]), _ptr(ws), ws.numel() * ws.element_size(),
                                         _stream(stream)))
     return out
+
+
+def estimate_tables(p: Problem, q: torch.Tensor, k_pool: torch.Tensor, page_table: torch.Tensor,
+                    top_frac: float, group_size: int, sink_blocks: int = 1,
+                    local_blocks: int = 4, k_mean: Optional[torch.Tensor] = None,
+                    k_mean_first_block: int = 0, bufs: Optional[dict] = None,
+                    out: Optional[Tuple[torch.Tensor, torch.Tensor]] = None,
+                    ws: Optional[torch.Tensor] = None, stream=None):
+    """Fused estimator -> union -> CSR: returns (tables, buffers); no masks."""
+    dev = q.device
+    b = bufs if bufs is not None else {}
+    if "q_mean" not in b:
+        b["q_mean"] = torch.empty((p.batch, p.num_q_heads, p.n_qblocks, p.head_dim),
+                                  dtype=torch.float32, device=dev)
+    if k_mean is not None:
+        b["k_mean"] = k_mean
+    elif "k_mean" not in b:
+        b["k_mean"] = torch.zeros((p.batch, p.num_kv_heads, p.max_kv_blocks, p.head_dim),
+                                  dtype=torch.float32, device=dev)
+    if "scores" not in b:
+        b["scores"] = torch.empty((p.batch, p.num_q_heads, p.n_qblocks, p.max_kv_blocks),
+                                  dtype=torch.float32, device=dev)
+    R = p.batch * p.n_groups(group_size)
+    if out is None:
+        out = (torch.empty(R + 1, dtype=torch.int32, device=dev),
+               torch.empty(R * p.max_kv_blocks, dtype=torch.int32, device=dev))
+    if ws is None:
+        ws = torch.empty(max(tables_workspace_bytes(p, group_size), 8), dtype=torch.uint8,
+                         device=dev)
+    _check(load().ca_estimate_tables(p.ref, _ptr(q), _ptr(k_pool), _ptr(page_table), top_frac,
+                                     sink_blocks, local_blocks, k_mean_first_block, group_size,
+                                     _ptr(b["q_mean"]), _ptr(b["k_mean"]), _ptr(b["scores"]),
+                                     _ptr(out[0]), _ptr(out[1]), _ptr(ws),
+                                     ws.numel() * ws.element_size(), _stream(stream)))
+    return out, b
 
 
 def attention_workspace_bytes(p: Problem, group_size: int, num_splits: int) -> int:

@@ -239,6 +239,17 @@ ca_status ca_block_scores(const ca_problem* p, const float* q_mean, const float*
                     "scores launch");
 }
 
+// The keys of one selection row live in LDS: raise the dynamic LDS cap for
+// long caches.
+static ca_status select_lds_ready(const ca::Dims& d) {
+  const size_t lds = (size_t)(d.max_nc > 0 ? d.max_nc : 1) * sizeof(uint32_t);
+  if (lds > 48 * 1024) {
+    hipError_t e = ca::raise_select_lds((int)lds);
+    if (e != hipSuccess) return hip_status(e, "raise select LDS limit");
+  }
+  return CA_OK;
+}
+
 ca_status ca_select_blocks(const ca_problem* p, const float* scores, float top_frac,
                            int32_t sink_blocks, int32_t local_blocks, uint64_t* masks,
                            void* stream) {
@@ -251,12 +262,7 @@ ca_status ca_select_blocks(const ca_problem* p, const float* scores, float top_f
     return fail(CA_ERR_SHAPE, "top_frac must be in [0, 1]");
   if (sink_blocks < 0 || local_blocks < 0)
     return fail(CA_ERR_SHAPE, "sink_blocks and local_blocks must be >= 0");
-  const size_t lds = (size_t)(d.max_nc > 0 ? d.max_nc : 1) * sizeof(uint32_t);
-  if (lds > 48 * 1024) {
-    // the keys of one row live in LDS; raise the dynamic LDS cap for long caches
-    hipError_t e = ca::raise_select_lds((int)lds);
-    if (e != hipSuccess) return hip_status(e, "raise select LDS limit");
-  }
+  if ((s = select_lds_ready(d)) != CA_OK) return s;
   return hip_status(ca::launch_select(d, scores, p->cached_len, top_frac, sink_blocks,
                                       local_blocks, masks, static_cast<hipStream_t>(stream)),
                     "select launch");
@@ -278,6 +284,47 @@ ca_status ca_estimate_masks(const ca_problem* p, const uint16_t* q, const uint16
     return s;
   if ((s = ca_block_scores(p, q_mean, k_mean, scores, stream)) != CA_OK) return s;
   return ca_select_blocks(p, scores, top_frac, sink_blocks, local_blocks, masks, stream);
+}
+
+ca_status ca_estimate_tables(const ca_problem* p, const uint16_t* q, const uint16_t* k_pool,
+                             const int32_t* page_table, float top_frac, int32_t sink_blocks,
+                             int32_t local_blocks, int32_t k_mean_first_block,
+                             int32_t group_size, float* q_mean, float* k_mean, float* scores,
+                             int32_t* kv_indptr, int32_t* kv_indices, void* ws, size_t ws_bytes,
+                             void* stream) {
+  ca::Dims d;
+  if (group_size < 1) return fail(CA_ERR_GROUP, "group_size must be >= 1");
+  ca_status s = check(p, group_size, &d);
+  if (s != CA_OK) return s;
+  if ((s = need_device(p)) != CA_OK) return s;
+  if (!q || !k_pool || !page_table || !q_mean || !k_mean || !scores || !kv_indptr || !kv_indices)
+    return fail(CA_ERR_NULL,
+                "q, k_pool, page_table, q_mean, k_mean, scores, kv_indptr and kv_indices are "
+                "required");
+  if (!(top_frac >= 0.f && top_frac <= 1.f))
+    return fail(CA_ERR_SHAPE, "top_frac must be in [0, 1]");
+  if (sink_blocks < 0 || local_blocks < 0)
+    return fail(CA_ERR_SHAPE, "sink_blocks and local_blocks must be >= 0");
+  if (k_mean_first_block < 0) return fail(CA_ERR_SHAPE, "first_block must be >= 0");
+  const int rows = d.B * (d.Hq / group_size);
+  const size_t need = (size_t)rows * d.W * sizeof(uint64_t);
+  if (ws == nullptr || ws_bytes < need)
+    return fail(CA_ERR_WORKSPACE, "fused tables need %zu workspace bytes, got %zu", need,
+                ws == nullptr ? (size_t)0 : ws_bytes);
+  if (reinterpret_cast<uintptr_t>(ws) % sizeof(uint64_t) != 0)
+    return fail(CA_ERR_WORKSPACE, "workspace must be 8-byte aligned");
+  if ((s = select_lds_ready(d)) != CA_OK) return s;
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  uint64_t* words = static_cast<uint64_t*>(ws);
+  hipError_t e = ca::launch_pool_q(d, q, q_mean, st, words, (int)((size_t)rows * d.W));
+  if (e == hipSuccess)
+    e = ca::launch_pool_k(d, k_pool, page_table, p->cached_len, k_mean_first_block, k_mean, st);
+  if (e == hipSuccess) e = ca::launch_scores(d, q_mean, k_mean, p->cached_len, scores, st);
+  if (e == hipSuccess)
+    e = ca::launch_select(d, scores, p->cached_len, top_frac, sink_blocks, local_blocks, nullptr,
+                          st, words, group_size);
+  if (e == hipSuccess) e = ca::launch_compact_words(d, rows, words, kv_indptr, kv_indices, st);
+  return hip_status(e, "fused estimate-tables launch");
 }
 
 static ca_status check_threshold(float alpha, float temperature, float sm_scale,

@@ -46,12 +46,18 @@ __device__ __forceinline__ void pool_rows(const uint16_t* __restrict__ base, siz
 }
 
 // One workgroup per (b, h, i): each wave sums a quarter of the Q-block's rows,
-// the four partial sums meet in LDS.
+// the four partial sums meet in LDS.  In the fused estimator-to-union path
+// this first stage also clears the group union words that the selection
+// ORs into (clear_words, n_clear; none otherwise).
 template <int D>
 __global__ __launch_bounds__(256) void pool_q_kernel(const uint16_t* __restrict__ q,
                                                      float* __restrict__ q_mean, int B, int C,
-                                                     int Hq, int q_block, int nqb) {
+                                                     int Hq, int q_block, int nqb,
+                                                     uint64_t* __restrict__ clear_words,
+                                                     int n_clear) {
   __shared__ __attribute__((aligned(16))) float part[4][D];
+  for (int x = blockIdx.x * 256 + threadIdx.x; x < n_clear; x += gridDim.x * 256)
+    clear_words[x] = 0ull;
   const int w = blockIdx.x;
   const int i = w % nqb;
   const int h = (w / nqb) % Hq;
@@ -188,7 +194,9 @@ __global__ __launch_bounds__(256) void select_kernel(const float* __restrict__ s
                                                      int nqb, int max_kv_blocks, int W,
                                                      int chunk_blocks, int qblock_blocks,
                                                      float top_frac, int sink_blocks,
-                                                     int local_blocks) {
+                                                     int local_blocks,
+                                                     unsigned long long* __restrict__ gwords,
+                                                     int group_size) {
   extern __shared__ uint32_t keys[];
   __shared__ int hist[256];
   __shared__ int wave_tot[4];
@@ -244,6 +252,10 @@ __global__ __launch_bounds__(256) void select_kernel(const float* __restrict__ s
   const int local_begin = nc - local_blocks;
   int carry = 0;  // keys equal to T already seen, in block order
   uint64_t* mrow = masks + (size_t)row * W;
+  // fused path: OR the row straight into the words of its group's table row
+  const int h = (row / nqb) % Hq;
+  unsigned long long* grow =
+      gwords ? gwords + ((size_t)b * (Hq / group_size) + h / group_size) * W : nullptr;
   for (int base = 0; base < W * 64; base += 256) {
     const int j = base + t;
     const bool cached = j < nc;
@@ -263,7 +275,10 @@ __global__ __launch_bounds__(256) void select_kernel(const float* __restrict__ s
                                     (j >= nc && j < causal_end));
     const uint64_t word = __ballot(sel || forced);
     const int widx = j >> 6;
-    if (lane_id() == 0 && widx < W) mrow[widx] = word;
+    if (lane_id() == 0 && widx < W) {
+      if (grow == nullptr) mrow[widx] = word;
+      else if (word) atomicOr(grow + widx, (unsigned long long)word);
+    }
     carry += total;
     __syncthreads();
   }
@@ -313,12 +328,15 @@ __global__ __launch_bounds__(256) void threshold_select_kernel(
 // ---------------------------------------------------------------------------
 // launchers
 // ---------------------------------------------------------------------------
-hipError_t launch_pool_q(const Dims& d, const uint16_t* q, float* q_mean, hipStream_t st) {
+hipError_t launch_pool_q(const Dims& d, const uint16_t* q, float* q_mean, hipStream_t st,
+                         uint64_t* clear_words, int n_clear) {
   dim3 grid(d.B * d.Hq * d.nqb);
   if (d.D == 128)
-    pool_q_kernel<128><<<grid, 256, 0, st>>>(q, q_mean, d.B, d.C, d.Hq, d.q_block, d.nqb);
+    pool_q_kernel<128><<<grid, 256, 0, st>>>(q, q_mean, d.B, d.C, d.Hq, d.q_block, d.nqb,
+                                             clear_words, n_clear);
   else
-    pool_q_kernel<64><<<grid, 256, 0, st>>>(q, q_mean, d.B, d.C, d.Hq, d.q_block, d.nqb);
+    pool_q_kernel<64><<<grid, 256, 0, st>>>(q, q_mean, d.B, d.C, d.Hq, d.q_block, d.nqb,
+                                            clear_words, n_clear);
   return hipGetLastError();
 }
 
@@ -358,12 +376,14 @@ hipError_t raise_select_lds(int bytes) {
 
 hipError_t launch_select(const Dims& d, const float* scores, const int32_t* cached_len,
                          float top_frac, int sink_blocks, int local_blocks, uint64_t* masks,
-                         hipStream_t st) {
+                         hipStream_t st, uint64_t* group_words, int group_size) {
   dim3 grid(d.B * d.Hq * d.nqb);
   const size_t lds = (size_t)(d.max_nc > 0 ? d.max_nc : 1) * sizeof(uint32_t);
   select_kernel<<<grid, 256, lds, st>>>(scores, cached_len, masks, d.Hq, d.nqb,
                                         d.max_kv_blocks, d.W, d.chunk_blocks,
-                                        d.q_block / kPage, top_frac, sink_blocks, local_blocks);
+                                        d.q_block / kPage, top_frac, sink_blocks, local_blocks,
+                                        reinterpret_cast<unsigned long long*>(group_words),
+                                        group_size);
   return hipGetLastError();
 }
 

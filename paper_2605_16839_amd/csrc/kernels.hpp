@@ -15,15 +15,18 @@ struct Dims {
   int max_nkb;       // max_b cached + chunk blocks
 };
 
-hipError_t launch_pool_q(const Dims& d, const uint16_t* q, float* q_mean, hipStream_t st);
+hipError_t launch_pool_q(const Dims& d, const uint16_t* q, float* q_mean, hipStream_t st,
+                         uint64_t* clear_words = nullptr, int n_clear = 0);
 hipError_t launch_pool_k(const Dims& d, const uint16_t* k_pool, const int32_t* page_table,
                          const int32_t* cached_len, int first_block, float* k_mean,
                          hipStream_t st);
 hipError_t launch_scores(const Dims& d, const float* q_mean, const float* k_mean,
                          const int32_t* cached_len, float* scores, hipStream_t st);
+// With group_words set, the selected rows are ORed into the (b, group) union
+// words (cleared beforehand) instead of being stored as masks.
 hipError_t launch_select(const Dims& d, const float* scores, const int32_t* cached_len,
                          float top_frac, int sink_blocks, int local_blocks, uint64_t* masks,
-                         hipStream_t st);
+                         hipStream_t st, uint64_t* group_words = nullptr, int group_size = 1);
 hipError_t raise_select_lds(int bytes);
 hipError_t launch_threshold_select(const Dims& d, const float* scores, const int32_t* cached_len,
                                    float margin, int sink_blocks, int local_blocks,
@@ -33,6 +36,9 @@ size_t tables_ws_bytes(const Dims& d, int group_size);
 hipError_t launch_tables(const Dims& d, const uint64_t* masks, const int32_t* cached_len,
                          int group_size, int32_t* kv_indptr, int32_t* kv_indices, void* ws,
                          hipStream_t st);
+// CSR from per-row union words (each row's count is its words' popcount).
+hipError_t launch_compact_words(const Dims& d, int rows, const uint64_t* words,
+                                int32_t* kv_indptr, int32_t* kv_indices, hipStream_t st);
 // Block-sparse rows (b, h, Q-block i) holding the union of the group of h,
 // causally limited to Q-block i (the block-sparse arm at matched tables).
 size_t union_rows_ws_bytes(const Dims& d, int group_size);

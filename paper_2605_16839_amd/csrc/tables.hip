@@ -62,26 +62,11 @@ __global__ __launch_bounds__(256) void union_kernel(const uint64_t* __restrict__
   if (t == 0) counts[r] = red[0] + red[1] + red[2] + red[3];
 }
 
-__global__ __launch_bounds__(256) void compact_kernel(const uint64_t* __restrict__ gwords,
-                                                      const int32_t* __restrict__ counts,
-                                                      int32_t* __restrict__ kv_indptr,
-                                                      int32_t* __restrict__ kv_indices, int W) {
-  __shared__ int red[4];
-  __shared__ int wave_tot[4];
-  const int r = blockIdx.x;
+// Writes the set bits of one row's words, ascending, from row_start on.
+__device__ void compact_row(const uint64_t* __restrict__ gw, int row_start,
+                            int32_t* __restrict__ kv_indices, int W, int* wave_tot) {
   const int t = threadIdx.x;
   const int wv = t >> 6;
-  int part = 0;
-  for (int x = t; x < r; x += 256) part += counts[x];
-  part = wave_sum(part);
-  if (lane_id() == 0) red[wv] = part;
-  __syncthreads();
-  const int row_start = red[0] + red[1] + red[2] + red[3];
-  if (t == 0) {
-    if (r == 0) kv_indptr[0] = 0;
-    kv_indptr[r + 1] = row_start + counts[r];
-  }
-  const uint64_t* gw = gwords + (size_t)r * W;
   int carry = 0;
   for (int base = 0; base < W * 64; base += 256) {
     const int j = base + t;
@@ -99,6 +84,65 @@ __global__ __launch_bounds__(256) void compact_kernel(const uint64_t* __restrict
     carry += total;
     __syncthreads();
   }
+}
+
+__global__ __launch_bounds__(256) void compact_kernel(const uint64_t* __restrict__ gwords,
+                                                      const int32_t* __restrict__ counts,
+                                                      int32_t* __restrict__ kv_indptr,
+                                                      int32_t* __restrict__ kv_indices, int W) {
+  __shared__ int red[4];
+  __shared__ int wave_tot[4];
+  const int r = blockIdx.x;
+  const int t = threadIdx.x;
+  int part = 0;
+  for (int x = t; x < r; x += 256) part += counts[x];
+  part = wave_sum(part);
+  if (lane_id() == 0) red[t >> 6] = part;
+  __syncthreads();
+  const int row_start = red[0] + red[1] + red[2] + red[3];
+  if (t == 0) {
+    if (r == 0) kv_indptr[0] = 0;
+    kv_indptr[r + 1] = row_start + counts[r];
+  }
+  compact_row(gwords + (size_t)r * W, row_start, kv_indices, W, wave_tot);
+}
+
+// Same, with the counts taken from the words themselves: row r starts after
+// the set bits of rows 0..r-1 (the fused estimator-to-union path, whose
+// words are complete only once every selection row has been ORed in).
+__global__ __launch_bounds__(256) void compact_words_kernel(const uint64_t* __restrict__ gwords,
+                                                            int32_t* __restrict__ kv_indptr,
+                                                            int32_t* __restrict__ kv_indices,
+                                                            int W) {
+  __shared__ int red[8];
+  __shared__ int wave_tot[4];
+  const int r = blockIdx.x;
+  const int t = threadIdx.x;
+  int before = 0, own = 0;
+  for (int x = t; x < (r + 1) * W; x += 256) {
+    const int c = __popcll(gwords[x]);
+    if (x < r * W) before += c;
+    else own += c;
+  }
+  before = wave_sum(before);
+  own = wave_sum(own);
+  if (lane_id() == 0) {
+    red[t >> 6] = before;
+    red[4 + (t >> 6)] = own;
+  }
+  __syncthreads();
+  const int row_start = red[0] + red[1] + red[2] + red[3];
+  if (t == 0) {
+    if (r == 0) kv_indptr[0] = 0;
+    kv_indptr[r + 1] = row_start + red[4] + red[5] + red[6] + red[7];
+  }
+  compact_row(gwords + (size_t)r * W, row_start, kv_indices, W, wave_tot);
+}
+
+hipError_t launch_compact_words(const Dims& d, int rows, const uint64_t* words,
+                                int32_t* kv_indptr, int32_t* kv_indices, hipStream_t st) {
+  compact_words_kernel<<<rows, 256, 0, st>>>(words, kv_indptr, kv_indices, d.W);
+  return hipGetLastError();
 }
 
 // Block-sparse arm at matched tables (Sec. 4.4): the union of execution group

@@ -143,3 +143,27 @@ def test_threshold_validation(lib):
     s = lib.ca_estimate_masks(p.ref, fake, fake, fake, 1.5, 1, 4, 0, fake, fake, fake, fake,
                               None)
     assert lib.ca_status_string(s).decode() == "CA_ERR_SHAPE"
+
+
+def test_fused_tables_validation(lib):
+    """ca_estimate_tables rejects a bad group, parameters and a short or
+    misaligned workspace on the host (fake device pointers, never dereferenced)."""
+    fake = ctypes.c_void_p(0x1000)
+    p = _prob()
+    p.c.cached_len = fake.value
+    need = lib.ca_tables_workspace_bytes(p.ref, 4)
+    assert need > 0
+
+    def call(top=0.05, gs=4, ws=fake, nbytes=need, first=0):
+        s = lib.ca_estimate_tables(p.ref, fake, fake, fake, top, 1, 4, first, gs, fake, fake,
+                                   fake, fake, fake, ws, nbytes, None)
+        return lib.ca_status_string(s).decode()
+
+    assert call(gs=3) == "CA_ERR_GROUP"
+    assert call(gs=0) == "CA_ERR_GROUP"
+    assert call(top=1.5) == "CA_ERR_SHAPE"
+    assert call(first=-1) == "CA_ERR_SHAPE"
+    assert call(ws=None) == "CA_ERR_WORKSPACE"
+    assert call(nbytes=8) == "CA_ERR_WORKSPACE"
+    assert call(ws=ctypes.c_void_p(0x1004)) == "CA_ERR_WORKSPACE"
+

@@ -255,6 +255,56 @@ def test_threshold_estimator_end_to_end(name, alpha, tau, workload_inputs, oracl
           f"{gb[..., :w.n_cached_blocks(0)].mean():.4f}")
 
 
+@pytest.mark.parametrize("name,gs", [("llama8b_32k", 4), ("llama8b_128k_final", 4),
+                                     ("batched_ragged_4seq", 4), ("qwen3_30b_128k_final", 4),
+                                     ("qwen3_30b_128k_final", 8), ("llama8b_32k", 1)])
+def test_fused_estimate_tables(name, gs, workload_inputs, oracle_estimate):
+    """Fused estimator -> union (no per-row masks): the tables equal the oracle's
+    union of the oracle masks, except blocks that are near ties (fp64 score within
+    1e-5 of the k-th score) in some row of the group; and they are bit-identical
+    to the unfused GPU path on the same inputs."""
+    d = workload_inputs(name)
+    w = d["workload"]
+    p = _problem(w)
+    x = device_inputs(d)
+    ref_masks, parts = oracle_estimate(name)
+    nkb = [w.n_kv_blocks(b) for b in range(w.batch)]
+    T = oracle.block_tables(ref_masks, gs, nkb)
+    (fip, fix), fb = ca.estimate_tables(p, x["q"], x["k"], x["pt"], w.top_frac, gs,
+                                        w.sink_blocks, w.local_blocks)
+    um, ub = ca.estimate_masks(p, x["q"], x["k"], x["pt"], w.top_frac, w.sink_blocks,
+                               w.local_blocks)
+    uip, uix = ca.build_block_tables(p, um, gs)
+    torch.cuda.synchronize()
+    fip, fix = fip.cpu().numpy(), fix.cpu().numpy()
+    assert np.array_equal(fip, uip.cpu().numpy())
+    assert np.array_equal(fix[:fip[-1]], uix.cpu().numpy()[:fip[-1]])
+    for b in range(w.batch):
+        nc = w.n_cached_blocks(b)
+        assert torch.equal(fb["scores"][b, ..., :nc], ub["scores"][b, ..., :nc])
+    G = w.num_q_heads // gs
+    differ = 0
+    for r in range(w.batch * G):
+        b, g = divmod(r, G)
+        got = set(fix[fip[r]:fip[r + 1]].tolist())
+        want = set(T[b][g])
+        if got == want:
+            continue
+        differ += 1
+        nc = w.n_cached_blocks(b)
+        k = oracle.n_selected(w.top_frac, nc)
+        for j in got ^ want:
+            assert j < nc, f"row {r}: a forced block {j} differs"
+            near = False
+            for h in range(g * gs, (g + 1) * gs):
+                for i in range(w.n_qblocks):
+                    s = parts["scores"][b][h, i][:nc]
+                    kth = np.sort(s)[::-1][k - 1]
+                    near |= abs(s[j] - kth) <= 1e-5
+            assert near, f"row {r}: block {j} differs without a near tie"
+    print(f"{name} gs={gs}: {differ} table rows differ by near ties")
+
+
 def _near_tie_check(gpu_masks, ref_masks, scores64, w, tol):
     """Rows may differ only where the fp64 scores of swapped blocks tie within tol."""
     gb, rb = oracle.unpack_masks(gpu_masks), oracle.unpack_masks(ref_masks)
