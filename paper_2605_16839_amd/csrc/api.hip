@@ -100,20 +100,18 @@ ca_status need_device(const ca_problem* p) {
   return CA_OK;
 }
 
-ca_status attention_tile_ok(const ca::Dims& d, int group_size) {
-  if (128 % group_size != 0)
-    return fail(CA_ERR_UNSUPPORTED, "group_size %d must divide 128", group_size);
-  const int qt = ca::attn_query_tile(group_size);
-  if (d.C % qt != 0)
-    return fail(CA_ERR_UNSUPPORTED, "chunk_len %d must be a multiple of %d for group_size %d",
-                d.C, qt, group_size);
+ca_status attention_tile_ok(int group_size, int table_mode) {
+  const int rows = ca::attn_rows_per_workgroup(table_mode);
+  if (rows % group_size != 0)
+    return fail(CA_ERR_UNSUPPORTED, "group_size %d must divide %d", group_size, rows);
   return CA_OK;
 }
 
 // Splits chosen when the caller passes num_splits = 0.
-int auto_splits(const ca::Dims& d, int group_size, size_t ws_bytes, bool have_ws) {
-  const int base = ca::attn_base_workgroups(d, group_size);
-  const int target = 2 * 256;  // two resident workgroups on each of 256 CUs
+int auto_splits(const ca::Dims& d, int group_size, size_t ws_bytes, bool have_ws,
+                int table_mode = ca::kTablesPerGroup) {
+  const int base = ca::attn_base_workgroups(d, group_size, table_mode);
+  const int target = ca::attn_resident_workgroups(table_mode);
   if (base >= target || !have_ws) return 1;
   int s = (target + base - 1) / base;
   const int max_by_len = d.max_nkb / 4 > 1 ? d.max_nkb / 4 : 1;
@@ -135,19 +133,20 @@ ca_status run_attention(const ca_problem* p, const uint16_t* q, const uint16_t* 
   if ((s = need_device(p)) != CA_OK) return s;
   if (!q || !k_pool || !v_pool || !out || (!page_table && table_mode != ca::kTablesPacked))
     return fail(CA_ERR_NULL, "q, k_pool, v_pool, page_table and out are required");
-  if (table_mode == ca::kTablesPerQTile && ca::attn_query_tile(group_size) != d.q_block)
+  if (table_mode == ca::kTablesPerQTile &&
+      ca::attn_query_tile(group_size, table_mode) != d.q_block)
     return fail(CA_ERR_UNSUPPORTED,
                 "block-sparse attention runs one head x one Q-block per tile: q_block must be "
-                "%d, got %d", ca::attn_query_tile(group_size), d.q_block);
+                "%d, got %d", ca::attn_query_tile(group_size, table_mode), d.q_block);
   if (table_mode == ca::kTablesPacked && packed_pages < 1)
     return fail(CA_ERR_SHAPE, "capacity_pages must be >= 1");
   if (!dense && (!kv_indptr || !kv_indices))
     return fail(CA_ERR_NULL, "kv_indptr and kv_indices are required");
-  if ((s = attention_tile_ok(d, group_size)) != CA_OK) return s;
+  if ((s = attention_tile_ok(group_size, table_mode)) != CA_OK) return s;
   if (num_splits < 0 || num_splits > 64)
     return fail(CA_ERR_SHAPE, "num_splits %d out of range [0, 64]", num_splits);
   int splits = num_splits;
-  if (splits == 0) splits = auto_splits(d, group_size, ws_bytes, ws != nullptr);
+  if (splits == 0) splits = auto_splits(d, group_size, ws_bytes, ws != nullptr, table_mode);
   if (splits > 1) {
     const size_t need = ca::attn_ws_bytes(d, splits);
     if (ws == nullptr || ws_bytes < need)

@@ -2,37 +2,41 @@
 // App. B.2), bf16 MFMA with fp32 online softmax, and the split-KV
 // log-sum-exp combine.
 //
-// Work decomposition (one workgroup = 4 wavefronts = 128 (head, query) rows):
+// Work decomposition: one workgroup = NW wavefronts, one per SIMD (each wave
+// holds up to 512 registers), 64 (head, query) rows per wave:
 //   * a table row r = b*G + g serves the group_size query heads of group g;
 //     all of them read the same KV pages, so a workgroup packs rows of every
-//     head of the group (group_size heads x 128/group_size chunk queries) and
-//     each KV page staged in LDS feeds all 128 rows;
-//   * wave w owns rows 32w..32w+31, one (head, query) pair per MFMA column;
-//   * the pages of the table are copied from HBM straight into LDS with
-//     16-byte direct-to-LDS loads (no register round trip); each lane picks
-//     its source chunk so that the LDS image is XOR-swizzled and the MFMA
-//     operand reads are bank-conflict free;
-//   * each wave computes S^T = K Q^T (keys x queries) with
-//     v_mfma_f32_32x32x16_bf16, so every lane holds one query column and the
-//     softmax statistics stay in-lane, then O^T += V^T P^T, the V^T
-//     fragments coming straight from the row-major V page through the gfx950
-//     transpose read ds_read_b64_tr_b16;
-//   * the copy of page i+1 is in flight while page i is processed (double
-//     buffered tiles, one barrier per page); the MFMA and softmax phases of
-//     the two workgroups resident on a CU overlap on each SIMD;
-//   * causal masking is applied only to the trailing entries whose keys can
-//     be later than the workgroup's first query, by absolute position
-//     64*j + r versus cached_len + t (positions from the logical block id,
-//     App. B.2); entries past the workgroup's last visible block are dropped
-//     (tables are ascending).
+//     head of the group (group_size heads x 64*NW/group_size chunk queries)
+//     and each KV page staged in LDS feeds all of them;
+//   * a wave's 64 rows are two 32-column MFMA tiles, so every K and V
+//     fragment it reads from LDS feeds two v_mfma_f32_32x32x16_bf16: half the
+//     LDS traffic per flop of a 32-row wave;
+//   * S^T = K Q^T (keys x queries): every lane holds one query column, so
+//     the softmax statistics are in-lane plus one v_permlane32_swap; then
+//     O^T += V^T P^T with the V^T fragments read straight from the row-major
+//     V page by the gfx950 transpose read ds_read_b64_tr_b16;
+//   * pages go from HBM into LDS with 16-byte direct-to-LDS loads (no
+//     register round trip) into XOR-swizzled tiles (conflict-free operand
+//     reads);
+//   * software pipeline: step i issues the copies of K(i+2) and V(i), the PV
+//     MFMAs of page i-1 and the QK MFMAs of page i+1, and between them (one
+//     MFMA per slot) the softmax of page i, so the matrix cores and the VALU
+//     of one wave work side by side; one barrier per page;
+//   * the causally masked diagonal pages (and an odd leftover page) run after
+//     the pipeline, one at a time: their keys are compared by absolute
+//     position 64*j + r against cached_len + t (positions from the logical
+//     block id, App. B.2); entries past the tile's last visible block are
+//     dropped (tables are ascending).
 #include <type_traits>
+#include <utility>
 
 #include "common.hpp"
 #include "kernels.hpp"
 
 namespace ca {
 
-constexpr int kRows = 128;   // (head, query) rows per workgroup
+constexpr int kWavesGroup = 4;   // waves per workgroup, per-group tables
+constexpr int kWavesQTile = 2;   // waves per workgroup, one head x 128 queries
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -63,6 +67,8 @@ struct AttnArgs {
 // V is read 8 bytes per lane by the transpose read, 32 lanes covering 4
 // consecutive rows x 4 chunks: each row's aligned group of 4 chunks must
 // move to a different aligned group of the window.
+// Both swizzles leave a row's pattern unchanged under +8 and +16 rows, so
+// the operand reads of one lane differ only by immediate offsets.
 template <int D>
 __device__ __forceinline__ int k_swz(int r, int c) {
   return D == 128 ? (c ^ (r & 15)) : (c ^ ((r >> 1) & 7));
@@ -76,44 +82,6 @@ __device__ __forceinline__ int v_swz(int r, int c) {
 // which only affects softmax weights < 2^-126).
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// o[x] *= alpha for every tile when `any` is non-zero.  The branch lives
-// inside the asm so that the accumulators keep their registers on both paths
-// (a compiler-level branch makes the register allocator copy all of them
-// every step).  Only taken when the exponent base moves (lazy rescaling);
-// the leading nops cover the MFMA-to-VALU and the trailing ones the
-// VALU-to-MFMA dependency distances of the accumulators.
-template <int NDT>
-__device__ __forceinline__ void rescale_tiles(f32x16 (&o)[NDT], float alpha, uint64_t any) {
-#pragma unroll
-  for (int x = 0; x < NDT; ++x) {
-    __asm__ volatile(
-        "s_cmp_eq_u64 %16, 0\n"
-        "s_cbranch_scc1 1f\n"
-        "s_nop 7\n s_nop 7\n s_nop 7\n"
-        "v_mul_f32 %0, %17, %0\n v_mul_f32 %1, %17, %1\n"
-        "v_mul_f32 %2, %17, %2\n v_mul_f32 %3, %17, %3\n"
-        "v_mul_f32 %4, %17, %4\n v_mul_f32 %5, %17, %5\n"
-        "v_mul_f32 %6, %17, %6\n v_mul_f32 %7, %17, %7\n"
-        "v_mul_f32 %8, %17, %8\n v_mul_f32 %9, %17, %9\n"
-        "v_mul_f32 %10, %17, %10\n v_mul_f32 %11, %17, %11\n"
-        "v_mul_f32 %12, %17, %12\n v_mul_f32 %13, %17, %13\n"
-        "v_mul_f32 %14, %17, %14\n v_mul_f32 %15, %17, %15\n"
-        "s_nop 7\n"
-        "1:"
-        : "+v"(o[x][0]), "+v"(o[x][1]), "+v"(o[x][2]), "+v"(o[x][3]), "+v"(o[x][4]),
-          "+v"(o[x][5]), "+v"(o[x][6]), "+v"(o[x][7]), "+v"(o[x][8]), "+v"(o[x][9]),
-          "+v"(o[x][10]), "+v"(o[x][11]), "+v"(o[x][12]), "+v"(o[x][13]), "+v"(o[x][14]),
-          "+v"(o[x][15])
-        : "s"(any), "v"(alpha)
-        : "scc");
-  }
-}
-
-template <bool DENSE>
-__device__ __forceinline__ int table_entry(const int32_t* __restrict__ idx, int base, int e) {
-  return DENSE ? e : idx[base + e];
-}
-
 typedef __attribute__((address_space(3))) void lds_void;
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
@@ -121,13 +89,13 @@ typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 // Copy one page (64 rows x D bf16, contiguous in HBM) into an LDS tile with
 // direct-to-LDS loads.  Each wave instruction fills 1 KB of the tile, lane l
 // writing bytes [16l, 16l+16); the lane's source is the chunk that the
-// swizzle maps there (the swizzles are involutions).
-template <int D, bool IS_V>
+// swizzle maps there (the swizzles are involutions).  NW waves share a page.
+template <int D, int NW, bool IS_V>
 __device__ __forceinline__ void page_to_lds(const uint16_t* __restrict__ src, uint16_t* tile,
                                             int wv, int lane) {
-  constexpr int CPR = D / 8;                             // 16-byte chunks per row
-  constexpr int ROWS_PER_INST = 64 / CPR;                // rows per 1 KB instruction
-  constexpr int INST_PER_WAVE = (64 * D * 2) / 1024 / 4; // 4 waves share a page
+  constexpr int CPR = D / 8;                               // 16-byte chunks per row
+  constexpr int ROWS_PER_INST = 64 / CPR;                  // rows per 1 KB instruction
+  constexpr int INST_PER_WAVE = (64 * D * 2) / 1024 / NW;
 #pragma unroll
   for (int m = 0; m < INST_PER_WAVE; ++m) {
     const int inst = wv * INST_PER_WAVE + m;
@@ -140,10 +108,14 @@ __device__ __forceinline__ void page_to_lds(const uint16_t* __restrict__ src, ui
 }
 
 // Wait for this wave's direct-to-LDS copies and tell the compiler that the
-// tiles behind p0/p1 changed (the copies write them outside its view).
-__device__ __forceinline__ void copies_landed(void* p0, void* p1) {
+// tiles behind the pointers changed (the copies write them outside its view).
+__device__ __forceinline__ void tile_written(const void* tile) {
+  __asm__ volatile("" : : "v"(tile) : "memory");
+}
+template <typename... T>
+__device__ __forceinline__ void copies_landed(const T*... tiles) {
   __builtin_amdgcn_s_waitcnt(0);
-  __asm__ volatile("" : : "v"(p0), "v"(p1) : "memory");
+  (tile_written(tiles), ...);
 }
 
 // NaN-propagating maximum (v_maximum3_f32 on gfx950).  fmaxf would quiet
@@ -171,74 +143,95 @@ __device__ __forceinline__ float halves_sum(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// S^T tile of one page: keys 0..31 in .lo, 32..63 in .hi.
-struct STile {
-  f32x16 lo, hi;
+// S^T tiles of one page for the wave's two column tiles: s[c][h] holds keys
+// 32h .. 32h+31 of column tile c; key of accumulator slot v (lane half hf):
+// 32h + 8*(v/4) + 4*hf + v%4.
+struct SPage {
+  f32x16 s[2][2];
+};
+// P^T fragments (bf16) of one page: p[c][kk] covers keys 16kk .. 16kk+15.
+struct PFrag {
+  bf16x8 p[2][4];
 };
 
-// S^T = K Q^T over one page: A = K rows (32 keys x 16 d per k-step), B = Q^T.
-template <int D>
-__device__ __forceinline__ void qk_page(STile& st, const uint16_t* __restrict__ ks,
-                                        const bf16x8 (&qf)[D / 16], int col, int half) {
-#pragma unroll
-  for (int v = 0; v < 16; ++v) { st.lo[v] = 0.f; st.hi[v] = 0.f; }
-#pragma unroll
-  for (int x = 0; x < D / 16; ++x) {
-    const int c = 2 * x + half;
-    const bf16x8 a0 = *reinterpret_cast<const bf16x8*>(ks + col * D + 8 * k_swz<D>(col, c));
-    const bf16x8 a1 =
-        *reinterpret_cast<const bf16x8*>(ks + (32 + col) * D + 8 * k_swz<D>(32 + col, c));
-    st.lo = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, qf[x], st.lo, 0, 0, 0);
-    st.hi = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, qf[x], st.hi, 0, 0, 0);
-  }
+// ---- MFMAs with explicit register classes (inline asm) ----
+// O^T accumulators and Q^T fragments live in AGPRs, S^T tiles and P^T
+// fragments in VGPRs.  The compiler cannot see the wait states these
+// instructions need, so the kernel places explicit s_nop fences where an
+// MFMA result is read by VALU code or a VALU result is read by an MFMA.
+__device__ __forceinline__ void mfma_o(f32x16& o, const bf16x8& a, const bf16x8& b) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(o) : "v"(a), "v"(b));
+}
+__device__ __forceinline__ void mfma_s0(f32x16& s, const bf16x8& a, const bf16x8& b) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&v"(s) : "v"(a), "a"(b));
+}
+__device__ __forceinline__ void mfma_s(f32x16& s, const bf16x8& a, const bf16x8& b) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(s) : "v"(a), "a"(b));
 }
 
-// V^T fragment for PV k-step kk and d tile x.  Lane (d row `col`, half) needs
-// the 8 keys 16kk + 4half + {0..3} and 16kk + 8 + 4half + {0..3}, the key
-// order of the P^T fragment taken from the S^T accumulator layout.  In a
-// 16-lane group, source lane 4m + q points at key row base + m, d columns
-// 4q..4q+3 of the group's 16 d; the transpose read then hands lane i the
-// four keys of d = group base + i.
-template <int D>
-__device__ __forceinline__ bf16x8 vt_frag(const uint16_t* __restrict__ vs, int lane, int x,
-                                          int kk) {
-  const int grp = lane >> 4, sl = lane & 15;
-  const int m = sl >> 2, q = sl & 3;
-  const int d = 32 * x + 16 * (grp & 1) + 4 * q;
-  const int c = d >> 3, sub = d & 7;
-  const int r0 = 16 * kk + 4 * (grp >> 1) + m;
-  const int r1 = r0 + 8;
-  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-      (lds_i16x4*)(vs + r0 * D + 8 * v_swz<D>(r0, c) + sub));
-  const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-      (lds_i16x4*)(vs + r1 * D + 8 * v_swz<D>(r1, c) + sub));
-  // whole-vector casts only: element-wise bf16 <-> i16 moves are not reliable
-  const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
-  const u32x4 w = {l2[0], l2[1], h2[0], h2[1]};
-  return __builtin_bit_cast(bf16x8, w);
+// Whole-tuple fence on the O^T accumulators: an MFMA result read or
+// overwritten by VALU code, or a VALU result read by an MFMA, needs wait
+// states the compiler cannot see through inline asm.
+template <int NDT>
+__device__ __forceinline__ void fence_o(f32x16 (&o)[2][NDT]) {
+#pragma unroll
+  for (int c = 0; c < 2; ++c)
+#pragma unroll
+    for (int x = 0; x < NDT; ++x) asm volatile("s_nop 7\n s_nop 7\n s_nop 7" : "+a"(o[c][x]));
 }
 
-template <int D, bool DENSE>
-__global__ __launch_bounds__(256, 2) void paged_attention_kernel(const AttnArgs a) {
-  constexpr int NKS = D / 16;   // k-steps of the QK contraction
-  constexpr int NDT = D / 32;   // 32-row d tiles of O^T
-  constexpr int PAGE = 64 * D;  // bf16 per page tile
-  constexpr int COPIES = 2 * (64 * D * 2) / 1024 / 4;   // copy instructions per wave per step
-  // Separate buffers (not one array) so that the compiler can tell the copy
-  // target of a step from the tiles that step reads.
+// Fences on S^T tiles (MFMA results about to be read by the softmax) and on
+// P^T fragments (VALU results about to be read by MFMAs).
+__device__ __forceinline__ void fence_s(SPage& s) {
+  asm volatile("s_nop 7\n s_nop 7\n s_nop 5"
+               : "+v"(s.s[0][0]), "+v"(s.s[0][1]), "+v"(s.s[1][0]), "+v"(s.s[1][1]));
+}
+__device__ __forceinline__ void fence_p(PFrag& p) {
+  asm volatile("s_nop 7\n s_nop 7\n s_nop 5"
+               : "+v"(p.p[0][0]), "+v"(p.p[0][1]), "+v"(p.p[0][2]), "+v"(p.p[0][3]),
+                 "+v"(p.p[1][0]), "+v"(p.p[1][1]), "+v"(p.p[1][2]), "+v"(p.p[1][3]));
+}
+
+// Forces v to be computed at this point of the instruction stream (an empty
+// volatile asm that reads it): keeps the softmax work of a slot from being
+// moved to its uses by the compiler.
+template <typename T>
+__device__ __forceinline__ void pin(const T& v) {
+  asm volatile("" : : "v"(v));
+}
+
+// Calls f(integral_constant<int, I>) for I = 0 .. N-1 (compile-time indices).
+template <typename F, int... I>
+__device__ __forceinline__ void static_for_impl(F& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+template <int D, int NW, bool DENSE>
+__global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnArgs a) {
+  constexpr int NKS = D / 16;          // QK k-steps
+  constexpr int NDT = D / 32;          // O^T d tiles
+  constexpr int PAGE = 64 * D;
+  constexpr int ROWS = 64 * NW;
+  constexpr int NPV = 4 * NDT;         // V^T fragments per page
+  constexpr int NQK = 2 * NKS;         // K fragments per page
+  constexpr int NFRAG = NPV + NQK;
+  constexpr int NSLOT = 2 * NFRAG;     // one MFMA per slot
+  constexpr int MAXS = 10;             // slots holding the max / rebase work
   __shared__ __attribute__((aligned(1024))) uint16_t k_s0[PAGE];
   __shared__ __attribute__((aligned(1024))) uint16_t k_s1[PAGE];
   __shared__ __attribute__((aligned(1024))) uint16_t v_s0[PAGE];
   __shared__ __attribute__((aligned(1024))) uint16_t v_s1[PAGE];
 
   const int t = threadIdx.x;
-  const int wv = t >> 6;
+  const int wv = __builtin_amdgcn_readfirstlane(t >> 6);
   const int lane = t & 63;
   const int col = lane & 31;
   const int half = lane >> 5;
 
-  // XCD-aware order: consecutive logical tiles (same table row) land on
-  // the same XCD and share its L2.
   int bid = blockIdx.x;
   const int nwg = gridDim.x;
   if ((nwg & 7) == 0) bid = (bid & 7) * (nwg >> 3) + (bid >> 3);
@@ -248,19 +241,26 @@ __global__ __launch_bounds__(256, 2) void paged_attention_kernel(const AttnArgs 
   const int b = rowid / a.G;
   const int g = rowid % a.G;
   const int gs = a.group_size;
-  const int QT = kRows / gs;
+  const int QT = ROWS / gs;            // chunk queries per tile
   const int q0 = qt * QT;
-  const int r = wv * 32 + col;
-  const int head = g * gs + r / QT;
-  const int tq = q0 + r % QT;
+  const int q_end = q0 + QT < a.C ? q0 + QT : a.C;   // the last tile may be partial
+  int head[2], tq[2];
+  bool valid[2];
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    const int r = wv * 64 + 32 * c + col;
+    head[c] = g * gs + r / QT;
+    tq[c] = q0 + r % QT;
+    valid[c] = tq[c] < a.C;
+    if (!valid[c]) tq[c] = a.C - 1;    // computes a copy of a real row, never stored
+  }
   const int kvh = (g * gs) / (a.Hq / a.Hkv);
-
   const int cl = a.cached_len[b];
   const int nc = cl / kPage;
   const int nkb = nc + a.C / kPage;
-  const int qpos = cl + tq;
-  const int j_last = (cl + q0 + QT - 1) / kPage;   // last block any row can see
-  const int mask_from = cl + q0;                    // keys beyond this need masking
+  const int qpos[2] = {cl + tq[0], cl + tq[1]};
+  const int j_last = (cl + q_end - 1) / kPage;     // last block any row can see
+  const int mask_from = cl + q0;                   // keys beyond this need masking
 
   int len, tbase = 0;
   if (DENSE) {
@@ -275,46 +275,51 @@ __global__ __launch_bounds__(256, 2) void paged_attention_kernel(const AttnArgs 
   const int e1 = (int)(((long long)len * (sp + 1)) / a.splits);
   const int32_t* ptab = a.page_table + ((size_t)b * a.Hkv + kvh) * a.max_kv_blocks;
 
-  // Q^T fragments: lane holds query column `col`, d = 16*ks + 8*half .. +7.
-  bf16x8 qf[NKS];
-  {
-    const uint16_t* qrow = a.q + (((size_t)b * a.C + tq) * a.Hq + head) * D + 8 * half;
+  bf16x8 qf[2][NKS];
 #pragma unroll
-    for (int ks = 0; ks < NKS; ++ks)
-      qf[ks] = *reinterpret_cast<const bf16x8*>(qrow + 16 * ks);
+  for (int c = 0; c < 2; ++c) {
+    const uint16_t* qrow = a.q + (((size_t)b * a.C + tq[c]) * a.Hq + head[c]) * D + 8 * half;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) {
+      qf[c][ks] = *reinterpret_cast<const bf16x8*>(qrow + 16 * ks);
+      asm volatile("s_nop 2" : "+a"(qf[c][ks]));   // into AGPRs before the first MFMA
+    }
   }
 
-  f32x16 o[NDT];
+  f32x16 o[2][NDT];
 #pragma unroll
-  for (int x = 0; x < NDT; ++x)
+  for (int c = 0; c < 2; ++c)
 #pragma unroll
-    for (int v = 0; v < 16; ++v) o[x][v] = 0.f;
-  float m_run = -INFINITY;   // running max, log2-scaled units
-  float l_run = 0.f;         // partial row sum over this lane's keys
+    for (int x = 0; x < NDT; ++x)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) o[c][x][v] = 0.f;
+  fence_o<NDT>(o);
+  float m_run[2] = {-INFINITY, -INFINITY};
+  float l_run[2] = {0.f, 0.f};
 
-  // Table entries e0 .. e_end-1 (entries past the last visible block are
-  // dropped; tables are ascending).  Those whose keys can be later than the
-  // first query of the tile need the causal mask and form a suffix.
   int e_end = e1;
   if (DENSE) {
     e_end = e1 < j_last + 1 ? e1 : j_last + 1;
   } else {
-    while (e_end > e0 && table_entry<DENSE>(a.kv_indices, tbase, e_end - 1) > j_last) --e_end;
+    while (e_end > e0 && a.kv_indices[tbase + e_end - 1] > j_last) --e_end;
   }
   const int n = e_end - e0;
   int n_main = n;
   while (n_main > 0 &&
-         kPage * table_entry<DENSE>(a.kv_indices, tbase, e0 + n_main - 1) + kPage - 1 > mask_from)
+         kPage * (DENSE ? e0 + n_main - 1 : a.kv_indices[tbase + e0 + n_main - 1]) + kPage - 1 >
+             mask_from)
     --n_main;
-  // Block and page ids of the entries, 64 at a time: lane l of blk_cur /
-  // pg_cur holds entry e0 + base + l (clamped to the last entry), the *_nxt
-  // pair the following 64; a step picks its ids with a scalar readlane.
+  // pages run by the software-pipelined loop: an even number of unmasked ones
+  const int n_pipe = n_main & ~1;
+
+  SPage SA, SB;
+  PFrag PA, PB;
   int base = 0, blk_cur = 0, pg_cur = 0, blk_nxt = 0, pg_nxt = 0;
   auto fetch = [&](int b0, int& blk, int& pg) {
     int idx = b0 + lane;
     idx = idx < n ? idx : n - 1;
     idx = idx < 0 ? 0 : idx;
-    blk = (n > 0) ? table_entry<DENSE>(a.kv_indices, tbase, e0 + idx) : 0;
+    blk = (n > 0) ? (DENSE ? e0 + idx : a.kv_indices[tbase + e0 + idx]) : 0;
     if (!DENSE && a.table_mode == kTablesPacked) {
       // packed pools hold the selected pages in table order (copy arm)
       const long long pp = (long long)tbase + e0 + idx;
@@ -325,7 +330,7 @@ __global__ __launch_bounds__(256, 2) void paged_attention_kernel(const AttnArgs 
   };
   fetch(0, blk_cur, pg_cur);
   fetch(64, blk_nxt, pg_nxt);
-  auto advance = [&](int i) {   // make i - base < 64
+  auto advance = [&](int i) {
     while (i - base >= 64) {
       base += 64;
       blk_cur = blk_nxt;
@@ -333,7 +338,7 @@ __global__ __launch_bounds__(256, 2) void paged_attention_kernel(const AttnArgs 
       fetch(base + 64, blk_nxt, pg_nxt);
     }
   };
-  auto id_of = [&](int cur, int nxt, int i) -> int {   // i - base in [0, 128)
+  auto id_of = [&](int cur, int nxt, int i) -> int {
     const int d = i - base;
     return d < 64 ? __builtin_amdgcn_readlane(cur, d) : __builtin_amdgcn_readlane(nxt, d - 64);
   };
@@ -341,143 +346,286 @@ __global__ __launch_bounds__(256, 2) void paged_attention_kernel(const AttnArgs 
     return pool + (size_t)id_of(pg_cur, pg_nxt, i) * (kPage * D);
   };
 
-  // Prologue: K and V of page 0 in LDS.
-  if (n > 0) {
-    page_to_lds<D, false>(page_ptr(a.k_pool, 0), k_s0, wv, lane);
-    page_to_lds<D, true>(page_ptr(a.v_pool, 0), v_s0, wv, lane);
+  // Per-lane byte offsets of the MFMA operand reads inside a page tile; the
+  // buffer, the 16-key block of a PV step and the upper 32 keys of a QK step
+  // are immediates.
+  uint32_t kofs[NKS], vofs[NDT];
+#pragma unroll
+  for (int x = 0; x < NKS; ++x)
+    kofs[x] = (uint32_t)(col * D * 2 + 16 * k_swz<D>(col, 2 * x + half));
+  {
+    const int grp = lane >> 4, sl = lane & 15;
+    const int m = sl >> 2, q = sl & 3;
+    const int r0 = 4 * (grp >> 1) + m;
+#pragma unroll
+    for (int x = 0; x < NDT; ++x) {
+      const int d = 32 * x + 16 * (grp & 1) + 4 * q;
+      vofs[x] = (uint32_t)(r0 * D * 2 + 16 * v_swz<D>(r0, d >> 3) + 2 * (d & 7));
+    }
   }
-  copies_landed(k_s0, v_s0);
-  __syncthreads();
+  // fragment F of a step: F < NPV is V^T fragment (kk = F / NDT, x = F % NDT),
+  // otherwise K fragment (k-step (F - NPV) / 2, keys 32 * ((F - NPV) % 2) ..)
+  auto load_frag = [&](int F, const uint16_t* vt, const uint16_t* kt) -> bf16x8 {
+    if (F < NPV) {
+      const int kk = F / NDT, x = F % NDT;
+      const char* p = reinterpret_cast<const char*>(vt) + vofs[x] + 16 * kk * D * 2;
+      const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p);
+      const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 8 * D * 2));
+      const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
+      const u32x4 w = {l2[0], l2[1], h2[0], h2[1]};
+      return __builtin_bit_cast(bf16x8, w);
+    }
+    const int G2 = F - NPV;
+    const char* p = reinterpret_cast<const char*>(kt) + kofs[G2 / 2] + (G2 % 2) * 32 * D * 2;
+    return *reinterpret_cast<const bf16x8*>(p);
+  };
 
-  // Step i (page e0 + i, buffer parity S = i & 1 as a compile-time constant so
-  // that the copy targets and the tiles read are distinct objects): the copy
-  // of page i+1 into buffers S^1 goes out first and lands while page i is
-  // processed from buffers S: S^T = K Q^T, online softmax, O^T += V^T P^T.
-  auto step = [&](auto masked, auto stage, int i) __attribute__((always_inline)) {
-    constexpr int S = decltype(stage)::value;
-    uint16_t* const k_here = S ? k_s1 : k_s0;
-    uint16_t* const k_next = S ? k_s0 : k_s1;
-    uint16_t* const v_here = S ? v_s1 : v_s0;
-    uint16_t* const v_next = S ? v_s0 : v_s1;
-    const int i1 = i + 1 < n ? i + 1 : n - 1;   // clamped: the copy stays valid, unused
-    page_to_lds<D, false>(page_ptr(a.k_pool, i1), k_next, wv, lane);
-    page_to_lds<D, true>(page_ptr(a.v_pool, i1), v_next, wv, lane);
-    STile st;
-    qk_page<D>(st, k_here, qf, col, half);
-
-    // ---- online softmax of page e0 + i ----
-    if constexpr (decltype(masked)::value) {
-      const int j = id_of(blk_cur, blk_nxt, i);
-      // key of accumulator slot v: 64*j + 8*(v/4) + 4*half + v%4 (+32 in .hi)
-      const int lim = qpos - kPage * j - 4 * half;
+  // Whole-page contractions (outside the pipelined loop).
+  auto qk_page = [&](SPage& st, const uint16_t* kt) __attribute__((always_inline)) {
+    static_for<NQK>([&](auto gtag) __attribute__((always_inline)) {
+      constexpr int G2 = decltype(gtag)::value, x = G2 / 2, h = G2 % 2;
+      const bf16x8 kf = load_frag(NPV + G2, kt, kt);
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int kp = 8 * (v >> 2) + (v & 3);
-        if (kp > lim) st.lo[v] = -INFINITY;
-        if (kp + 32 > lim) st.hi[v] = -INFINITY;
+      for (int c = 0; c < 2; ++c) {
+        if constexpr (x == 0) mfma_s0(st.s[c][h], kf, qf[c][x]);
+        else mfma_s(st.s[c][h], kf, qf[c][x]);
       }
-    }
-    float mx = max3(st.lo[0], st.hi[0], st.lo[1]);
-    mx = max3(mx, st.hi[1], st.lo[2]);
+    });
+  };
+  auto pv_page = [&](const PFrag& pf, const uint16_t* vt) __attribute__((always_inline)) {
+    static_for<NPV>([&](auto ftag) __attribute__((always_inline)) {
+      constexpr int F = decltype(ftag)::value;
+      const bf16x8 vf = load_frag(F, vt, vt);
 #pragma unroll
-    for (int v = 2; v < 15; ++v) mx = max3(mx, st.hi[v], st.lo[v + 1]);
-    mx = max3(mx, st.hi[15], st.hi[15]);
-    mx = halves_max(mx) * a.scale_log2;
-    // move the base only when the page's max exceeds it by the slack
-    // (-inf > -inf + slack is false: a fully masked row keeps its base)
-    const bool rebase = mx > m_run + kRescaleSlack;
-    const float alpha = rebase ? fast_exp2(m_run - mx) : 1.0f;
-    m_run = rebase ? mx : m_run;
-    l_run *= alpha;
-    rescale_tiles<NDT>(o, alpha, __ballot(rebase));
-    const float m_base = (m_run == -INFINITY) ? 0.f : m_run;
-#pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      st.lo[v] = fast_exp2(fmaf(st.lo[v], a.scale_log2, -m_base));
-      st.hi[v] = fast_exp2(fmaf(st.hi[v], a.scale_log2, -m_base));
-    }
-    float ps0 = st.lo[0], ps1 = st.hi[0];
-#pragma unroll
-    for (int v = 1; v < 16; ++v) { ps0 += st.lo[v]; ps1 += st.hi[v]; }
-    l_run += ps0 + ps1;
-    // P^T fragments: k-step kk covers accumulator slots 8*(kk%2)..+7
-    bf16x8 pf[4];
-#pragma unroll
-    for (int x = 0; x < 8; ++x) {
-      pf[0][x] = (__bf16)st.lo[x];
-      pf[1][x] = (__bf16)st.lo[8 + x];
-      pf[2][x] = (__bf16)st.hi[x];
-      pf[3][x] = (__bf16)st.hi[8 + x];
-    }
+      for (int c = 0; c < 2; ++c) mfma_o(o[c][F % NDT], vf, pf.p[c][F / NDT]);
+    });
+  };
 
-    // ---- O^T += V^T P^T ----
+  // Prologue: K(0) -> k_s0, K(1) -> k_s1, and V(0) into the buffer the first
+  // step's PV reads, with a zero P: that PV adds nothing and every tile read
+  // is initialised.  Then S(0).
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
+  for (int c = 0; c < 2; ++c)
 #pragma unroll
-      for (int x = 0; x < NDT; ++x)
-        o[x] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vt_frag<D>(v_here, lane, x, kk),
-                                                       pf[kk], o[x], 0, 0, 0);
+    for (int kk = 0; kk < 4; ++kk) PB.p[c][kk] = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
+  if (n_pipe > 0) {
+    page_to_lds<D, NW, false>(page_ptr(a.k_pool, 0), k_s0, wv, lane);
+    page_to_lds<D, NW, false>(page_ptr(a.k_pool, 1), k_s1, wv, lane);
+    page_to_lds<D, NW, true>(page_ptr(a.v_pool, 0), v_s1, wv, lane);
+    copies_landed(k_s0, k_s1, v_s1);
+    __syncthreads();
+    qk_page(SA, k_s0);
+    __syncthreads();
+  }
+
+  // Step i: DMA K(i+2) -> k[i%2], V(i) -> v[i%2]; PV(i-1) from v[(i-1)%2] and
+  // P(i-1); QK(i+1) from k[(i+1)%2]; softmax(i) of S(i) into P(i).  One MFMA
+  // per slot, the softmax work spread over the slots.
+  auto step = [&](auto par, int i) __attribute__((always_inline)) {
+    constexpr int P = decltype(par)::value;
+    SPage& sc = P ? SB : SA;
+    SPage& sn = P ? SA : SB;
+    PFrag& pn = P ? PB : PA;
+    PFrag& po = P ? PA : PB;
+    uint16_t* const k_dma = P ? k_s1 : k_s0;
+    const uint16_t* const k_rd = P ? k_s0 : k_s1;
+    uint16_t* const v_dma = P ? v_s1 : v_s0;
+    const uint16_t* const v_rd = P ? v_s0 : v_s1;
+    const int i2 = i + 2 < n_pipe ? i + 2 : n_pipe - 1;
+    page_to_lds<D, NW, false>(page_ptr(a.k_pool, i2), k_dma, wv, lane);
+    page_to_lds<D, NW, true>(page_ptr(a.v_pool, i), v_dma, wv, lane);
+    fence_s(sc);
+    fence_p(po);
+    float mx[2] = {-INFINITY, -INFINITY}, alpha[2] = {1.f, 1.f}, nmb[2] = {0.f, 0.f};
+    float ps[2] = {0.f, 0.f};
+    bool rb_any = false;
+    bf16x8 fr[NFRAG];
+    fr[0] = load_frag(0, v_rd, k_rd);
+    fr[1] = load_frag(1, v_rd, k_rd);
+    static_for<NSLOT>([&](auto stag) __attribute__((always_inline)) {
+      constexpr int s = decltype(stag)::value;
+      constexpr int F = s / 2, c = s % 2;
+      if constexpr (c == 0 && F + 2 < NFRAG) fr[F + 2] = load_frag(F + 2, v_rd, k_rd);
+      if constexpr (F < NPV) {
+        mfma_o(o[c][F % NDT], fr[F], po.p[c][F / NDT]);
+      } else {
+        constexpr int G2 = F - NPV, x = G2 / 2, h = G2 % 2;
+        if constexpr (x == 0) mfma_s0(sn.s[c][h], fr[F], qf[c][x]);
+        else mfma_s(sn.s[c][h], fr[F], qf[c][x]);
+      }
+      // softmax work of this slot
+      if constexpr (s < 8) {
+        constexpr int cc = s / 4, k0 = 4 * (s % 4);
+#pragma unroll
+        for (int k = k0; k < k0 + 4; ++k) mx[cc] = max3(mx[cc], sc.s[cc][0][k], sc.s[cc][1][k]);
+        pin(mx[cc]);
+      } else if constexpr (s < MAXS) {
+        constexpr int cc = s - 8;
+        const float m = halves_max(mx[cc]) * a.scale_log2;
+        const bool rebase = m > m_run[cc] + kRescaleSlack;
+        alpha[cc] = rebase ? fast_exp2(m_run[cc] - m) : 1.0f;
+        m_run[cc] = rebase ? m : m_run[cc];
+        rb_any |= rebase;
+        nmb[cc] = (m_run[cc] == -INFINITY) ? 0.f : -m_run[cc];
+        pin(nmb[cc]);
+        pin(alpha[cc]);
+      } else {
+        constexpr int NOPS = 72;
+        constexpr int lo = ((s - MAXS) * NOPS) / (NSLOT - MAXS);
+        constexpr int hi = ((s - MAXS + 1) * NOPS) / (NSLOT - MAXS);
+        static_for<hi - lo>([&](auto otag) __attribute__((always_inline)) {
+          constexpr int op = lo + decltype(otag)::value;
+          constexpr int u = op / 9, k = op % 9, cc = u / 4, kk = u % 4;
+          f32x16& sv = sc.s[cc][kk / 2];
+          if constexpr (k < 8) {
+            constexpr int v = 8 * (kk % 2) + k;
+            const float e = fast_exp2(fmaf(sv[v], a.scale_log2, nmb[cc]));
+            sv[v] = e;
+            ps[cc] += e;
+            pin(ps[cc]);
+          } else {
+#pragma unroll
+            for (int x = 0; x < 8; ++x) pn.p[cc][kk][x] = (__bf16)sv[8 * (kk % 2) + x];
+            pin(pn.p[cc][kk]);
+          }
+        });
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    });
+#pragma unroll
+    for (int c = 0; c < 2; ++c) l_run[c] = l_run[c] * alpha[c] + ps[c];
+    const uint64_t any = __ballot(rb_any);
+    if (any) {   // the exponent base moved on some lane: rescale O (rare)
+      fence_o<NDT>(o);
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int x = 0; x < NDT; ++x) o[c][x] *= alpha[c];
+      fence_o<NDT>(o);
     }
-    copies_landed(k_next, v_next);
+    copies_landed(k_dma, v_dma);
     __syncthreads();
   };
-  using Plain = std::integral_constant<bool, false>;
-  using Masked = std::integral_constant<bool, true>;
-  using S0 = std::integral_constant<int, 0>;
-  using S1 = std::integral_constant<int, 1>;
-  int i = 0;
-  for (; i + 1 < n_main; i += 2) {
-    advance(i);
-    step(Plain{}, S0{}, i);
-    step(Plain{}, S1{}, i + 1);
-  }
-  if (i < n_main) {             // i is even here
-    advance(i);
-    step(Plain{}, S0{}, i);
-    ++i;
-  }
-  for (; i < n; ++i) {
-    advance(i);
-    if (i & 1) step(Masked{}, S1{}, i);
-    else step(Masked{}, S0{}, i);
+  using P0 = std::integral_constant<int, 0>;
+  using P1 = std::integral_constant<int, 1>;
+  if (n_pipe > 0) {
+    for (int i = 0; i < n_pipe; i += 2) {
+      advance(i);
+      step(P0{}, i);
+      advance(i + 1);
+      step(P1{}, i + 1);
+    }
+    // PV of page n_pipe - 1 (odd: its P is PB, its V in v_s1)
+    fence_p(PB);
+    pv_page(PB, v_s1);
+    __syncthreads();
   }
 
-  // ---- epilogue ----
-  const float l_tot = halves_sum(l_run);
-  const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
-  const float lse_val = l_tot > 0.f ? (m_run + log2f(l_tot)) * kLn2 : -INFINITY;
-  const size_t qrow_idx = ((size_t)b * a.Hq + head) * a.C + tq;   // [B, Hq, C] order
-  if (a.splits == 1) {
-    uint16_t* orow = a.out + (((size_t)b * a.C + tq) * a.Hq + head) * D;
+  // Remaining pages (the causally masked diagonal ones and an odd leftover),
+  // one at a time without overlap: K and V of the page to LDS, S = K Q^T,
+  // mask, softmax, O += V^T P^T.
+  for (int i = n_pipe; i < n; ++i) {
+    advance(i);
+    page_to_lds<D, NW, false>(page_ptr(a.k_pool, i), k_s0, wv, lane);
+    page_to_lds<D, NW, true>(page_ptr(a.v_pool, i), v_s0, wv, lane);
+    copies_landed(k_s0, v_s0);
+    __syncthreads();
+    qk_page(SA, k_s0);
+    fence_s(SA);
+    if (i >= n_main) {
+      const int j = id_of(blk_cur, blk_nxt, i);
 #pragma unroll
-    for (int x = 0; x < NDT; ++x) {
+      for (int c = 0; c < 2; ++c) {
+        const int lim = qpos[c] - kPage * j - 4 * half;
 #pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        const int d = 32 * x + 8 * q4 + 4 * half;
-        uint2 pk;
-        pk.x = pack_bf16x2(o[x][4 * q4 + 0] * inv, o[x][4 * q4 + 1] * inv);
-        pk.y = pack_bf16x2(o[x][4 * q4 + 2] * inv, o[x][4 * q4 + 3] * inv);
-        *reinterpret_cast<uint2*>(orow + d) = pk;
+        for (int v = 0; v < 16; ++v) {
+          const int kp = 8 * (v >> 2) + (v & 3);
+          if (kp > lim) SA.s[c][0][v] = -INFINITY;
+          if (kp + 32 > lim) SA.s[c][1][v] = -INFINITY;
+        }
       }
     }
-    if (a.lse != nullptr && half == 0) a.lse[qrow_idx] = lse_val;
-  } else {
-    const size_t prow = (size_t)sp * a.B * a.Hq * a.C + qrow_idx;
-    float* po = a.part_o + prow * D;
+    float alpha[2];
+    bool rb_any = false;
 #pragma unroll
-    for (int x = 0; x < NDT; ++x) {
+    for (int c = 0; c < 2; ++c) {
+      float mx = -INFINITY;
 #pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        const int d = 32 * x + 8 * q4 + 4 * half;
-        *reinterpret_cast<float4*>(po + d) =
-            make_float4(o[x][4 * q4 + 0] * inv, o[x][4 * q4 + 1] * inv,
-                        o[x][4 * q4 + 2] * inv, o[x][4 * q4 + 3] * inv);
-      }
+      for (int k = 0; k < 16; ++k) mx = max3(mx, SA.s[c][0][k], SA.s[c][1][k]);
+      const float m = halves_max(mx) * a.scale_log2;
+      const bool rebase = m > m_run[c] + kRescaleSlack;
+      alpha[c] = rebase ? fast_exp2(m_run[c] - m) : 1.0f;
+      m_run[c] = rebase ? m : m_run[c];
+      rb_any |= rebase;
+      const float nmb = (m_run[c] == -INFINITY) ? 0.f : -m_run[c];
+      float ps = 0.f;
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const float e = fast_exp2(fmaf(SA.s[c][h][v], a.scale_log2, nmb));
+          SA.s[c][h][v] = e;
+          ps += e;
+        }
+      l_run[c] = l_run[c] * alpha[c] + ps;
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+        for (int x = 0; x < 8; ++x) PA.p[c][kk][x] = (__bf16)SA.s[c][kk / 2][8 * (kk % 2) + x];
     }
-    if (half == 0) a.part_lse[prow] = lse_val;
+    if (__ballot(rb_any)) {
+      fence_o<NDT>(o);
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int x = 0; x < NDT; ++x) o[c][x] *= alpha[c];
+      fence_o<NDT>(o);
+    }
+    fence_p(PA);
+    pv_page(PA, v_s0);
+    __syncthreads();
+  }
+  fence_o<NDT>(o);
+
+  // epilogue
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    const float l_tot = halves_sum(l_run[c]);
+    const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
+    const float lse_val = l_tot > 0.f ? (m_run[c] + log2f(l_tot)) * kLn2 : -INFINITY;
+    const size_t qrow_idx = ((size_t)b * a.Hq + head[c]) * a.C + tq[c];
+    if (!valid[c]) continue;
+    if (a.splits == 1) {
+      uint16_t* orow = a.out + (((size_t)b * a.C + tq[c]) * a.Hq + head[c]) * D;
+#pragma unroll
+      for (int x = 0; x < NDT; ++x) {
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const int d = 32 * x + 8 * q4 + 4 * half;
+          uint2 pk;
+          pk.x = pack_bf16x2(o[c][x][4 * q4 + 0] * inv, o[c][x][4 * q4 + 1] * inv);
+          pk.y = pack_bf16x2(o[c][x][4 * q4 + 2] * inv, o[c][x][4 * q4 + 3] * inv);
+          *reinterpret_cast<uint2*>(orow + d) = pk;
+        }
+      }
+      if (a.lse != nullptr && half == 0) a.lse[qrow_idx] = lse_val;
+    } else {
+      const size_t prow = (size_t)sp * a.B * a.Hq * a.C + qrow_idx;
+      float* po = a.part_o + prow * D;
+#pragma unroll
+      for (int x = 0; x < NDT; ++x) {
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const int d = 32 * x + 8 * q4 + 4 * half;
+          *reinterpret_cast<float4*>(po + d) =
+              make_float4(o[c][x][4 * q4 + 0] * inv, o[c][x][4 * q4 + 1] * inv,
+                          o[c][x][4 * q4 + 2] * inv, o[c][x][4 * q4 + 3] * inv);
+        }
+      }
+      if (half == 0) a.part_lse[prow] = lse_val;
+    }
   }
 }
-
 
 // Copy arm (Sec. 4.4): pack the selected K and V pages of every table row into
 // contiguous pools in table order (packed page p = table entry p of the CSR),
@@ -576,16 +724,34 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
   if (lse != nullptr && sub == 0) lse[row] = wsum > 0.f ? mx + logf(wsum) : -INFINITY;
 }
 
-int attn_query_tile(int group_size) { return kRows / group_size; }
+int attn_rows_per_workgroup(int table_mode) {
+  return 64 * (table_mode == kTablesPerQTile ? kWavesQTile : kWavesGroup);
+}
 
-int attn_base_workgroups(const Dims& d, int group_size) {
-  return d.B * (d.Hq / group_size) * (d.C / attn_query_tile(group_size));
+int attn_query_tile(int group_size, int table_mode) {
+  return attn_rows_per_workgroup(table_mode) / group_size;
+}
+
+int attn_base_workgroups(const Dims& d, int group_size, int table_mode) {
+  const int qt = attn_query_tile(group_size, table_mode);
+  return d.B * (d.Hq / group_size) * ((d.C + qt - 1) / qt);
+}
+
+int attn_resident_workgroups(int table_mode) {
+  // one wave per SIMD: 4 waves per CU on 256 CUs
+  return 256 * 4 / (attn_rows_per_workgroup(table_mode) / 64);
 }
 
 size_t attn_ws_bytes(const Dims& d, int splits) {
   if (splits <= 1) return 0;
   const size_t rows = (size_t)d.B * d.Hq * d.C;
   return (size_t)splits * rows * (d.D + 1) * sizeof(float);
+}
+
+template <int D, int NW>
+static void launch_kernel(const AttnArgs& a, bool dense, int nwg, hipStream_t st) {
+  if (dense) paged_attention_kernel<D, NW, true><<<nwg, 64 * NW, 0, st>>>(a);
+  else paged_attention_kernel<D, NW, false><<<nwg, 64 * NW, 0, st>>>(a);
 }
 
 hipError_t launch_attention(const Dims& d, const AttnLaunch& L, hipStream_t st) {
@@ -609,18 +775,20 @@ hipError_t launch_attention(const Dims& d, const AttnLaunch& L, hipStream_t st) 
   a.max_kv_blocks = d.max_kv_blocks;
   a.group_size = L.group_size;
   a.G = d.Hq / L.group_size;
-  a.n_qtiles = d.C / attn_query_tile(L.group_size);
+  const int qt = attn_query_tile(L.group_size, L.table_mode);
+  a.n_qtiles = (d.C + qt - 1) / qt;
   a.splits = L.splits;
   a.table_mode = L.table_mode;
   a.packed_pages = L.packed_pages;
   a.scale_log2 = L.sm_scale * kLog2e;
-  const int nwg = attn_base_workgroups(d, L.group_size) * L.splits;
+  const int nwg = attn_base_workgroups(d, L.group_size, L.table_mode) * L.splits;
+  const bool qtile = L.table_mode == kTablesPerQTile;
   if (d.D == 128) {
-    if (L.dense) paged_attention_kernel<128, true><<<nwg, 256, 0, st>>>(a);
-    else paged_attention_kernel<128, false><<<nwg, 256, 0, st>>>(a);
+    if (qtile) launch_kernel<128, kWavesQTile>(a, L.dense, nwg, st);
+    else launch_kernel<128, kWavesGroup>(a, L.dense, nwg, st);
   } else {
-    if (L.dense) paged_attention_kernel<64, true><<<nwg, 256, 0, st>>>(a);
-    else paged_attention_kernel<64, false><<<nwg, 256, 0, st>>>(a);
+    if (qtile) launch_kernel<64, kWavesQTile>(a, L.dense, nwg, st);
+    else launch_kernel<64, kWavesGroup>(a, L.dense, nwg, st);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || L.splits == 1) return e;

@@ -70,8 +70,10 @@ struct AttnLaunch {
   int table_mode = kTablesPerGroup;
   long long packed_pages = 0;
 };
-int attn_query_tile(int group_size);                    // chunk queries per workgroup
-int attn_base_workgroups(const Dims& d, int group_size);
+int attn_rows_per_workgroup(int table_mode);             // (head, query) rows per workgroup
+int attn_query_tile(int group_size, int table_mode);     // chunk queries per workgroup
+int attn_base_workgroups(const Dims& d, int group_size, int table_mode);
+int attn_resident_workgroups(int table_mode);            // workgroups the GPU holds at once
 size_t attn_ws_bytes(const Dims& d, int splits);
 hipError_t launch_attention(const Dims& d, const AttnLaunch& a, hipStream_t st);
 hipError_t launch_gather(const Dims& d, const uint16_t* k_pool, const uint16_t* v_pool,
