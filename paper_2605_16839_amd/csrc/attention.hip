@@ -107,6 +107,22 @@ __device__ __forceinline__ void page_to_lds(const uint16_t* __restrict__ src, ui
   }
 }
 
+// One of the 1 KB copy instructions of page_to_lds (instruction m of this
+// wave), so that a step can spread its copies between MFMAs.
+template <int D, int NW, bool IS_V>
+__device__ __forceinline__ void page_part_to_lds(const uint16_t* __restrict__ src, uint16_t* tile,
+                                                 int wv, int lane, int m) {
+  constexpr int CPR = D / 8;
+  constexpr int ROWS_PER_INST = 64 / CPR;
+  constexpr int INST_PER_WAVE = (64 * D * 2) / 1024 / NW;
+  const int inst = wv * INST_PER_WAVE + m;
+  const int r = inst * ROWS_PER_INST + lane / CPR;
+  const int cpos = lane % CPR;
+  const int c = IS_V ? v_swz<D>(r, cpos) : k_swz<D>(r, cpos);
+  const uint32_t off = (uint32_t)(r * D + c * 8);
+  __builtin_amdgcn_global_load_lds(src + off, (lds_void*)(tile + inst * 512), 16, 0, 0);
+}
+
 // Wait for this wave's direct-to-LDS copies and tell the compiler that the
 // tiles behind the pointers changed (the copies write them outside its view).
 __device__ __forceinline__ void tile_written(const void* tile) {
@@ -182,6 +198,12 @@ __device__ __forceinline__ void fence_o(f32x16 (&o)[2][NDT]) {
 
 // Fences on S^T tiles (MFMA results about to be read by the softmax) and on
 // P^T fragments (VALU results about to be read by MFMAs).
+__device__ __forceinline__ void fence_sp(SPage& s, PFrag& p) {
+  asm volatile("s_nop 7\n s_nop 7\n s_nop 4"
+               : "+v"(s.s[0][0]), "+v"(s.s[0][1]), "+v"(s.s[1][0]), "+v"(s.s[1][1]),
+                 "+v"(p.p[0][0]), "+v"(p.p[0][1]), "+v"(p.p[0][2]), "+v"(p.p[0][3]),
+                 "+v"(p.p[1][0]), "+v"(p.p[1][1]), "+v"(p.p[1][2]), "+v"(p.p[1][3]));
+}
 __device__ __forceinline__ void fence_s(SPage& s) {
   asm volatile("s_nop 7\n s_nop 7\n s_nop 5"
                : "+v"(s.s[0][0]), "+v"(s.s[0][1]), "+v"(s.s[1][0]), "+v"(s.s[1][1]));
@@ -220,6 +242,8 @@ __global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnA
   constexpr int NQK = 2 * NKS;         // K fragments per page
   constexpr int NFRAG = NPV + NQK;
   constexpr int NSLOT = 2 * NFRAG;     // one MFMA per slot
+  constexpr int DMA_PER_STEP = 2 * (64 * D * 2) / 1024 / NW;   // copy instructions per wave
+  constexpr int DMA_STRIDE = (NSLOT / 2) / DMA_PER_STEP > 0 ? (NSLOT / 2) / DMA_PER_STEP : 1;
   constexpr int MAXS = 10;             // slots holding the max / rebase work
   __shared__ __attribute__((aligned(1024))) uint16_t k_s0[PAGE];
   __shared__ __attribute__((aligned(1024))) uint16_t k_s1[PAGE];
@@ -432,20 +456,30 @@ __global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnA
     uint16_t* const v_dma = P ? v_s1 : v_s0;
     const uint16_t* const v_rd = P ? v_s0 : v_s1;
     const int i2 = i + 2 < n_pipe ? i + 2 : n_pipe - 1;
-    page_to_lds<D, NW, false>(page_ptr(a.k_pool, i2), k_dma, wv, lane);
-    page_to_lds<D, NW, true>(page_ptr(a.v_pool, i), v_dma, wv, lane);
-    fence_s(sc);
-    fence_p(po);
+    const uint16_t* const k_src = page_ptr(a.k_pool, i2);
+    const uint16_t* const v_src = page_ptr(a.v_pool, i);
+    fence_sp(sc, po);
     float mx[2] = {-INFINITY, -INFINITY}, alpha[2] = {1.f, 1.f}, nmb[2] = {0.f, 0.f};
     float ps[2] = {0.f, 0.f};
     bool rb_any = false;
     bf16x8 fr[NFRAG];
     fr[0] = load_frag(0, v_rd, k_rd);
     fr[1] = load_frag(1, v_rd, k_rd);
+    fr[2] = load_frag(2, v_rd, k_rd);
     static_for<NSLOT>([&](auto stag) __attribute__((always_inline)) {
       constexpr int s = decltype(stag)::value;
       constexpr int F = s / 2, c = s % 2;
-      if constexpr (c == 0 && F + 2 < NFRAG) fr[F + 2] = load_frag(F + 2, v_rd, k_rd);
+      if constexpr (c == 0 && F + 3 < NFRAG) fr[F + 3] = load_frag(F + 3, v_rd, k_rd);
+      // the copies of K(i+2) and V(i), one instruction every DMA_STRIDE slots
+      // over the first half of the step (issued all at once they queue in
+      // the address unit and stall the wave)
+      if constexpr (s % DMA_STRIDE == 0 && s / DMA_STRIDE < DMA_PER_STEP) {
+        constexpr int m = s / DMA_STRIDE;
+        if constexpr (m < DMA_PER_STEP / 2)
+          page_part_to_lds<D, NW, false>(k_src, k_dma, wv, lane, m);
+        else
+          page_part_to_lds<D, NW, true>(v_src, v_dma, wv, lane, m - DMA_PER_STEP / 2);
+      }
       if constexpr (F < NPV) {
         mfma_o(o[c][F % NDT], fr[F], po.p[c][F / NDT]);
       } else {
