@@ -30,17 +30,25 @@
  *   K page and the V page.  page_table is int32 [B, Hkv, max_kv_blocks];
  *   entries at j >= nKB_b are ignored.
  * - Per sequence b: cached_len[b] tokens are already in the cache and the
- *   chunk adds chunk_len tokens, so nC_b = cached_len[b] / page_size cached
- *   blocks and nKB_b = nC_b + chunk_len / page_size blocks in total; chunk
- *   token t sits at absolute position cached_len[b] + t, key r of block j at
- *   page_size * j + r.
+ *   chunk adds chunk_len tokens (any lengths).  Chunk token t sits at
+ *   absolute position cached_len[b] + t, key r of block j at
+ *   page_size * j + r.  nC_b = floor(cached_len[b] / page_size) blocks are
+ *   full of cached tokens (the candidates of the selector); the sequence
+ *   occupies nKB_b = ceil((cached_len[b] + chunk_len) / page_size) blocks.
+ *   A block holding both cached and chunk tokens counts as a chunk block.
+ *   The rows of a sequence's last page past its end (cached_len[b] +
+ *   chunk_len) are not part of it and may hold anything, NaN included:
+ *   pooling does not read them and attention gives them no weight.  Every
+ *   page of the pool is nevertheless read whole, so it must be allocated
+ *   whole (page_size rows).
  * - Query head h belongs to KV head h / (Hq / Hkv) and to execution group
  *   h / group_size (contiguous heads, Sec. 3.2 and App. B.1: the KV group by
  *   default, or 4-head sub-groups of a larger KV group).  group_size must
  *   divide Hq / Hkv.
  * - Masks are uint64 [B, Hq, nQB, W], W = ceil(max_kv_blocks / 64),
- *   nQB = chunk_len / q_block: bit (j & 63) of word (j >> 6) of row (b,h,i)
- *   is M[b,h,i,j].  Only blocks j < nKB_b are meaningful.
+ *   nQB = ceil(chunk_len / q_block) (the last Q-block may hold fewer than
+ *   q_block queries): bit (j & 63) of word (j >> 6) of row (b,h,i) is
+ *   M[b,h,i,j].  Only blocks j < nKB_b are meaningful.
  * - Tables: kv_indptr int32 [B*G + 1] and kv_indices int32 (capacity
  *   B*G*max_kv_blocks); row r = b*G + g lists T[b,g] as ascending LOGICAL
  *   block ids in kv_indices[kv_indptr[r] .. kv_indptr[r+1]).
@@ -61,13 +69,13 @@
 extern "C" {
 #endif
 
-#define CA_ABI_VERSION 2
+#define CA_ABI_VERSION 3
 
 typedef enum ca_status {
   CA_OK = 0,
   CA_ERR_NULL = 1,          /* a required pointer is NULL                       */
   CA_ERR_SHAPE = 2,         /* a size is out of range or inconsistent           */
-  CA_ERR_UNALIGNED = 3,     /* a length is not a multiple of page_size/q_block  */
+  CA_ERR_UNALIGNED = 3,     /* no longer returned: any lengths are accepted     */
   CA_ERR_GROUP = 4,         /* group_size does not divide Hq / Hkv              */
   CA_ERR_WORKSPACE = 5,     /* workspace missing or too small                   */
   CA_ERR_UNSUPPORTED = 6,   /* head_dim / page_size / q_block not built for     */
@@ -82,9 +90,9 @@ typedef struct ca_problem {
   int32_t head_dim;          /* D, 64 or 128                                    */
   int32_t page_size;         /* tokens per KV block == page; must be 64         */
   int32_t q_block;           /* query block of the masks: 64 or 128             */
-  int32_t chunk_len;         /* C >= 1; multiple of page_size and q_block       */
+  int32_t chunk_len;         /* C >= 1, any length                              */
   int32_t max_kv_blocks;     /* row stride of page_table, >= max_b nKB_b, <= 16384 */
-  const int32_t* cached_len_host; /* HOST [B]: multiples of page_size, may be 0 */
+  const int32_t* cached_len_host; /* HOST [B]: >= 0, any length                 */
   const int32_t* cached_len;      /* DEVICE [B]: the same values                */
 } ca_problem;
 
@@ -99,15 +107,20 @@ ca_status ca_check_problem(const ca_problem* p, int32_t group_size);
 
 /* ------------------------------------------------------------------------
  * 1. Estimator (the selector; see the file header).  Stage by stage:
- *    q_mean[b,h,i]   = mean of the q_block query rows of Q-block i, head h
- *    k_mean[b,kvh,j] = mean of the page_size key rows of block j
+ *    q_mean[b,h,i]   = mean of the query rows of Q-block i, head h (the
+ *                      last Q-block's mean is over the rows it holds)
+ *    k_mean[b,kvh,j] = mean of the key rows of block j before the sequence
+ *                      end (all page_size rows but in a partial last block)
  *    scores[b,h,i,j] = q_mean[b,h,i] . k_mean[b,kvh(h),j], j < nC_b
  *    masks: top k = ceil(top_frac * nC_b) (float32 product, at most nC_b)
  *           cached blocks per row by score descending then j ascending
  *           (-0.0 ranks equal to +0.0), OR sink blocks {0..sink_blocks-1},
  *           OR the local window {nC_b-local_blocks .. nC_b-1}, OR the
- *           chunk-causal blocks {nC_b .. nC_b + (i+1)*q_block/page_size - 1},
- *           all clipped to [0, nKB_b); every other bit of the row is 0.
+ *           chunk-causal blocks {nC_b .. e_i - 1}, e_i = 1 + the block that
+ *           holds the last query of Q-block i, i.e.
+ *           e_i = (cached_len + min((i+1)*q_block, C) - 1) / page_size + 1
+ *           (nC_b + (i+1)*q_block/page_size for aligned lengths), all
+ *           clipped to [0, nKB_b); every other bit of the row is 0.
  * Pooling and scores accumulate in float32.
  * ---------------------------------------------------------------------- */
 
@@ -118,7 +131,8 @@ ca_status ca_pool_q_blocks(const ca_problem* p, const uint16_t* q, float* q_mean
 /* k_mean fp32 [B, Hkv, max_kv_blocks, D]: blocks j in [first_block, nKB_b) of
  * every sequence are (re)computed from k_pool; the others are left untouched,
  * so a caller that keeps k_mean across chunks passes first_block = the number
- * of blocks pooled by earlier chunks. */
+ * of blocks that were full when earlier chunks pooled them (a block pooled
+ * while partial has to be pooled again; min_b nC_b is always safe). */
 ca_status ca_pool_k_blocks(const ca_problem* p, const uint16_t* k_pool,
                            const int32_t* page_table, int32_t first_block,
                            float* k_mean, void* stream);
@@ -250,7 +264,7 @@ ca_status ca_dense_paged_chunk_attention(const ca_problem* p, const uint16_t* q,
  *    (b,h,i) = the set bits j < nKB_b of its own mask row M[b,h,i,:]
  *    (the raw mask executed directly); group_size > 0: row (b,h,i) = the
  *    union table T[b, h/group_size] of section 2, limited to the blocks
- *    Q-block i can see (j < nC_b + (i+1)*q_block/page_size), which is the
+ *    Q-block i can see (j < e_i of section 1), which is the
  *    same unioned mask the zero-copy path executes (the matched-table
  *    ablation of Sec. 4.4).
  *    Workspace: ca_block_sparse_tables_workspace_bytes(p, group_size).
@@ -306,7 +320,8 @@ ca_status ca_packed_chunk_attention(const ca_problem* p, const uint16_t* q,
  * Debug helper: synchronises `stream`, copies the tables to the host and
  * checks kv_indptr[0] == 0, non-decreasing row bounds within capacity,
  * entries strictly ascending and < nKB_b, and (if require_chunk_open) that
- * every chunk block nC_b..nKB_b-1 is present.  Returns CA_ERR_INVALID_TABLE
+ * every chunk block nC_b..nKB_b-1 is present (nC_b = floor(cached_len /
+ * page_size), nKB_b = ceil((cached_len + chunk_len) / page_size)).  Returns CA_ERR_INVALID_TABLE
  * with a description in ca_last_error_detail() on the first violation.
  * ---------------------------------------------------------------------- */
 ca_status ca_validate_tables(const ca_problem* p, int32_t group_size,

@@ -28,7 +28,7 @@ from .bf16 import bf16_to_f64  # noqa: F401
 from .estimator import (  # noqa: F401
     q_block_means, k_block_means, block_scores, select_top_blocks,
     masks_from_scores, n_selected, estimate_masks, EstimatorParams, threshold_margin,
-    select_threshold_blocks, masks_from_threshold,
+    select_threshold_blocks, masks_from_threshold, n_kv_blocks, causal_block_end,
 )
 from .tables import unpack_masks, block_tables, tables_to_csr, union_densities  # noqa: F401
 from .attention import (  # noqa: F401

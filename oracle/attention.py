@@ -7,7 +7,10 @@ sequence b (absolute position p = cached_len_b + t):
    (``k_pool[page_table[b, kvh, j]]``), in table order, together with each
    key's absolute position 64*j + r -- an explicit gather, which is exactly
    the copy that zero-copy execution avoids (Sec. 3.3) and so an independent
-   way of computing what the in-place kernel must produce;
+   way of computing what the in-place kernel must produce.  Only keys at
+   positions before the sequence end cached_len_b + C exist: the rows of the
+   last page past it (a length that is not a multiple of 64) are not part of
+   the sequence and are dropped, whatever they hold;
 2. z = sm_scale * q . k for every gathered key, with z = -inf where the key
    position exceeds p (causal masking in absolute positions, App. B.2 last
    paragraph: positions come from the logical block id, never from a key's
@@ -33,15 +36,19 @@ from .bf16 import bf16_to_f64
 
 
 def gather_selected(k_pool_bits, v_pool_bits, page_table, b: int, kvh: int,
-                    table: Sequence[int]) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
-    """Explicit copy of the selected pages: Ksel, Vsel [n*page, D] and key positions."""
+                    table: Sequence[int],
+                    seq_len: Optional[int] = None) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """Explicit copy of the selected pages: Ksel, Vsel [n, D] and key positions.
+
+    Rows at positions >= ``seq_len`` (when given) are left out."""
     page = k_pool_bits.shape[1]
     ks, vs, pos = [], [], []
     for j in table:
         pid = page_table[b, kvh, j]
-        ks.append(bf16_to_f64(k_pool_bits[pid]))
-        vs.append(bf16_to_f64(v_pool_bits[pid]))
-        pos.append(page * int(j) + np.arange(page))
+        rows = page if seq_len is None else max(0, min(page, int(seq_len) - page * int(j)))
+        ks.append(bf16_to_f64(k_pool_bits[pid][:rows]))
+        vs.append(bf16_to_f64(v_pool_bits[pid][:rows]))
+        pos.append(page * int(j) + np.arange(rows))
     D = k_pool_bits.shape[2]
     if not ks:
         return np.zeros((0, D)), np.zeros((0, D)), np.zeros(0, dtype=np.int64)
@@ -73,7 +80,8 @@ def attention_rows(q: np.ndarray, qpos: np.ndarray, ksel: np.ndarray,
 
 
 def dense_tables(n_blocks: Sequence[int], num_groups: int) -> List[List[List[int]]]:
-    """T[b][g] = every block of sequence b (the all-ones mask)."""
+    """T[b][g] = every block of sequence b (the all-ones mask); n_blocks[b] = nKB_b
+    = ceil((cached_len_b + C) / 64)."""
     return [[list(range(int(n))) for _ in range(num_groups)] for n in n_blocks]
 
 
@@ -110,7 +118,7 @@ def chunk_attention(q_bits: np.ndarray, k_pool_bits: np.ndarray,
     for (b, g), hs in by_group.items():
         kvh = (g * group_size) // ratio
         ksel, vsel, kpos = gather_selected(k_pool_bits, v_pool_bits, page_table,
-                                           b, kvh, tables[b][g])
+                                           b, kvh, tables[b][g], int(cached_len[b]) + C)
         qpos = int(cached_len[b]) + t_idx
         for h in hs:
             q = bf16_to_f64(q_bits[b, t_idx, h, :])
@@ -137,20 +145,20 @@ def block_sparse_attention(q_bits: np.ndarray, k_pool_bits: np.ndarray,
     B, C, Hq, D = q_bits.shape
     Hkv = page_table.shape[1]
     ratio = Hq // Hkv
-    chunk_blocks = C // k_pool_bits.shape[1]
+    page = k_pool_bits.shape[1]
     if heads is None:
         heads = [(b, h) for b in range(B) for h in range(Hq)]
     t_all = np.arange(C) if queries is None else np.asarray(queries)
     out = np.full((B, C, Hq, D), np.nan)
     lse = np.full((B, Hq, C), np.nan)
     for (b, h) in heads:
-        nkb = int(cached_len[b]) // k_pool_bits.shape[1] + chunk_blocks
+        nkb = -(-(int(cached_len[b]) + C) // page)
         kvh = h // ratio
         for i in sorted(set((t_all // q_block).tolist())):
             t_idx = t_all[t_all // q_block == i]
             table = [j for j in range(nkb) if mask_bits[b, h, i, j]]
             ksel, vsel, kpos = gather_selected(k_pool_bits, v_pool_bits, page_table,
-                                               b, kvh, table)
+                                               b, kvh, table, int(cached_len[b]) + C)
             q = bf16_to_f64(q_bits[b, t_idx, h, :])
             o, l = attention_rows(q, int(cached_len[b]) + t_idx, ksel, vsel, kpos, sm_scale)
             out[b, t_idx, h, :] = o

@@ -165,7 +165,7 @@ class Problem:
 
     @property
     def n_qblocks(self) -> int:
-        return self.chunk_len // self.q_block
+        return -(-self.chunk_len // self.q_block)
 
     @property
     def words(self) -> int:

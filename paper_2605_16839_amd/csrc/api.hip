@@ -53,24 +53,20 @@ ca_status check(const ca_problem* p, int32_t group_size, ca::Dims* d) {
   if (p->q_block != 64 && p->q_block != 128)
     return fail(CA_ERR_UNSUPPORTED, "q_block %d not supported (64, 128)", p->q_block);
   if (p->chunk_len < 1) return fail(CA_ERR_SHAPE, "chunk_len must be >= 1");
-  if (p->chunk_len % p->page_size != 0 || p->chunk_len % p->q_block != 0)
-    return fail(CA_ERR_UNALIGNED, "chunk_len %d must be a multiple of page_size and q_block",
-                p->chunk_len);
   if (p->max_kv_blocks < 1 || p->max_kv_blocks > ca::kMaxKvBlocks)
     return fail(CA_ERR_SHAPE, "max_kv_blocks %d out of range [1, %d]", p->max_kv_blocks,
                 ca::kMaxKvBlocks);
-  const int chunk_blocks = p->chunk_len / p->page_size;
-  int max_nc = 0;
+  int max_nc = 0, max_nkb = 0;
   for (int b = 0; b < p->batch; ++b) {
     const int c = p->cached_len_host[b];
-    if (c < 0 || c % p->page_size != 0)
-      return fail(CA_ERR_UNALIGNED, "cached_len[%d] = %d is not a non-negative multiple of %d",
-                  b, c, p->page_size);
-    const long long nkb = (long long)(c / p->page_size) + chunk_blocks;
+    if (c < 0) return fail(CA_ERR_SHAPE, "cached_len[%d] = %d is negative", b, c);
+    // any lengths: the last block of a sequence may be partial
+    const long long nkb = ((long long)c + p->chunk_len + p->page_size - 1) / p->page_size;
     if (nkb > p->max_kv_blocks)
       return fail(CA_ERR_SHAPE, "sequence %d needs %lld blocks > max_kv_blocks %d", b, nkb,
                   p->max_kv_blocks);
     if (c / p->page_size > max_nc) max_nc = c / p->page_size;
+    if (nkb > max_nkb) max_nkb = (int)nkb;
   }
   if (group_size > 0) {
     const int ratio = p->num_q_heads / p->num_kv_heads;
@@ -86,11 +82,10 @@ ca_status check(const ca_problem* p, int32_t group_size, ca::Dims* d) {
     d->q_block = p->q_block;
     d->C = p->chunk_len;
     d->max_kv_blocks = p->max_kv_blocks;
-    d->nqb = p->chunk_len / p->q_block;
+    d->nqb = (p->chunk_len + p->q_block - 1) / p->q_block;
     d->W = (p->max_kv_blocks + 63) / 64;
-    d->chunk_blocks = chunk_blocks;
     d->max_nc = max_nc;
-    d->max_nkb = max_nc + chunk_blocks;
+    d->max_nkb = max_nkb;
   }
   return ok();
 }
@@ -544,7 +539,7 @@ ca_status ca_validate_tables(const ca_problem* p, int32_t group_size, const int3
   for (int r = 0; r < R; ++r) {
     const int b = r / G;
     const int nc = p->cached_len_host[b] / d.page;
-    const int nkb = nc + d.chunk_blocks;
+    const int nkb = ca::blocks_for(p->cached_len_host[b] + d.C);
     int prev = -1, chunk_seen = 0;
     for (int x = ip[r]; x < ip[r + 1]; ++x) {
       const int j = ix[x];
@@ -554,9 +549,9 @@ ca_status ca_validate_tables(const ca_problem* p, int32_t group_size, const int3
       if (j >= nc) ++chunk_seen;
       prev = j;
     }
-    if (require_chunk_open && chunk_seen != d.chunk_blocks)
+    if (require_chunk_open && chunk_seen != nkb - nc)
       return fail(CA_ERR_INVALID_TABLE, "row %d holds %d of the %d chunk blocks", r, chunk_seen,
-                  d.chunk_blocks);
+                  nkb - nc);
   }
   return ok();
 }

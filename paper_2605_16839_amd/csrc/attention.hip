@@ -280,8 +280,7 @@ __global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnA
   }
   const int kvh = (g * gs) / (a.Hq / a.Hkv);
   const int cl = a.cached_len[b];
-  const int nc = cl / kPage;
-  const int nkb = nc + a.C / kPage;
+  const int nkb = blocks_for(cl + a.C);
   const int qpos[2] = {cl + tq[0], cl + tq[1]};
   const int j_last = (cl + q_end - 1) / kPage;     // last block any row can see
   const int mask_from = cl + q0;                   // keys beyond this need masking
@@ -323,7 +322,9 @@ __global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnA
 
   int e_end = e1;
   if (DENSE) {
+    // a split may start past the tile's last visible block: then it is empty
     e_end = e1 < j_last + 1 ? e1 : j_last + 1;
+    e_end = e_end > e0 ? e_end : e0;
   } else {
     while (e_end > e0 && a.kv_indices[tbase + e_end - 1] > j_last) --e_end;
   }
@@ -564,6 +565,17 @@ __global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnA
     page_to_lds<D, NW, true>(page_ptr(a.v_pool, i), v_s0, wv, lane);
     copies_landed(k_s0, v_s0);
     __syncthreads();
+    if (i >= n_main) {
+      // The rows of a sequence's last page past its end are not part of it
+      // and may hold anything: their weights are exactly 0, so their V rows
+      // are zeroed to keep 0 * NaN out of O (their K scores are masked).
+      const int past = kPage * id_of(blk_cur, blk_nxt, i) + kPage - (cl + a.C);
+      if (past > 0) {
+        uint4* vz = reinterpret_cast<uint4*>(v_s0 + (kPage - past) * D);
+        for (int x = t; x < past * D / 8; x += 64 * NW) vz[x] = make_uint4(0u, 0u, 0u, 0u);
+        __syncthreads();
+      }
+    }
     qk_page(SA, k_s0);
     fence_s(SA);
     if (i >= n_main) {

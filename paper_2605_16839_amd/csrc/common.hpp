@@ -33,6 +33,19 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return (uint32_t)float_to_bf16_bits(lo) | ((uint32_t)float_to_bf16_bits(hi) << 16);
 }
 
+// Blocks holding at least one of `len` tokens (a sequence's last block may be
+// partial).
+__host__ __device__ __forceinline__ int blocks_for(int len) { return (len + kPage - 1) / kPage; }
+
+// One past the last chunk-causal block of Q-block i: the block that holds the
+// Q-block's last query (chunk token t sits at position cached_len + t; the
+// last Q-block of a chunk may hold fewer than q_block queries).
+__host__ __device__ __forceinline__ int causal_block_end(int cached_len, int C, int i,
+                                                         int q_block) {
+  const int last = (i + 1) * q_block < C ? (i + 1) * q_block - 1 : C - 1;
+  return (cached_len + last) / kPage + 1;
+}
+
 __device__ __forceinline__ int lane_id() { return __lane_id(); }
 
 template <typename T>

@@ -63,32 +63,39 @@ __global__ __launch_bounds__(256) void pool_q_kernel(const uint16_t* __restrict_
   const int h = (w / nqb) % Hq;
   const int b = w / (nqb * Hq);
   const int wv = threadIdx.x >> 6;
-  const int rows = q_block / 4;
-  const uint16_t* base = q + (((size_t)b * C + (size_t)i * q_block + (size_t)wv * rows) * Hq + h) * D;
+  const int quarter = q_block / 4;
+  // the chunk's last Q-block may hold fewer rows; its mean is over those
+  const int n_valid = C - i * q_block < q_block ? C - i * q_block : q_block;
+  int rows = n_valid - wv * quarter;
+  rows = rows < 0 ? 0 : (rows > quarter ? quarter : rows);
+  const uint16_t* base =
+      q + (((size_t)b * C + (size_t)i * q_block + (size_t)wv * quarter) * Hq + h) * D;
   pool_rows<D>(base, (size_t)Hq * D, rows, part[wv], 1.0f);
   __syncthreads();
   const int t = threadIdx.x;
   if (t < D)
     q_mean[(size_t)w * D + t] = ((part[0][t] + part[1][t]) + (part[2][t] + part[3][t])) *
-                                (1.0f / (float)q_block);
+                                (1.0f / (float)n_valid);
 }
 
-// One wave per (b, kvh, j), j in [first_block, nKB_b).
+// One wave per (b, kvh, j), j in [first_block, nKB_b).  A sequence's last
+// block is pooled over its rows before the sequence end only.
 template <int D>
 __global__ __launch_bounds__(256) void pool_k_kernel(const uint16_t* __restrict__ k_pool,
                                                      const int32_t* __restrict__ page_table,
                                                      const int32_t* __restrict__ cached_len,
                                                      float* __restrict__ k_mean, int Hkv,
-                                                     int max_kv_blocks, int chunk_blocks,
+                                                     int max_kv_blocks, int C,
                                                      int first_block) {
   const int bk = blockIdx.y;  // b * Hkv + kvh
   const int b = bk / Hkv;
   const int j = first_block + blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int nkb = cached_len[b] / kPage + chunk_blocks;
-  if (j >= nkb) return;
+  const int seq = cached_len[b] + C;
+  if (j >= blocks_for(seq)) return;
+  const int rows = seq - kPage * j < kPage ? seq - kPage * j : kPage;
   const int page = page_table[(size_t)bk * max_kv_blocks + j];
-  pool_rows<D>(k_pool + (size_t)page * kPage * D, D, kPage,
-               k_mean + ((size_t)bk * max_kv_blocks + j) * D, 1.0f / (float)kPage);
+  pool_rows<D>(k_pool + (size_t)page * kPage * D, D, rows,
+               k_mean + ((size_t)bk * max_kv_blocks + j) * D, 1.0f / (float)rows);
 }
 
 // ---------------------------------------------------------------------------
@@ -192,7 +199,7 @@ __global__ __launch_bounds__(256) void select_kernel(const float* __restrict__ s
                                                      const int32_t* __restrict__ cached_len,
                                                      uint64_t* __restrict__ masks, int Hq,
                                                      int nqb, int max_kv_blocks, int W,
-                                                     int chunk_blocks, int qblock_blocks,
+                                                     int C, int q_block,
                                                      float top_frac, int sink_blocks,
                                                      int local_blocks,
                                                      unsigned long long* __restrict__ gwords,
@@ -206,8 +213,9 @@ __global__ __launch_bounds__(256) void select_kernel(const float* __restrict__ s
   const int wv = t >> 6;
   const int i = row % nqb;
   const int b = row / (nqb * Hq);
-  const int nc = cached_len[b] / kPage;
-  const int nkb = nc + chunk_blocks;
+  const int cl = cached_len[b];
+  const int nc = cl / kPage;            // full cached blocks: the candidates
+  const int nkb = blocks_for(cl + C);
   int k = 0;
   if (nc > 0) {
     k = (int)ceilf(top_frac * (float)nc);
@@ -247,7 +255,7 @@ __global__ __launch_bounds__(256) void select_kernel(const float* __restrict__ s
   }
   const uint32_t T = prefix;
 
-  const int causal_end = nc + (i + 1) * qblock_blocks;
+  const int causal_end = causal_block_end(cl, C, i, q_block);
   const int sink_end = sink_blocks < nc ? sink_blocks : nc;
   const int local_begin = nc - local_blocks;
   int carry = 0;  // keys equal to T already seen, in block order
@@ -291,16 +299,17 @@ __global__ __launch_bounds__(256) void select_kernel(const float* __restrict__ s
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void threshold_select_kernel(
     const float* __restrict__ scores, const int32_t* __restrict__ cached_len,
-    uint64_t* __restrict__ masks, int Hq, int nqb, int max_kv_blocks, int W, int chunk_blocks,
-    int qblock_blocks, float margin, int sink_blocks, int local_blocks) {
+    uint64_t* __restrict__ masks, int Hq, int nqb, int max_kv_blocks, int W, int C,
+    int q_block, float margin, int sink_blocks, int local_blocks) {
   __shared__ float red[4];
   const int row = blockIdx.x;
   const int t = threadIdx.x;
   const int wv = t >> 6;
   const int i = row % nqb;
   const int b = row / (nqb * Hq);
-  const int nc = cached_len[b] / kPage;
-  const int nkb = nc + chunk_blocks;
+  const int cl = cached_len[b];
+  const int nc = cl / kPage;
+  const int nkb = blocks_for(cl + C);
   const float* s = scores + (size_t)row * max_kv_blocks;
   float mx = -INFINITY;
   for (int j = t; j < nc; j += 256) mx = fmaxf(mx, s[j]);
@@ -310,7 +319,7 @@ __global__ __launch_bounds__(256) void threshold_select_kernel(
   __syncthreads();
   mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
   const float thr = mx + margin;
-  const int causal_end = nc + (i + 1) * qblock_blocks;
+  const int causal_end = causal_block_end(cl, C, i, q_block);
   const int sink_end = sink_blocks < nc ? sink_blocks : nc;
   const int local_begin = nc - local_blocks;
   uint64_t* mrow = masks + (size_t)row * W;
@@ -348,10 +357,10 @@ hipError_t launch_pool_k(const Dims& d, const uint16_t* k_pool, const int32_t* p
   dim3 grid((span + 3) / 4, d.B * d.Hkv);
   if (d.D == 128)
     pool_k_kernel<128><<<grid, 256, 0, st>>>(k_pool, page_table, cached_len, k_mean, d.Hkv,
-                                             d.max_kv_blocks, d.chunk_blocks, first_block);
+                                             d.max_kv_blocks, d.C, first_block);
   else
     pool_k_kernel<64><<<grid, 256, 0, st>>>(k_pool, page_table, cached_len, k_mean, d.Hkv,
-                                            d.max_kv_blocks, d.chunk_blocks, first_block);
+                                            d.max_kv_blocks, d.C, first_block);
   return hipGetLastError();
 }
 
@@ -380,8 +389,8 @@ hipError_t launch_select(const Dims& d, const float* scores, const int32_t* cach
   dim3 grid(d.B * d.Hq * d.nqb);
   const size_t lds = (size_t)(d.max_nc > 0 ? d.max_nc : 1) * sizeof(uint32_t);
   select_kernel<<<grid, 256, lds, st>>>(scores, cached_len, masks, d.Hq, d.nqb,
-                                        d.max_kv_blocks, d.W, d.chunk_blocks,
-                                        d.q_block / kPage, top_frac, sink_blocks, local_blocks,
+                                        d.max_kv_blocks, d.W, d.C, d.q_block, top_frac,
+                                        sink_blocks, local_blocks,
                                         reinterpret_cast<unsigned long long*>(group_words),
                                         group_size);
   return hipGetLastError();
@@ -393,9 +402,8 @@ hipError_t launch_threshold_select(const Dims& d, const float* scores, const int
                                    uint64_t* masks, hipStream_t st) {
   dim3 grid(d.B * d.Hq * d.nqb);
   threshold_select_kernel<<<grid, 256, 0, st>>>(scores, cached_len, masks, d.Hq, d.nqb,
-                                                d.max_kv_blocks, d.W, d.chunk_blocks,
-                                                d.q_block / kPage, margin, sink_blocks,
-                                                local_blocks);
+                                                d.max_kv_blocks, d.W, d.C, d.q_block,
+                                                margin, sink_blocks, local_blocks);
   return hipGetLastError();
 }
 

@@ -8,11 +8,10 @@ namespace ca {
 // Validated problem sizes, derived once on the host.
 struct Dims {
   int B, Hq, Hkv, D, page, q_block, C, max_kv_blocks;
-  int nqb;           // C / q_block
+  int nqb;           // ceil(C / q_block)
   int W;             // mask words per row
-  int chunk_blocks;  // C / page
-  int max_nc;        // max_b cached blocks
-  int max_nkb;       // max_b cached + chunk blocks
+  int max_nc;        // max_b full cached blocks, floor(cached_len_b / page)
+  int max_nkb;       // max_b blocks of the sequence, ceil((cached_len_b + C) / page)
 };
 
 hipError_t launch_pool_q(const Dims& d, const uint16_t* q, float* q_mean, hipStream_t st,

@@ -23,13 +23,13 @@ __global__ __launch_bounds__(256) void union_kernel(const uint64_t* __restrict__
                                                     uint64_t* __restrict__ gwords,
                                                     int32_t* __restrict__ counts, int Hq,
                                                     int nqb, int W, int group_size, int G,
-                                                    int chunk_blocks) {
+                                                    int C) {
   __shared__ unsigned long long acc[kMaxWords];
   __shared__ int red[4];
   const int r = blockIdx.x;
   const int b = r / G, g = r % G;
   const int t = threadIdx.x;
-  const int nkb = cached_len[b] / kPage + chunk_blocks;
+  const int nkb = blocks_for(cached_len[b] + C);
   for (int w = t; w < W; w += 256) acc[w] = 0ull;
   __syncthreads();
   const int rows = group_size * nqb;
@@ -147,14 +147,15 @@ hipError_t launch_compact_words(const Dims& d, int rows, const uint64_t* words,
 
 // Block-sparse arm at matched tables (Sec. 4.4): the union of execution group
 // g(h) as the mask row of every (b, h, Q-block i), limited to the blocks that
-// Q-block i can see causally (j < nC_b + (i+1)*q_block/page).  One workgroup
-// per (b, h, i) row; words from the group rows written by union_kernel.
+// Q-block i can see causally (up to the block holding its last query).  One
+// workgroup per (b, h, i) row; words from the group rows written by
+// union_kernel.
 __global__ __launch_bounds__(256) void expand_union_kernel(const uint64_t* __restrict__ gwords,
                                                            const int32_t* __restrict__ cached_len,
                                                            uint64_t* __restrict__ rwords,
                                                            int32_t* __restrict__ counts, int Hq,
                                                            int nqb, int W, int group_size,
-                                                           int q_block, int page) {
+                                                           int q_block, int C) {
   __shared__ int red[4];
   const int r = blockIdx.x;                 // (b*Hq + h)*nqb + i
   const int i = r % nqb;
@@ -162,7 +163,7 @@ __global__ __launch_bounds__(256) void expand_union_kernel(const uint64_t* __res
   const int b = r / (nqb * Hq);
   const int G = Hq / group_size;
   const int t = threadIdx.x;
-  const int lim = cached_len[b] / page + (i + 1) * q_block / page;
+  const int lim = causal_block_end(cached_len[b], C, i, q_block);
   const uint64_t* src = gwords + ((size_t)b * G + h / group_size) * W;
   int cnt = 0;
   for (int w = t; w < W; w += 256) {
@@ -196,11 +197,11 @@ hipError_t launch_union_rows(const Dims& d, const uint64_t* masks, const int32_t
       static_cast<char*>(ws) + tables_ws_bytes(d, group_size));
   int32_t* rcounts = reinterpret_cast<int32_t*>(rwords + (size_t)R * d.W);
   union_kernel<<<RG, 256, 0, st>>>(masks, cached_len, gwords, gcounts, d.Hq, d.nqb, d.W,
-                                   group_size, G, d.chunk_blocks);
+                                   group_size, G, d.C);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   expand_union_kernel<<<R, 256, 0, st>>>(gwords, cached_len, rwords, rcounts, d.Hq, d.nqb, d.W,
-                                         group_size, d.q_block, d.page);
+                                         group_size, d.q_block, d.C);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   compact_kernel<<<R, 256, 0, st>>>(rwords, rcounts, kv_indptr, kv_indices, d.W);
@@ -220,7 +221,7 @@ hipError_t launch_tables(const Dims& d, const uint64_t* masks, const int32_t* ca
   uint64_t* gwords = static_cast<uint64_t*>(ws);
   int32_t* counts = reinterpret_cast<int32_t*>(gwords + (size_t)R * d.W);
   union_kernel<<<R, 256, 0, st>>>(masks, cached_len, gwords, counts, d.Hq, d.nqb, d.W,
-                                  group_size, G, d.chunk_blocks);
+                                  group_size, G, d.C);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   compact_kernel<<<R, 256, 0, st>>>(gwords, counts, kv_indptr, kv_indices, d.W);

@@ -50,6 +50,7 @@ class Workload:
     local_blocks: int = 4
     needles_per_kv_head: int = 0
     needle_beta: float = 2.0
+    poison_tail: bool = False              # NaN in the rows of each last page past the end
     rho: float = 0.0
     q_prescale: float = 1.0
     group_size: int = 4                    # query heads per execution group
@@ -62,7 +63,7 @@ class Workload:
 
     @property
     def n_qblocks(self) -> int:
-        return self.chunk_len // self.q_block
+        return -(-self.chunk_len // self.q_block)
 
     @property
     def words(self) -> int:
@@ -72,7 +73,10 @@ class Workload:
         return self.cached_lens[b] // self.page_size
 
     def n_kv_blocks(self, b: int) -> int:
-        return (self.cached_lens[b] + self.chunk_len) // self.page_size
+        return -(-(self.cached_lens[b] + self.chunk_len) // self.page_size)
+
+    def seq_len(self, b: int) -> int:
+        return self.cached_lens[b] + self.chunk_len
 
     @property
     def num_groups(self) -> int:
@@ -89,10 +93,11 @@ class Workload:
 
 
 def _llama(name, seed, cached_lens, top_frac, needles, description, **kw):
-    nkb_max = max((c + 2048) // PAGE for c in cached_lens)
+    chunk = kw.pop("chunk_len", 2048)
+    nkb_max = max(-(-(c + chunk) // PAGE) for c in cached_lens)
     return Workload(
         name=name, seed=seed, batch=len(cached_lens), num_q_heads=32,
-        num_kv_heads=kw.pop("num_kv_heads", 8), head_dim=128, q_block=128, chunk_len=2048,
+        num_kv_heads=kw.pop("num_kv_heads", 8), head_dim=128, q_block=128, chunk_len=chunk,
         cached_lens=tuple(cached_lens), max_kv_blocks=kw.pop("max_kv_blocks", nkb_max),
         sm_scale=1.0 / math.sqrt(128.0), mask_kind="estimator",
         top_frac=top_frac, needles_per_kv_head=needles, rho=RHO_CALIBRATED,
@@ -124,6 +129,20 @@ WORKLOADS = {
         "qwen3_30b_128k_final", 6, (129024,), 0.05, 32,
         "Qwen3-30B-A3B-like layer (32/4 heads), 128K final chunk, top 5%, sub-groups of 4",
         num_kv_heads=4),
+    # lengths that are not multiples of 64 or of q_block: a partial last
+    # Q-block, a block holding both cached and chunk tokens, a partial last
+    # page whose rows past the sequence end hold NaN, and a sequence with no
+    # cached tokens.
+    "tiny_unaligned": Workload(
+        name="tiny_unaligned", seed=7, batch=3, num_q_heads=8, num_kv_heads=2,
+        head_dim=64, q_block=64, chunk_len=200, cached_lens=(1000, 37, 0),
+        max_kv_blocks=20, sm_scale=1.0 / 8.0, mask_kind="estimator", top_frac=0.25,
+        poison_tail=True,
+        description="unaligned lengths: 3 sequences (1000, 37, 0 cached) + 200-token chunk"),
+    "llama8b_unaligned": _llama(
+        "llama8b_unaligned", 8, (100001, 4999, 0), 0.05, 8,
+        "LLaMA-3.1-8B layer, unaligned: 100001 / 4999 / 0 cached + 2000-token chunk",
+        chunk_len=2000, poison_tail=True),
     "sweep_128k_64chunks": _llama(
         "sweep_128k_64chunks", 5, (129024,), 0.05, 64,
         "131072-token sequence prefilled in 64 chunks of 2048, top 5%",

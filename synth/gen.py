@@ -65,26 +65,31 @@ def pack_bits(bits: np.ndarray, words: int) -> np.ndarray:
 
 
 def random_masks(seed: int, batch: int, num_q_heads: int, n_qblocks: int,
-                 q_block: int, page: int, cached_blocks: Sequence[int],
+                 q_block: int, page: int, cached_lens: Sequence[int],
                  chunk_len: int, words: int, p: float, sink_blocks: int = 1,
                  causal: bool = True) -> np.ndarray:
-    """Bernoulli(p) bits over cached blocks, plus sink and chunk-causal bits.
+    """Bernoulli(p) bits over the full cached blocks, plus sink and chunk-causal bits.
 
-    Returns uint64 ``[B, Hq, nQB, words]``.  This is the mask recipe of the
-    tiny workload, and (with other ``p``) an input family for table tests.
+    ``cached_lens`` are token counts.  The chunk-causal bits of Q-block i
+    run from block cached_len // page up to the block holding the chunk's
+    token min((i+1)*q_block, C) - 1.  Returns uint64 ``[B, Hq, nQB, words]``.
+    This is the mask recipe of the tiny workload, and (with other ``p``) an
+    input family for table tests.
     """
     rng = _rng(seed, _T_MASK)
     out = np.zeros((batch, num_q_heads, n_qblocks, words), dtype=np.uint64)
     for b in range(batch):
-        nc = int(cached_blocks[b])
-        nkb = nc + chunk_len // page
+        cl = int(cached_lens[b])
+        nc = cl // page
+        nkb = -(-(cl + chunk_len) // page)
         bits = np.zeros((num_q_heads, n_qblocks, nkb), dtype=bool)
         if nc:
             bits[:, :, :nc] = rng.random((num_q_heads, n_qblocks, nc)) < p
             bits[:, :, :min(sink_blocks, nc)] = True
         if causal:
             for i in range(n_qblocks):
-                bits[:, i, nc:nc + ((i + 1) * q_block) // page] = True
+                last = cl + min((i + 1) * q_block, chunk_len) - 1
+                bits[:, i, nc:last // page + 1] = True
         out[b] = pack_bits(bits, words)
     return out
 
@@ -192,6 +197,28 @@ def _apply_needle(kb: np.ndarray, j: int, u: np.ndarray, beta: float) -> None:
     kb[j] = bf16_round(blk)
 
 
+BF16_QNAN = np.uint16(0x7FC0)
+
+
+def poison_past_end(w: Workload, k_pool: np.ndarray, v_pool: np.ndarray,
+                    pt: np.ndarray) -> None:
+    """NaN in every K and V row of a sequence's last page past its end.
+
+    Those rows are not part of the sequence (a paged cache leaves them
+    unwritten); filling them with NaN makes any read that lets them into a
+    result visible."""
+    page = w.page_size
+    for b in range(w.batch):
+        n = w.n_kv_blocks(b)
+        valid = w.seq_len(b) - page * (n - 1)
+        if valid == page:
+            continue
+        for kvh in range(w.num_kv_heads):
+            pid = pt[b, kvh, n - 1]
+            k_pool[pid, valid:, :] = BF16_QNAN
+            v_pool[pid, valid:, :] = BF16_QNAN
+
+
 def make_inputs(w: Workload) -> Dict[str, object]:
     """All inputs of one chunk step of workload ``w`` (not the sweep)."""
     B, Hkv, ratio = w.batch, w.num_kv_heads, w.ratio
@@ -207,6 +234,8 @@ def make_inputs(w: Workload) -> Dict[str, object]:
         for b in range(B):
             nc = ncb[b]
             lo, hi = w.sink_blocks, nc - w.local_blocks
+            if hi - lo < w.needles_per_kv_head:
+                continue                  # too short a cache for needles
             for kvh in range(Hkv):
                 js = rng.choice(np.arange(lo, hi), size=w.needles_per_kv_head, replace=False)
                 for j in np.sort(js):
@@ -223,11 +252,13 @@ def make_inputs(w: Workload) -> Dict[str, object]:
             _apply_needle(kb, j, _needle_direction(q[b], h, i, w.q_block), w.needle_beta)
 
     k_pool, v_pool = _fill_kv(w, pt, total, nkb, needle_fn if needles else None)
+    if w.poison_tail:
+        poison_past_end(w, k_pool, v_pool, pt)
 
     masks = None
     if w.mask_kind == "bernoulli":
         masks = random_masks(w.seed, B, w.num_q_heads, w.n_qblocks, w.q_block,
-                             w.page_size, ncb, w.chunk_len, w.words,
+                             w.page_size, w.cached_lens, w.chunk_len, w.words,
                              w.bernoulli_p, w.sink_blocks)
     return dict(workload=w, q=q, k_pool=k_pool, v_pool=v_pool, page_table=pt,
                 cached_len=np.array(w.cached_lens, dtype=np.int32),

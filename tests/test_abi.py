@@ -54,15 +54,20 @@ def test_valid_problems(lib):
     assert _status(_prob(num_q_heads=4, num_kv_heads=1, head_dim=64, q_block=64, chunk_len=256,
                          max_kv_blocks=20, cached_len=[1024])) == 0
     assert _status(_prob(cached_len=[0])) == 0
+    # any lengths: partial last Q-block and page, a block shared by cache and chunk
+    assert _status(_prob(chunk_len=2000)) == 0
+    assert _status(_prob(cached_len=[129000])) == 0          # 131048 tokens: 2048 blocks
+    assert _status(_prob(chunk_len=1, cached_len=[1])) == 0
 
 
 @pytest.mark.parametrize("kw,group,code", [
     (dict(head_dim=96), 4, "CA_ERR_UNSUPPORTED"),
     (dict(q_block=32), 4, "CA_ERR_UNSUPPORTED"),
-    (dict(chunk_len=2000), 4, "CA_ERR_UNALIGNED"),
-    (dict(cached_len=[129000]), 4, "CA_ERR_UNALIGNED"),
-    (dict(cached_len=[-64]), 4, "CA_ERR_UNALIGNED"),
+    (dict(cached_len=[-64]), 4, "CA_ERR_SHAPE"),
+    (dict(cached_len=[-1]), 4, "CA_ERR_SHAPE"),
     (dict(cached_len=[129088]), 4, "CA_ERR_SHAPE"),           # needs 2049 blocks
+    (dict(cached_len=[129025]), 4, "CA_ERR_SHAPE"),           # 131073 tokens: 2049 blocks
+    (dict(chunk_len=0), 4, "CA_ERR_SHAPE"),
     (dict(max_kv_blocks=20000, cached_len=[64]), 4, "CA_ERR_SHAPE"),
     (dict(num_kv_heads=5), 4, "CA_ERR_SHAPE"),
     (dict(), 3, "CA_ERR_GROUP"),

@@ -46,7 +46,8 @@ def _bs_csr(bits, w):
     return np.array(indptr, dtype=np.int32), np.array(indices, dtype=np.int32)
 
 
-@pytest.mark.parametrize("name", ["tiny_gqa_1k", "llama8b_32k", "batched_ragged_4seq"])
+@pytest.mark.parametrize("name", ["tiny_gqa_1k", "llama8b_32k", "batched_ragged_4seq",
+                                  "tiny_unaligned", "llama8b_unaligned"])
 def test_copy_arm_gather_and_bitexact(name, workload_inputs, oracle_estimate):
     d = workload_inputs(name)
     w = d["workload"]
@@ -68,6 +69,7 @@ def test_copy_arm_gather_and_bitexact(name, workload_inputs, oracle_estimate):
     pick = np.unique(np.linspace(0, ip[-1] - 1, 64).astype(np.int64))
     kh = kp[torch.as_tensor(pick, device="cuda")].view(torch.int16).cpu().numpy()
     vh = vp[torch.as_tensor(pick, device="cuda")].view(torch.int16).cpu().numpy()
+    # bit patterns (NaN rows past a sequence end are copied as they are)
     assert np.array_equal(kh.view(np.uint16), d["k_pool"][src[pick]])
     assert np.array_equal(vh.view(np.uint16), d["v_pool"][src[pick]])
     for splits in (1, 0):
@@ -89,16 +91,16 @@ def _union_rows_csr(masks, w):
     T = oracle.block_tables(masks, w.group_size, nkb)
     indptr, indices = [0], []
     for b in range(w.batch):
-        nc = w.n_cached_blocks(b)
         for h in range(w.num_q_heads):
             for i in range(w.n_qblocks):
-                lim = nc + (i + 1) * w.q_block // w.page_size
+                lim = oracle.causal_block_end(w.cached_lens[b], w.chunk_len, i, w.q_block,
+                                              w.page_size)
                 indices += [j for j in T[b][h // w.group_size] if j < lim]
                 indptr.append(len(indices))
     return np.array(indptr, dtype=np.int32), np.array(indices, dtype=np.int32), T
 
 
-@pytest.mark.parametrize("name", ["llama8b_32k", "batched_ragged_4seq"])
+@pytest.mark.parametrize("name", ["llama8b_32k", "batched_ragged_4seq", "llama8b_unaligned"])
 def test_block_sparse_tables_bitexact(name, workload_inputs, oracle_estimate):
     d = workload_inputs(name)
     w = d["workload"]
@@ -116,7 +118,7 @@ def test_block_sparse_tables_bitexact(name, workload_inputs, oracle_estimate):
     assert np.array_equal(ix.cpu().numpy()[:rip[-1]], rix)
 
 
-@pytest.mark.parametrize("name", ["llama8b_32k", "batched_ragged_4seq"])
+@pytest.mark.parametrize("name", ["llama8b_32k", "batched_ragged_4seq", "llama8b_unaligned"])
 def test_block_sparse_matched_tables_attention(name, workload_inputs, oracle_estimate):
     """Block-sparse execution of the unioned tables computes the zero-copy result."""
     d = workload_inputs(name)
@@ -157,7 +159,7 @@ def _bs_oracle_rows(d, bits, sm_scale, rows):
     return ref, ref_lse
 
 
-@pytest.mark.parametrize("name", ["llama8b_32k", "batched_ragged_4seq"])
+@pytest.mark.parametrize("name", ["llama8b_32k", "batched_ragged_4seq", "llama8b_unaligned"])
 def test_block_sparse_attention_sampled(name, workload_inputs, oracle_estimate):
     d = workload_inputs(name)
     w = d["workload"]

@@ -94,31 +94,38 @@ def test_tables_tiny_bitexact(workload_inputs):
         _assert_tables_equal(_gpu_tables(p, d["masks"], gs), ref)
 
 
-@pytest.mark.parametrize("seed", range(4))
+@pytest.mark.parametrize("seed", range(6))
 def test_tables_adversarial(seed):
-    """Ragged batch, garbage bits beyond nKB, word-edge bits, empty and full rows."""
+    """Ragged batch, garbage bits beyond nKB, word-edge bits, empty and full rows;
+    seeds 4 and 5 use lengths that are not multiples of 64 (nKB = ceil)."""
     rng = np.random.default_rng(100 + seed)
     cached = [0, 64 * 31, 64 * 64, 64 * 129][: 1 + seed % 4]
+    C = 256
+    if seed >= 4:
+        cached = [5, 64 * 31 + 1, 64 * 64 - 1, 64 * 129 + 63][: 2 + seed % 4]
+        C = 200
     cached = [int(c) for c in cached]
-    B, Hq, Hkv, C, qb = len(cached), 16, 2, 256, 64
-    maxkb = max(c // 64 for c in cached) + C // 64 + 3
+    B, Hq, Hkv, qb = len(cached), 16, 2, 64
+    nqb = -(-C // qb)
+    maxkb = max(-(-(c + C) // 64) for c in cached) + 3
     W = (maxkb + 63) // 64
     p = ca.Problem(B, Hq, Hkv, 64, qb, C, maxkb, cached)
-    raw = rng.integers(0, 2**63, size=(B, Hq, C // qb, W), dtype=np.int64).astype(np.uint64)
-    dens = rng.random((B, Hq, C // qb, W * 64)) < [0.0, 0.01, 0.2, 1.0][seed]
+    raw = rng.integers(0, 2**63, size=(B, Hq, nqb, W), dtype=np.int64).astype(np.uint64)
+    dens = rng.random((B, Hq, nqb, W * 64)) < [0.0, 0.01, 0.2, 1.0, 0.2, 0.01][seed]
     masks = synth.gen.pack_bits(dens, W) | (raw & np.uint64(1 << (seed * 7)))
     masks[0, 0, 0, :] = 0                                     # an all-zero row
     if W > 1:
         masks[-1, -1, -1, 0] |= np.uint64(1) << np.uint64(63)  # word edge 63/64
         masks[-1, -1, -1, 1] |= np.uint64(1)
     for gs in (1, 2, 4, 8):
-        nkb = [c // 64 + C // 64 for c in cached]
+        nkb = [oracle.n_kv_blocks(c, C, 64) for c in cached]
         ref = oracle.tables_to_csr(oracle.block_tables(masks, gs, nkb))
         _assert_tables_equal(_gpu_tables(p, masks, gs), ref)
 
 
 @pytest.mark.parametrize("name", ["llama8b_32k", "llama8b_128k_final", "batched_ragged_4seq",
-                                  "qwen3_30b_128k_final"])
+                                  "qwen3_30b_128k_final", "tiny_unaligned",
+                                  "llama8b_unaligned"])
 def test_tables_workloads_bitexact(name, workload_inputs, oracle_estimate):
     d = workload_inputs(name)
     w = d["workload"]
@@ -139,7 +146,8 @@ def test_tables_workloads_bitexact(name, workload_inputs, oracle_estimate):
 # ---------------------------------------------------------------------------
 # estimator
 # ---------------------------------------------------------------------------
-@pytest.mark.parametrize("name", ["tiny_gqa_1k", "llama8b_32k", "batched_ragged_4seq"])
+@pytest.mark.parametrize("name", ["tiny_gqa_1k", "llama8b_32k", "batched_ragged_4seq",
+                                  "tiny_unaligned", "llama8b_unaligned"])
 def test_pooling_and_scores(name, workload_inputs, oracle_estimate):
     d = workload_inputs(name)
     w = d["workload"]
@@ -149,7 +157,8 @@ def test_pooling_and_scores(name, workload_inputs, oracle_estimate):
     if parts is None:
         nkb = [w.n_kv_blocks(b) for b in range(w.batch)]
         qm = oracle.q_block_means(d["q"], w.q_block)
-        km = oracle.k_block_means(d["k_pool"], d["page_table"], nkb)
+        km = oracle.k_block_means(d["k_pool"], d["page_table"], nkb,
+                                  [w.seq_len(b) for b in range(w.batch)])
         sc = oracle.block_scores(qm, km, [w.n_cached_blocks(b) for b in range(w.batch)])
     else:
         qm, km, sc = parts["q_mean"], parts["k_mean"], parts["scores"]
@@ -187,7 +196,8 @@ def test_select_tied_scores_bitexact(nc_list, top_frac, sink, local):
         scores[b, :, :, :nc] = s
         per_b.append(s)
     params = oracle.EstimatorParams(top_frac, sink, local)
-    ref = oracle.masks_from_scores(per_b, nc_list, 64, qb, p.words, params)
+    ref = oracle.masks_from_scores(per_b, [64 * n for n in nc_list], C, 64, qb, p.words,
+                                   params)
     got = ca.select_blocks(p, torch.from_numpy(scores).cuda(), top_frac, sink, local)
     torch.cuda.synchronize()
     assert np.array_equal(u64_host(got), ref)
@@ -211,13 +221,15 @@ def test_threshold_select_bitexact(nc_list, alpha, tau):
         scores[b, :, :, :nc] = s
         per_b.append(s)
     margin = oracle.threshold_margin(alpha, tau, sm)
-    ref = oracle.masks_from_threshold(per_b, nc_list, 64, qb, p.words, margin, 1, 4)
+    ref = oracle.masks_from_threshold(per_b, [64 * n for n in nc_list], C, 64, qb, p.words,
+                                      margin, 1, 4)
     got = ca.select_blocks_threshold(p, torch.from_numpy(scores).cuda(), alpha, tau, sm)
     torch.cuda.synchronize()
     assert np.array_equal(u64_host(got), ref)
 
 
 @pytest.mark.parametrize("name,alpha,tau", [("llama8b_32k", 0.03, 16.0),
+                                            ("llama8b_unaligned", 0.03, 16.0),
                                             ("llama8b_128k_final", 0.06, 16.0)])
 def test_threshold_estimator_end_to_end(name, alpha, tau, workload_inputs, oracle_estimate):
     """GPU threshold masks vs the oracle's on fp64 scores: only blocks whose fp64
@@ -232,8 +244,8 @@ def test_threshold_estimator_end_to_end(name, alpha, tau, workload_inputs, oracl
     torch.cuda.synchronize()
     margin = oracle.threshold_margin(alpha, tau, w.sm_scale)
     s32 = [np.asarray(sb, dtype=np.float32) for sb in parts["scores"]]
-    ref = oracle.masks_from_threshold(s32, [w.n_cached_blocks(b) for b in range(w.batch)],
-                                      w.page_size, w.q_block, w.words, margin, w.sink_blocks,
+    ref = oracle.masks_from_threshold(s32, w.cached_lens, w.chunk_len, w.page_size,
+                                      w.q_block, w.words, margin, w.sink_blocks,
                                       w.local_blocks)
     gb, rb = oracle.unpack_masks(u64_host(got)), oracle.unpack_masks(ref)
     flips = 0
@@ -257,7 +269,8 @@ def test_threshold_estimator_end_to_end(name, alpha, tau, workload_inputs, oracl
 
 @pytest.mark.parametrize("name,gs", [("llama8b_32k", 4), ("llama8b_128k_final", 4),
                                      ("batched_ragged_4seq", 4), ("qwen3_30b_128k_final", 4),
-                                     ("qwen3_30b_128k_final", 8), ("llama8b_32k", 1)])
+                                     ("qwen3_30b_128k_final", 8), ("llama8b_32k", 1),
+                                     ("tiny_unaligned", 4), ("llama8b_unaligned", 4)])
 def test_fused_estimate_tables(name, gs, workload_inputs, oracle_estimate):
     """Fused estimator -> union (no per-row masks): the tables equal the oracle's
     union of the oracle masks, except blocks that are near ties (fp64 score within
@@ -327,7 +340,8 @@ def _near_tie_check(gpu_masks, ref_masks, scores64, w, tol):
 
 
 @pytest.mark.parametrize("name", ["llama8b_32k", "llama8b_128k_final", "batched_ragged_4seq",
-                                  "qwen3_30b_128k_final"])
+                                  "qwen3_30b_128k_final", "tiny_unaligned",
+                                  "llama8b_unaligned"])
 def test_estimator_end_to_end(name, workload_inputs, oracle_estimate):
     d = workload_inputs(name)
     w = d["workload"]
@@ -368,7 +382,8 @@ def test_attention_tiny_groups_and_sharp(gs, scale_mult, workload_inputs):
     p = _problem(w)
     x = device_inputs(d)
     nc = w.n_cached_blocks(0)
-    masks = synth.random_masks(5, 1, 4, w.n_qblocks, w.q_block, 64, [nc], w.chunk_len, w.words, 0.05)
+    masks = synth.random_masks(5, 1, 4, w.n_qblocks, w.q_block, 64, [w.cached_lens[0]],
+                               w.chunk_len, w.words, 0.05)
     T = oracle.block_tables(masks, gs, [w.n_kv_blocks(0)])
     sm = w.sm_scale * scale_mult
     ref, ref_lse = oracle.chunk_attention(d["q"], d["k_pool"], d["v_pool"], d["page_table"],
@@ -376,6 +391,59 @@ def test_attention_tiny_groups_and_sharp(gs, scale_mult, workload_inputs):
     for splits in (1, 2):
         got, lse = _run_attention(p, x, oracle.tables_to_csr(T), gs, sm, num_splits=splits)
         print(compare_attention(got, lse, ref, ref_lse))
+
+
+@pytest.mark.parametrize("splits", [1, 3, 0])
+def test_attention_unaligned_full(splits, workload_inputs, oracle_estimate):
+    """Every output row on three sequences of 1000 / 37 / 0 cached tokens + a
+    200-token chunk (partial last query tile and page, a block shared by cache
+    and chunk); the K/V rows past each sequence end hold NaN.  Estimator
+    tables, then the dense baseline, then a sharp softmax on the same tables."""
+    name = "tiny_unaligned"
+    d = workload_inputs(name)
+    w = d["workload"]
+    p = _problem(w)
+    x = device_inputs(d)
+    masks, _ = oracle_estimate(name)
+    T, csr = _oracle_tables(masks, w)
+    ref, ref_lse = oracle.chunk_attention(d["q"], d["k_pool"], d["v_pool"], d["page_table"],
+                                          d["cached_len"], T, w.group_size, w.sm_scale)
+    got, lse = _run_attention(p, x, csr, w.group_size, w.sm_scale, num_splits=splits)
+    print("tables", compare_attention(got, lse, ref, ref_lse))
+    Td = oracle.dense_tables([w.n_kv_blocks(b) for b in range(w.batch)], w.num_groups)
+    ref, ref_lse = oracle.chunk_attention(d["q"], d["k_pool"], d["v_pool"], d["page_table"],
+                                          d["cached_len"], Td, w.group_size, w.sm_scale)
+    got, lse = _run_attention(p, x, None, w.group_size, w.sm_scale, num_splits=splits,
+                              dense=True)
+    print("dense", compare_attention(got, lse, ref, ref_lse))
+    for gs in (1, 2):
+        Tg = oracle.block_tables(masks, gs, [w.n_kv_blocks(b) for b in range(w.batch)])
+        ref, ref_lse = oracle.chunk_attention(d["q"], d["k_pool"], d["v_pool"], d["page_table"],
+                                              d["cached_len"], Tg, gs, w.sm_scale * 8)
+        got, lse = _run_attention(p, x, oracle.tables_to_csr(Tg), gs, w.sm_scale * 8,
+                                  num_splits=splits)
+        print("sharp gs", gs, compare_attention(got, lse, ref, ref_lse))
+
+
+@pytest.mark.parametrize("C,cached", [(1, (0, 63, 64)), (63, (1, 0)), (65, (127,)),
+                                      (129, (4095, 1))])
+def test_attention_unaligned_edges(C, cached):
+    """Single-token and near-page chunks on caches of 0, 1, 63, 64, 127 ... tokens:
+    dense and all-open-table attention against the oracle, every row."""
+    nkb = max(-(-(c + C) // 64) for c in cached)
+    w = synth.get_workload("tiny_unaligned", chunk_len=C, cached_lens=cached,
+                           batch=len(cached), max_kv_blocks=nkb)
+    d = synth.make_inputs(w)
+    p = _problem(w)
+    x = device_inputs(d)
+    T = oracle.dense_tables([w.n_kv_blocks(b) for b in range(w.batch)], w.num_groups)
+    ref, ref_lse = oracle.chunk_attention(d["q"], d["k_pool"], d["v_pool"], d["page_table"],
+                                          d["cached_len"], T, w.group_size, w.sm_scale)
+    got, lse = _run_attention(p, x, oracle.tables_to_csr(T), w.group_size, w.sm_scale,
+                              num_splits=1)
+    compare_attention(got, lse, ref, ref_lse)
+    got, lse = _run_attention(p, x, None, w.group_size, w.sm_scale, num_splits=0, dense=True)
+    compare_attention(got, lse, ref, ref_lse)
 
 
 def test_attention_first_chunk_no_cache():
@@ -388,12 +456,16 @@ def test_attention_first_chunk_no_cache():
                                           d["cached_len"], T, w.group_size, w.sm_scale)
     got, lse = _run_attention(p, x, csr, w.group_size, w.sm_scale, num_splits=1)
     compare_attention(got, lse, ref, ref_lse)
-    got, lse = _run_attention(p, x, None, w.group_size, w.sm_scale, num_splits=1, dense=True)
-    compare_attention(got, lse, ref, ref_lse)
+    # dense with splits: the early query tiles see fewer blocks than later
+    # splits start at (those splits are empty)
+    for splits in (1, 3):
+        got, lse = _run_attention(p, x, None, w.group_size, w.sm_scale, num_splits=splits,
+                                  dense=True)
+        compare_attention(got, lse, ref, ref_lse)
 
 
 @pytest.mark.parametrize("name", ["llama8b_32k", "llama8b_128k_final", "batched_ragged_4seq",
-                                  "qwen3_30b_128k_final"])
+                                  "qwen3_30b_128k_final", "llama8b_unaligned"])
 def test_attention_workloads_sampled(name, workload_inputs, oracle_estimate):
     d = workload_inputs(name)
     w = d["workload"]
@@ -411,7 +483,7 @@ def test_attention_workloads_sampled(name, workload_inputs, oracle_estimate):
     print(name, "sharp", compare_attention(got, lse, ref, ref_lse, rows[::3]))
 
 
-@pytest.mark.parametrize("name", ["llama8b_32k", "batched_ragged_4seq"])
+@pytest.mark.parametrize("name", ["llama8b_32k", "batched_ragged_4seq", "llama8b_unaligned"])
 def test_dense_baseline_sampled(name, workload_inputs):
     d = workload_inputs(name)
     w = d["workload"]

@@ -145,12 +145,24 @@ def test_attention_hand_worked():
     # a query that sees nothing: output 0, lse = -inf
     out, lse = oracle.chunk_attention(q, kp, vp, pt, [0], [[[1]]], 1, 1.0)
     assert np.all(out[0, 0, 0] == 0) and lse[0, 0, 0] == -np.inf
+    # one cached token + the 2-token chunk: the sequence ends inside block 1,
+    # whose second row (position 3) is not part of it and holds NaN
+    kp2, vp2 = kp.copy(), vp.copy()
+    kp2[0, 1, :] = 0x7FC0
+    vp2[0, 1, :] = 0x7FC0
+    out, lse = oracle.chunk_attention(q, kp2, vp2, pt, [1], [[[0, 1]]], 1, 1.0)
+    np.testing.assert_allclose(out[0, 0, 0], [e / (e + 1), 1 / (e + 1)], rtol=1e-14)
+    np.testing.assert_allclose(out[0, 1, 0], [1.0, 3 * e / (2 * e + 1)], rtol=1e-14)
+    np.testing.assert_allclose(lse[0, 0], [math.log(e + 1), math.log(2 * e + 1)], rtol=1e-14)
 
 
-def _contiguous_kv(d, b, kvh, nkb):
+def _contiguous_kv(d, b, kvh, nkb, seq_len=None):
+    """The sequence's keys and values as contiguous [seq_len, D] tensors."""
     pt = d["page_table"][b, kvh, :nkb]
     K = oracle.bf16_to_f64(d["k_pool"][pt]).reshape(nkb * d["k_pool"].shape[1], -1)
     V = oracle.bf16_to_f64(d["v_pool"][pt]).reshape(nkb * d["v_pool"].shape[1], -1)
+    if seq_len is not None:
+        K, V = K[:seq_len], V[:seq_len]
     return torch.from_numpy(K), torch.from_numpy(V)
 
 
@@ -159,15 +171,15 @@ def _sdpa_ref(d, b, h, queries, keep_blocks=None):
     w = d["workload"]
     ratio = w.num_q_heads // w.num_kv_heads
     nkb = w.n_kv_blocks(b)
-    K, V = _contiguous_kv(d, b, h // ratio, nkb)
+    K, V = _contiguous_kv(d, b, h // ratio, nkb, w.seq_len(b))
     q = torch.from_numpy(oracle.bf16_to_f64(d["q"][b, queries, h, :]))
-    kpos = torch.arange(nkb * w.page_size)
+    kpos = torch.arange(w.seq_len(b))
     qpos = torch.as_tensor(w.cached_lens[b] + np.asarray(queries))
     allow = kpos[None, :] <= qpos[:, None]
     if keep_blocks is not None:
         kb = torch.zeros(nkb, dtype=torch.bool)
         kb[list(keep_blocks)] = True
-        allow &= kb.repeat_interleave(w.page_size)[None, :]
+        allow &= kb.repeat_interleave(w.page_size)[None, :w.seq_len(b)]
     o = torch.nn.functional.scaled_dot_product_attention(
         q[None, None], K[None, None], V[None, None], attn_mask=allow[None, None],
         scale=w.sm_scale)
@@ -223,7 +235,8 @@ def test_gathered_equals_masked_dense(workload_inputs):
     d = workload_inputs("tiny_gqa_1k")
     w = d["workload"]
     nc = w.n_cached_blocks(0)
-    masks = synth.random_masks(11, 1, 4, w.n_qblocks, w.q_block, w.page_size, [nc],
+    masks = synth.random_masks(11, 1, 4, w.n_qblocks, w.q_block, w.page_size,
+                               [w.cached_lens[0]],
                                w.chunk_len, w.words, 0.04)
     for gs in (1, 2):
         T = oracle.block_tables(masks, gs, [w.n_kv_blocks(0)])
@@ -256,7 +269,8 @@ def test_block_sparse_rows_equal_masked_sdpa(workload_inputs):
     d = workload_inputs("tiny_gqa_1k")
     w = d["workload"]
     nc = w.n_cached_blocks(0)
-    masks = synth.random_masks(13, 1, 4, w.n_qblocks, w.q_block, w.page_size, [nc],
+    masks = synth.random_masks(13, 1, 4, w.n_qblocks, w.q_block, w.page_size,
+                               [w.cached_lens[0]],
                                w.chunk_len, w.words, 0.1)
     bits = oracle.unpack_masks(masks)
     out, lse = oracle.block_sparse_attention(d["q"], d["k_pool"], d["v_pool"], d["page_table"],
@@ -280,7 +294,8 @@ def test_block_sparse_group_uniform_rows_equal_union(workload_inputs):
     d = workload_inputs("tiny_gqa_1k")
     w = d["workload"]
     nc = w.n_cached_blocks(0)
-    one = synth.random_masks(17, 1, 1, 1, w.q_block, w.page_size, [nc], w.chunk_len, w.words, 0.2)
+    one = synth.random_masks(17, 1, 1, 1, w.q_block, w.page_size, [w.cached_lens[0]],
+                             w.chunk_len, w.words, 0.2)
     sel = oracle.unpack_masks(one)[0, 0, 0, :nc]
     nkb = w.n_kv_blocks(0)
     bits = np.zeros((1, 4, w.n_qblocks, 64 * w.words), dtype=bool)
@@ -313,6 +328,16 @@ def test_block_means_closed_form():
     km = oracle.k_block_means(pool, pt, [3])
     for j, p in enumerate([2, 0, 1]):
         np.testing.assert_array_equal(km[0, 0, j], 31.5 + np.arange(D) + 60 * p)
+    # a sequence ending 10 rows into block 2: that block's mean is over rows 0..9
+    km = oracle.k_block_means(pool, pt, [3], seq_len=[2 * 64 + 10])
+    np.testing.assert_array_equal(km[0, 0, 2], 4.5 + np.arange(D) + 60 * 1)
+    np.testing.assert_array_equal(km[0, 0, 0], 31.5 + np.arange(D) + 60 * 2)
+    # a chunk of 200 rows in Q-blocks of 64: four blocks, the last of rows 192..199
+    q = _bf16(np.broadcast_to(np.arange(200, dtype=np.float32)[None, :, None, None],
+                              (1, 200, Hq, D)))
+    qm = oracle.q_block_means(q, qb)
+    assert qm.shape == (1, Hq, 4, D)
+    assert np.all(qm[0, :, 3, :] == 195.5) and np.all(qm[0, :, 2, :] == 128 + 31.5)
 
 
 def test_block_scores_index_mapping():
@@ -374,6 +399,96 @@ def test_estimator_hand_built_case():
     for i, causal in enumerate([{10}, {10, 11}]):
         want = sum(1 << j for j in sel | causal)
         assert int(masks[0, 0, i, 0]) == want
+
+
+def test_estimator_hand_built_unaligned():
+    """Block 10 holds the last 5 cached tokens and the first 59 of the chunk: it is a
+    chunk block (open for every Q-block, never a top-k candidate); the 100-token
+    chunk ends 41 rows into block 11; Q-block 1 holds 36 rows."""
+    D, page, qb, C = 4, 64, 64, 100
+    cl = 10 * page + 5
+    nkb = oracle.n_kv_blocks(cl, C, page)
+    assert nkb == 12
+    kvals = [(j % 5) - 2 for j in range(nkb)]
+    kvals[10] = 50                        # would win every top-k if it were a candidate
+    pool = np.stack([_bf16(np.tile(np.array([v, 0, 0, 0], np.float32), (page, 1))) for v in kvals])
+    pt = np.arange(nkb, dtype=np.int32)[None, None, :]
+    q = _bf16(np.tile(np.array([1, 0, 0, 0], np.float32), (1, C, 1, 1)))
+    masks = oracle.estimate_masks(q, pool, pt, [cl], page, qb, C, 1,
+                                  oracle.EstimatorParams(top_frac=0.25, sink_blocks=1, local_blocks=2))
+    assert masks.shape == (1, 1, 2, 1)
+    sel = {4, 9, 3} | {0} | {8, 9}
+    for i in range(2):
+        assert int(masks[0, 0, i, 0]) == sum(1 << j for j in sel | {10, 11})
+
+
+def test_unaligned_causal_bits_bruteforce(oracle_estimate, workload_inputs):
+    """Chunk bits (j >= nC) of every mask row = the blocks, other than full cached
+    ones, that hold a key some query of the Q-block may see, enumerated key by key;
+    the cached bits hold between k and k + sink + local blocks."""
+    name = "tiny_unaligned"
+    d = workload_inputs(name)
+    w = d["workload"]
+    masks, _ = oracle_estimate(name)
+    bits = oracle.unpack_masks(masks)
+    assert w.n_qblocks == 4 and [w.n_kv_blocks(b) for b in range(3)] == [19, 4, 4]
+    for b in range(w.batch):
+        cl = w.cached_lens[b]
+        nc = cl // w.page_size
+        k = oracle.n_selected(w.top_frac, nc)
+        for i in range(w.n_qblocks):
+            want = set()
+            for t in range(i * w.q_block, min((i + 1) * w.q_block, w.chunk_len)):
+                for pos in range(cl + t + 1):
+                    if pos // w.page_size >= nc:
+                        want.add(pos // w.page_size)
+            for h in range(w.num_q_heads):
+                row = bits[b, h, i]
+                assert set(np.nonzero(row[nc:])[0] + nc) == want
+                cnt = int(row[:nc].sum())
+                assert k <= cnt <= k + min(w.sink_blocks + w.local_blocks, nc)
+
+
+def test_unaligned_all_open_equals_dense_sdpa(workload_inputs):
+    """All-ones masks on sequences of 1000, 37 and 0 cached tokens + a 200-token
+    chunk, NaN in every K/V row past each sequence end: the oracle equals torch's
+    fp64 attention over the contiguous sequence, and no NaN gets through."""
+    d = workload_inputs("tiny_unaligned")
+    w = d["workload"]
+    nkb = [w.n_kv_blocks(b) for b in range(w.batch)]
+    ones = np.full((w.batch, w.num_q_heads, w.n_qblocks, w.words),
+                   np.uint64(0xFFFFFFFFFFFFFFFF))
+    T = oracle.block_tables(ones, w.group_size, nkb)
+    assert T == oracle.dense_tables(nkb, w.num_groups)
+    out, lse = oracle.chunk_attention(d["q"], d["k_pool"], d["v_pool"], d["page_table"],
+                                      d["cached_len"], T, w.group_size, w.sm_scale)
+    assert np.isfinite(out).all() and np.isfinite(lse).all()
+    for b in range(w.batch):
+        for h in range(w.num_q_heads):
+            ref = _sdpa_ref(d, b, h, np.arange(w.chunk_len))
+            np.testing.assert_allclose(out[b, :, h, :], ref, atol=1e-12, rtol=0)
+
+
+def test_unaligned_block_sparse_rows_equal_masked_sdpa(workload_inputs):
+    """Block-sparse execution of the estimator's raw mask rows on unaligned lengths
+    == masked fp64 SDPA with that row's blocks open (partial last Q-block and page)."""
+    d = workload_inputs("tiny_unaligned")
+    w = d["workload"]
+    masks = oracle.estimate_masks(d["q"], d["k_pool"], d["page_table"], d["cached_len"],
+                                  w.page_size, w.q_block, w.chunk_len, w.words,
+                                  oracle.EstimatorParams(w.top_frac, w.sink_blocks,
+                                                         w.local_blocks))
+    bits = oracle.unpack_masks(masks)
+    out, _ = oracle.block_sparse_attention(d["q"], d["k_pool"], d["v_pool"], d["page_table"],
+                                           d["cached_len"], bits, w.q_block, w.sm_scale)
+    assert np.isfinite(out).all()
+    for b in range(w.batch):
+        for h in (0, 5):
+            for i in range(w.n_qblocks):
+                t = np.arange(i * w.q_block, min((i + 1) * w.q_block, w.chunk_len))
+                keep = [j for j in range(w.n_kv_blocks(b)) if bits[b, h, i, j]]
+                ref = _sdpa_ref(d, b, h, t, keep_blocks=keep)
+                np.testing.assert_allclose(out[b, t, h, :], ref, atol=1e-12, rtol=0)
 
 
 def test_estimator_recall_and_popcount(oracle_estimate, workload_inputs):

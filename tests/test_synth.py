@@ -118,3 +118,22 @@ def test_subgroup_densities_qwen_shape(oracle_estimate, workload_inputs):
     bits = oracle.unpack_masks(masks)
     assert all(bits[b, h, i, j] for (b, kvh, j, h, i) in d["needles"])
 
+
+
+def test_unaligned_workload_shapes_and_poisoned_tails(workload_inputs):
+    """Lengths that are not multiples of 64: ceil block and Q-block counts, and
+    NaN in exactly the K/V rows of each last page past the sequence end."""
+    d = workload_inputs("tiny_unaligned")
+    w = d["workload"]
+    assert w.n_qblocks == 4                                    # 200 = 3 * 64 + 8
+    assert [w.n_cached_blocks(b) for b in range(3)] == [15, 0, 0]
+    assert [w.n_kv_blocks(b) for b in range(3)] == [19, 4, 4]
+    for b in range(w.batch):
+        n = w.n_kv_blocks(b)
+        valid = w.seq_len(b) - 64 * (n - 1)                    # 24, 45, 8 rows
+        for kvh in range(w.num_kv_heads):
+            for pool in (d["k_pool"], d["v_pool"]):
+                last = synth.bf16_bits_to_f32(pool[d["page_table"][b, kvh, n - 1]])
+                assert np.isfinite(last[:valid]).all() and np.isnan(last[valid:]).all()
+                before = synth.bf16_bits_to_f32(pool[d["page_table"][b, kvh, :n - 1]])
+                assert np.isfinite(before).all()
