@@ -86,6 +86,17 @@ typedef __attribute__((address_space(3))) void lds_void;
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
+// Raw buffer resource of one page (64 rows x D bf16).  The page copies use
+// buffer loads to LDS rather than global_load_lds: while a global_load_lds is
+// in flight the compiler cannot count LDS reads (it treats the copy as a flat
+// access that may touch LDS) and makes every operand read wait for all
+// outstanding LDS reads, which defeats the fragment prefetch.  Offsets past
+// the page would read 0 instead of faulting.
+constexpr int kRawBufferWord3 = 0x00020000;   // gfx9 raw buffer, 32-bit data format
+#define CA_PAGE_RSRC(page, D)                                                              \
+  __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(page), 0, kPage * (D) * 2,      \
+                                    kRawBufferWord3)
+
 // Copy one page (64 rows x D bf16, contiguous in HBM) into an LDS tile with
 // direct-to-LDS loads.  Each wave instruction fills 1 KB of the tile, lane l
 // writing bytes [16l, 16l+16); the lane's source is the chunk that the
@@ -103,7 +114,8 @@ __device__ __forceinline__ void page_to_lds(const uint16_t* __restrict__ src, ui
     const int cpos = lane % CPR;
     const int c = IS_V ? v_swz<D>(r, cpos) : k_swz<D>(r, cpos);
     const uint32_t off = (uint32_t)(r * D + c * 8);   // unsigned: scalar base + 32-bit offset
-    __builtin_amdgcn_global_load_lds(src + off, (lds_void*)(tile + inst * 512), 16, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(CA_PAGE_RSRC(src, D), (lds_void*)(tile + inst * 512),
+                                             16, 2 * off, 0, 0, 0);
   }
 }
 
@@ -120,7 +132,8 @@ __device__ __forceinline__ void page_part_to_lds(const uint16_t* __restrict__ sr
   const int cpos = lane % CPR;
   const int c = IS_V ? v_swz<D>(r, cpos) : k_swz<D>(r, cpos);
   const uint32_t off = (uint32_t)(r * D + c * 8);
-  __builtin_amdgcn_global_load_lds(src + off, (lds_void*)(tile + inst * 512), 16, 0, 0);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(CA_PAGE_RSRC(src, D), (lds_void*)(tile + inst * 512),
+                                           16, 2 * off, 0, 0, 0);
 }
 
 // Wait for this wave's direct-to-LDS copies and tell the compiler that the
