@@ -44,6 +44,8 @@ def parse():
     ap.add_argument("--chunk-sweep", action="store_true",
                     help="also prefill one 128K sequence chunk by chunk at chunk sizes "
                          "512/1024/2048 (Table 5) and report cumulative stage times")
+    ap.add_argument("--density-sweep", action="store_true",
+                    help="attention at matched cached densities on seeded random tables")
     ap.add_argument("--threshold-sweep", action="store_true",
                     help="also run the alpha-threshold selector at several (alpha, temperature)")
     ap.add_argument("--no-arms", action="store_true",
@@ -98,20 +100,95 @@ def copy_calibration():
 def selected_flops(w, ip: np.ndarray, ix: np.ndarray) -> float:
     """4*D per unmasked (query, key) pair over each group's table.
 
-    Cached blocks are fully visible to every chunk query; the chunk's own
-    blocks contribute the causal triangle C(C+1)/2 per query head.
+    Full cached blocks are visible to every chunk query; the cached tokens of
+    a block shared with the chunk (a cached length that is not a multiple of
+    the page) too, and that block is always in the table; the chunk's own
+    tokens contribute the causal triangle C(C+1)/2 per query head.
     """
     G = w.num_q_heads // w.group_size
     C = w.chunk_len
     tot = 0.0
     for b in range(w.batch):
         nc = w.n_cached_blocks(b)
+        tail = w.cached_lens[b] - nc * w.page_size
         for g in range(G):
             r = b * G + g
             row = ix[ip[r]:ip[r + 1]]
             cached = int(np.count_nonzero(row < nc))
-            tot += w.group_size * (C * w.page_size * cached + C * (C + 1) / 2)
+            tot += w.group_size * (C * (w.page_size * cached + tail) + C * (C + 1) / 2)
     return tot * 4 * w.head_dim
+
+
+def percentiles(v) -> dict:
+    return {"median": round(float(np.median(v)), 4), "p10": round(float(np.percentile(v, 10)), 4),
+            "p90": round(float(np.percentile(v, 90)), 4)}
+
+
+def per_launch_ms(torch, fn, n, stream, flush=None):
+    """n single launches of fn, each between its own pair of events; with
+    flush, a 512 MiB buffer is overwritten before each launch so that no
+    K/V page is left in L2 or the Infinity Cache."""
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    out = []
+    for _ in range(n):
+        if flush is not None:
+            flush.fill_(1)
+        e0, e1 = ev(), ev()
+        host_ahead(torch)
+        e0.record(stream)
+        fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        out.append(e0.elapsed_time(e1))
+    return out
+
+
+DENSITIES = (0.1, 0.2, 0.3, 0.5, 1.0)
+
+
+def density_sweep(ca, p, w, q, kp, vp, pt, dense_ms, args, stream, ev):
+    """The attention kernel on seeded random tables that keep a fixed fraction
+    of every sequence's full cached blocks (plus all chunk blocks), the
+    execution-only view of Sec. 4.4: kernel throughput separated from what
+    any selector keeps."""
+    import torch
+
+    import synth
+
+    gs = w.group_size
+    G = w.num_q_heads // gs
+    chunk_blocks = {w.n_kv_blocks(b) - w.n_cached_blocks(b) for b in range(w.batch)}
+    if len(chunk_blocks) != 1:
+        return {"skipped": "sequences differ in their number of chunk blocks"}
+    ncb = [w.n_cached_blocks(b) for b in range(w.batch)]
+    out = torch.empty_like(q)
+    aws_n = ca.attention_workspace_bytes(p, gs, 0)
+    aws = torch.empty(aws_n, dtype=torch.uint8, device=q.device) if aws_n else None
+    res = []
+    for dens in DENSITIES:
+        ip, ix = synth.random_tables(w.seed, w.batch, G, ncb, next(iter(chunk_blocks)), dens)
+        tabs = (torch.from_numpy(ip).to(q.device),
+                torch.from_numpy(np.concatenate([ix, np.zeros(max(1, G * w.batch * w.max_kv_blocks
+                                                                  - len(ix)), np.int32)])
+                                 ).to(q.device))
+        ca.validate_tables(p, gs, tabs)
+        run = lambda: ca.chunk_attention(p, q, (kp, vp), pt, tabs, gs, w.sm_scale,
+                                         num_splits=0, out=out, ws=aws)
+        for _ in range(args.warmup):
+            run()
+        torch.cuda.synchronize()
+        t0, t1 = ev(), ev()
+        t0.record(stream)
+        for _ in range(args.steps):
+            run()
+        t1.record(stream)
+        torch.cuda.synchronize()
+        ms = t0.elapsed_time(t1) / args.steps
+        tf = selected_flops(w, ip, ix) / (ms * 1e-3) / 1e12
+        res.append({"cached_density": dens, "attention_ms": round(ms, 4),
+                    "tflops": round(tf, 1), "frac_of_peak": round(tf / PEAK_BF16_TFLOPS, 4),
+                    "speedup_vs_dense": round(dense_ms / ms, 3)})
+    return res
 
 
 def cpu_baseline(w, d, tables_T, sample_queries: int):
@@ -523,6 +600,13 @@ def main():
     a1.record(stream)
     torch.cuda.synchronize()
     attn_ms = a0.elapsed_time(a1) / args.steps
+    # the same launch one at a time: warm caches, then after a 512 MiB overwrite
+    one = lambda: ca.chunk_attention(p, q, (kp, vp), pt, tables, gs, w.sm_scale, num_splits=0,
+                                     out=out, lse=lse, ws=aws)
+    warm_each = per_launch_ms(torch, one, args.steps, stream)
+    scratch = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    flushed_each = per_launch_ms(torch, one, args.steps, stream, flush=scratch)
+    del scratch
 
     # ---- dense paged baseline ----
     dargs = dict(num_splits=0, out=out_dense, ws=dws)
@@ -572,6 +656,8 @@ def main():
         "speedup_vs_dense": round(dense_ms / ms_per_step, 3),
         "speedup_vs_dense_kernel_only": round(dense_ms / attn_ms, 3),
         "attention_kernel_ms": round(attn_ms, 4),
+        "attention_kernel_single_launch_ms": {"warm": percentiles(warm_each),
+                                              "flushed": percentiles(flushed_each)},
         "executed_cached_density": round(density, 4),
         "densities": stage_densities(w, np.unpackbits(bufs["masks"].cpu().numpy().view(np.uint8),
                                                       axis=-1, bitorder="little").astype(bool)),
@@ -587,6 +673,8 @@ def main():
     if not args.no_arms:
         res["arms"] = strategy_arms(ca, p, w, q, kp, vp, pt, bufs["masks"], tables, ip,
                                     args, stream, ev)
+    if args.density_sweep:
+        res["density_sweep"] = density_sweep(ca, p, w, q, kp, vp, pt, dense_ms, args, stream, ev)
     if args.threshold_sweep:
         res["threshold_sweep"] = threshold_sweep(ca, p, w, q, kp, vp, pt, dense_ms, args,
                                                  stream, ev)

@@ -483,6 +483,23 @@ def test_attention_workloads_sampled(name, workload_inputs, oracle_estimate):
     print(name, "sharp", compare_attention(got, lse, ref, ref_lse, rows[::3]))
 
 
+@pytest.mark.parametrize("density", [0.1, 0.5])
+def test_attention_matched_density_tables_sampled(density, workload_inputs):
+    """Seeded random tables at a fixed cached density (the tables of the bench's
+    matched-density sweep), sampled rows against the oracle."""
+    d = workload_inputs("llama8b_32k")
+    w = d["workload"]
+    p = _problem(w)
+    x = device_inputs(d)
+    ip, ix = synth.random_tables(w.seed, w.batch, w.num_groups, [w.n_cached_blocks(0)],
+                                 w.n_kv_blocks(0) - w.n_cached_blocks(0), density)
+    got, lse = _run_attention(p, x, (ip, ix), w.group_size, w.sm_scale, num_splits=0)
+    rows = sample_rows(w.batch, w.num_q_heads, w.chunk_len, seed=w.seed + 5, heads_per_b=2,
+                       n_random=8)
+    ref, ref_lse = _oracle_rows(d, (ip, ix), w.group_size, w.sm_scale, rows)
+    print(density, compare_attention(got, lse, ref, ref_lse, rows))
+
+
 @pytest.mark.parametrize("name", ["llama8b_32k", "batched_ragged_4seq", "llama8b_unaligned"])
 def test_dense_baseline_sampled(name, workload_inputs):
     d = workload_inputs(name)
