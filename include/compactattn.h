@@ -224,12 +224,20 @@ ca_status ca_estimate_tables(const ca_problem* p, const uint16_t* q, const uint1
  *    lse = -inf.
  *    num_splits: 1 = one pass per query tile; > 1 = the table of each row is
  *    cut into that many consecutive pieces whose partial results are merged
- *    by log-sum-exp (needs workspace); 0 = let the library choose (it uses
- *    splits only when the query tiles alone cannot fill the GPU and the
- *    workspace is large enough).  Workspace:
- *    ca_attention_workspace_bytes(p, group_size, num_splits) bytes (0 when no
- *    split is needed; for num_splits = 0 it returns the size that lets the
- *    library pick freely).
+ *    by log-sum-exp (needs workspace); 0 = let the library choose:
+ *      - when the query tiles fill the GPU, B * G is a multiple of 8 and the
+ *        workspace holds ca_attention_workspace_bytes(p, group_size, 0):
+ *        every table row is cut in two at a point computed on the GPU from
+ *        the table lengths, so that the 8 XCDs of the MI355X carry equal
+ *        loads (rows r with r % 8 = x run on XCD x, which also runs the
+ *        second pieces of XCD x-1's rows); the dense baseline does this only
+ *        when the sequences differ in length;
+ *      - otherwise splits only when the query tiles alone cannot fill the
+ *        GPU and the workspace is large enough.
+ *    The result does not depend on the choice beyond floating-point rounding.
+ *    Workspace: ca_attention_workspace_bytes(p, group_size, num_splits)
+ *    bytes (0 when no split is needed; for num_splits = 0 it returns the
+ *    size that lets the library pick freely).
  * ---------------------------------------------------------------------- */
 size_t ca_attention_workspace_bytes(const ca_problem* p, int32_t group_size,
                                     int32_t num_splits);

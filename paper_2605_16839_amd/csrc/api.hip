@@ -116,6 +116,27 @@ int auto_splits(const ca::Dims& d, int group_size, size_t ws_bytes, bool have_ws
   return s < 1 ? 1 : s;
 }
 
+// num_splits = 0 on per-group tables whose query tiles already fill the GPU:
+// two pieces per table row, cut so that the 8 XCDs carry equal loads (the
+// execution groups of one XCD otherwise differ in table length).  Needs the
+// rows to spread evenly over the XCDs.  Dense rows of equal length (every
+// sequence the same length) are balanced already.
+bool xcd_balance_ok(const ca::Dims& d, const ca_problem* p, int group_size, int table_mode,
+                    bool dense) {
+  if (table_mode == ca::kTablesPerQTile) return false;
+  const int R = d.B * (d.Hq / group_size);
+  if (R % 8 != 0) return false;
+  if (ca::attn_base_workgroups(d, group_size, table_mode) <
+      ca::attn_resident_workgroups(table_mode))
+    return false;
+  if (dense) {
+    for (int b = 1; b < d.B; ++b)
+      if (p->cached_len_host[b] != p->cached_len_host[0]) return true;
+    return false;
+  }
+  return true;
+}
+
 ca_status run_attention(const ca_problem* p, const uint16_t* q, const uint16_t* k_pool,
                         const uint16_t* v_pool, const int32_t* page_table,
                         const int32_t* kv_indptr, const int32_t* kv_indices, int32_t group_size,
@@ -141,7 +162,12 @@ ca_status run_attention(const ca_problem* p, const uint16_t* q, const uint16_t* 
   if (num_splits < 0 || num_splits > 64)
     return fail(CA_ERR_SHAPE, "num_splits %d out of range [0, 64]", num_splits);
   int splits = num_splits;
-  if (splits == 0) splits = auto_splits(d, group_size, ws_bytes, ws != nullptr, table_mode);
+  bool xcd = false;
+  if (splits == 0) {
+    xcd = xcd_balance_ok(d, p, group_size, table_mode, dense) && ws != nullptr &&
+          ws_bytes >= ca::attn_xcd_ws_bytes(d, group_size);
+    splits = xcd ? 2 : auto_splits(d, group_size, ws_bytes, ws != nullptr, table_mode);
+  }
   if (splits > 1) {
     const size_t need = ca::attn_ws_bytes(d, splits);
     if (ws == nullptr || ws_bytes < need)
@@ -161,6 +187,7 @@ ca_status run_attention(const ca_problem* p, const uint16_t* q, const uint16_t* 
   L.group_size = group_size;
   L.sm_scale = sm_scale;
   L.splits = splits;
+  L.xcd_balanced = xcd;
   L.ws = ws;
   L.dense = dense;
   L.table_mode = table_mode;
@@ -399,7 +426,14 @@ size_t ca_attention_workspace_bytes(const ca_problem* p, int32_t group_size, int
   if (group_size < 1 || check(p, group_size, &d) != CA_OK) return 0;
   if (num_splits < 0 || num_splits > 64) return 0;
   int s = num_splits;
-  if (s == 0) s = auto_splits(d, group_size, (size_t)-1, true);
+  if (s == 0) {
+    // room for the XCD-balanced split, or for the splits chosen without it
+    const size_t uni = ca::attn_ws_bytes(d, auto_splits(d, group_size, (size_t)-1, true));
+    const size_t bal = xcd_balance_ok(d, p, group_size, ca::kTablesPerGroup, false)
+                           ? ca::attn_xcd_ws_bytes(d, group_size)
+                           : 0;
+    return bal > uni ? bal : uni;
+  }
   return ca::attn_ws_bytes(d, s);
 }
 

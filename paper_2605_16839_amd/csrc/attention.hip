@@ -56,7 +56,12 @@ struct AttnArgs {
   int table_mode;          // kTablesPerGroup / kTablesPerQTile / kTablesPacked
   long long packed_pages;  // capacity of the packed pools (kTablesPacked)
   float scale_log2;
+  // XCD-balanced two-piece split (splits == 2): table row r is cut at entry
+  // split_at[r]; nullptr = cut in the middle
+  const int32_t* split_at;
 };
+
+constexpr int kXcds = 8;   // MI355X: 8 accelerator complex dies, 32 CUs and one L2 each
 
 // Swizzled position (16-byte chunk) of chunk c of row r in an LDS page tile.
 // gfx950 LDS has 64 banks of 4 bytes; a 16-byte read is served 16 lanes per
@@ -272,9 +277,25 @@ __global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnA
   int bid = blockIdx.x;
   const int nwg = gridDim.x;
   if ((nwg & 7) == 0) bid = (bid & 7) * (nwg >> 3) + (bid >> 3);
-  const int sp = bid % a.splits;
-  const int qt = (bid / a.splits) % a.n_qtiles;
-  const int rowid = bid / (a.splits * a.n_qtiles);
+  int sp, qt, rowid;
+  if (a.split_at != nullptr) {
+    // XCD x (logical workgroups [x, x+1) * nwg/8) holds the rows r with
+    // r % 8 = x (group x of every sequence when G = 8); it first runs piece 0
+    // of its own rows' tiles, then piece 1 of the previous XCD's rows' tiles:
+    // each piece is read by all tiles of its row on one XCD, in step, through
+    // that XCD's L2
+    const int per_xcd = nwg / kXcds, own = per_xcd / 2;
+    const int x = bid / per_xcd;
+    int j = bid % per_xcd;
+    sp = j < own ? 0 : 1;
+    if (sp) j -= own;
+    rowid = (sp ? x + kXcds - 1 : x) % kXcds + kXcds * (j / a.n_qtiles);
+    qt = j % a.n_qtiles;
+  } else {
+    sp = bid % a.splits;
+    qt = (bid / a.splits) % a.n_qtiles;
+    rowid = bid / (a.splits * a.n_qtiles);
+  }
   const int b = rowid / a.G;
   const int g = rowid % a.G;
   const int gs = a.group_size;
@@ -307,8 +328,16 @@ __global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnA
     tbase = a.kv_indptr[trow];
     len = a.kv_indptr[trow + 1] - tbase;
   }
-  const int e0 = (int)(((long long)len * sp) / a.splits);
-  const int e1 = (int)(((long long)len * (sp + 1)) / a.splits);
+  int e0, e1;
+  if (a.split_at != nullptr) {
+    int cut = a.split_at[rowid];
+    cut = cut < 0 ? 0 : (cut > len ? len : cut);
+    e0 = sp ? cut : 0;
+    e1 = sp ? len : cut;
+  } else {
+    e0 = (int)(((long long)len * sp) / a.splits);
+    e1 = (int)(((long long)len * (sp + 1)) / a.splits);
+  }
   const int32_t* ptab = a.page_table + ((size_t)b * a.Hkv + kvh) * a.max_kv_blocks;
 
   bf16x8 qf[2][NKS];
@@ -783,6 +812,65 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
   if (lse != nullptr && sub == 0) lse[row] = wsum > 0.f ? mx + logf(wsum) : -INFINITY;
 }
 
+// Cut points of the XCD-balanced two-piece split.  The R = 8m table rows are
+// spread over the 8 XCDs by r % 8 (XCD x holds rows x, x+8, ..; its load
+// alone is L_x table entries).  XCD x runs the first C_x
+// entries of its own rows and the remaining L_{x-1} - C_{x-1} of the previous
+// XCD's rows, so its load is C_x + L_{x-1} - C_{x-1}; equal loads S = sum L / 8
+// give C_x = C_{x-1} + S - L_{x-1}, fixed up to the choice of C_0, which is
+// taken in the middle of the range that keeps every 0 <= C_x <= L_x (clamped
+// when no such choice exists).  C_x is shared among the rows of XCD x in
+// proportion to their lengths.  Dense tables: row r has nKB_b entries.
+__global__ __launch_bounds__(256) void xcd_split_kernel(const int32_t* __restrict__ kv_indptr,
+                                                        const int32_t* __restrict__ cached_len,
+                                                        int32_t* __restrict__ split_at, int R,
+                                                        int G, int C, int dense) {
+  __shared__ long long L[kXcds], Cx[kXcds];
+  const int m = R / kXcds;
+  const int t = threadIdx.x;
+  auto row_len = [&](int r) -> long long {
+    return dense ? (long long)blocks_for(cached_len[r / G] + C)
+                 : (long long)(kv_indptr[r + 1] - kv_indptr[r]);
+  };
+  if (t < kXcds) {   // L_x, one thread per XCD
+    long long v = 0;
+    for (int k = 0; k < m; ++k) v += row_len(t + kXcds * k);
+    L[t] = v;
+  }
+  __syncthreads();
+  if (t == 0) {
+    long long total = 0;
+    for (int x = 0; x < kXcds; ++x) total += L[x];
+    // D_x = sum_{k=1..x} (S - L_{k-1}) in units of 1/8 entry (S = total / 8);
+    // 8 C_0 is taken in the middle of the range keeping 0 <= C_x <= L_x
+    long long D8[kXcds];
+    D8[0] = 0;
+    for (int x = 1; x < kXcds; ++x) D8[x] = D8[x - 1] + total - 8 * L[x - 1];
+    long long lo = 0, hi = 8 * L[0];
+    for (int x = 0; x < kXcds; ++x) {
+      lo = lo > -D8[x] ? lo : -D8[x];
+      hi = hi < 8 * L[x] - D8[x] ? hi : 8 * L[x] - D8[x];
+    }
+    const long long c0 = (lo + hi) / 2;   // lo > hi: no exact balance, clamped below
+    for (int x = 0; x < kXcds; ++x) {
+      long long cx = (c0 + D8[x]) / 8;
+      Cx[x] = cx < 0 ? 0 : (cx > L[x] ? L[x] : cx);
+    }
+  }
+  __syncthreads();
+  if (t < kXcds) {   // C_x over the rows of XCD x in proportion to their lengths
+    long long before = 0;
+    for (int k = 0; k < m; ++k) {
+      const int r = t + kXcds * k;
+      const long long len = row_len(r);
+      const long long a0 = L[t] > 0 ? (before * Cx[t]) / L[t] : 0;
+      const long long a1 = L[t] > 0 ? ((before + len) * Cx[t]) / L[t] : 0;
+      split_at[r] = (int32_t)(a1 - a0);
+      before += len;
+    }
+  }
+}
+
 int attn_rows_per_workgroup(int table_mode) {
   return 64 * (table_mode == kTablesPerQTile ? kWavesQTile : kWavesGroup);
 }
@@ -805,6 +893,10 @@ size_t attn_ws_bytes(const Dims& d, int splits) {
   if (splits <= 1) return 0;
   const size_t rows = (size_t)d.B * d.Hq * d.C;
   return (size_t)splits * rows * (d.D + 1) * sizeof(float);
+}
+
+size_t attn_xcd_ws_bytes(const Dims& d, int group_size) {
+  return attn_ws_bytes(d, 2) + (size_t)d.B * (d.Hq / group_size) * sizeof(int32_t);
 }
 
 template <int D, int NW>
@@ -840,6 +932,16 @@ hipError_t launch_attention(const Dims& d, const AttnLaunch& L, hipStream_t st) 
   a.table_mode = L.table_mode;
   a.packed_pages = L.packed_pages;
   a.scale_log2 = L.sm_scale * kLog2e;
+  a.split_at = nullptr;
+  if (L.xcd_balanced) {
+    const int R = d.B * a.G;
+    int32_t* cut = reinterpret_cast<int32_t*>(static_cast<char*>(L.ws) + attn_ws_bytes(d, 2));
+    xcd_split_kernel<<<1, 256, 0, st>>>(L.kv_indptr, L.cached_len, cut, R, a.G, d.C,
+                                        L.dense ? 1 : 0);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    a.split_at = cut;
+  }
   const int nwg = attn_base_workgroups(d, L.group_size, L.table_mode) * L.splits;
   const bool qtile = L.table_mode == kTablesPerQTile;
   if (d.D == 128) {

@@ -68,12 +68,16 @@ struct AttnLaunch {
   bool dense;
   int table_mode = kTablesPerGroup;
   long long packed_pages = 0;
+  // splits == 2 with the cut of every table row chosen so that the 8 XCDs
+  // carry equal loads (needs B * G % 8 == 0 and attn_xcd_ws_bytes of ws)
+  bool xcd_balanced = false;
 };
 int attn_rows_per_workgroup(int table_mode);             // (head, query) rows per workgroup
 int attn_query_tile(int group_size, int table_mode);     // chunk queries per workgroup
 int attn_base_workgroups(const Dims& d, int group_size, int table_mode);
 int attn_resident_workgroups(int table_mode);            // workgroups the GPU holds at once
 size_t attn_ws_bytes(const Dims& d, int splits);
+size_t attn_xcd_ws_bytes(const Dims& d, int group_size);
 hipError_t launch_attention(const Dims& d, const AttnLaunch& a, hipStream_t st);
 hipError_t launch_gather(const Dims& d, const uint16_t* k_pool, const uint16_t* v_pool,
                          const int32_t* page_table, const int32_t* kv_indptr,

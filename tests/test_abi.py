@@ -97,8 +97,13 @@ def test_workspace_sizes(lib):
     assert ca.tables_workspace_bytes(p, 4) == 8 * 32 * 8 + 8 * 4
     assert ca.attention_workspace_bytes(p, 4, 1) == 0
     assert ca.attention_workspace_bytes(p, 4, 2) == 2 * 32 * 2048 * 129 * 4
-    # 512 query tiles already fill the GPU: automatic choice needs no workspace
-    assert ca.attention_workspace_bytes(p, 4, 0) == 0
+    # 256 query tiles fill the GPU and the 8 table rows spread over the 8 XCDs:
+    # the automatic choice cuts every row in two (two partial sets + 8 cut points)
+    assert ca.attention_workspace_bytes(p, 4, 0) == 2 * 32 * 2048 * 129 * 4 + 8 * 4
+    # 6 table rows do not spread evenly over the XCDs: the uniform choice, here
+    # 2 splits because 192 query tiles cannot fill the 256 resident workgroups
+    six = _prob(num_q_heads=24, num_kv_heads=6)
+    assert ca.attention_workspace_bytes(six, 4, 0) == 2 * 24 * 2048 * 129 * 4
     tiny = _prob(num_q_heads=4, num_kv_heads=1, head_dim=64, q_block=64, chunk_len=256,
                  max_kv_blocks=20, cached_len=[1024])
     assert ca.attention_workspace_bytes(tiny, 4, 0) > 0

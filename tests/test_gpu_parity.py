@@ -500,6 +500,29 @@ def test_attention_matched_density_tables_sampled(density, workload_inputs):
     print(density, compare_attention(got, lse, ref, ref_lse, rows))
 
 
+def test_attention_xcd_split_unbalanceable_tables(workload_inputs):
+    """Tables no cut can balance over the XCDs (group 7 holds every cached
+    block, the others only the chunk): the automatic two-piece split clamps its
+    cut points and leaves empty pieces, and still matches the oracle."""
+    d = workload_inputs("llama8b_32k")
+    w = d["workload"]
+    p = _problem(w)
+    x = device_inputs(d)
+    nc, nkb = w.n_cached_blocks(0), w.n_kv_blocks(0)
+    rows = [list(range(nc, nkb))] * (w.num_groups - 1) + [list(range(nkb))]
+    T = [rows]
+    csr = oracle.tables_to_csr(T)
+    got0, lse0 = _run_attention(p, x, csr, w.group_size, w.sm_scale, num_splits=0)
+    got1, lse1 = _run_attention(p, x, csr, w.group_size, w.sm_scale, num_splits=1)
+    rows_s = sample_rows(w.batch, w.num_q_heads, w.chunk_len, seed=w.seed + 11, heads_per_b=3,
+                         n_random=8)
+    ref, ref_lse = _oracle_rows(d, T, w.group_size, w.sm_scale, rows_s)
+    print("auto", compare_attention(got0, lse0, ref, ref_lse, rows_s))
+    print("one split", compare_attention(got1, lse1, ref, ref_lse, rows_s))
+    # the two schedules differ only in rounding
+    assert np.abs(got0 - got1).max() <= 2e-2 and np.abs(lse0 - lse1).max() <= 1e-3
+
+
 @pytest.mark.parametrize("name", ["llama8b_32k", "batched_ragged_4seq", "llama8b_unaligned"])
 def test_dense_baseline_sampled(name, workload_inputs):
     d = workload_inputs(name)
