@@ -57,8 +57,10 @@ struct AttnArgs {
   long long packed_pages;  // capacity of the packed pools (kTablesPacked)
   float scale_log2;
   // XCD-balanced two-piece split (splits == 2): table row r is cut at entry
-  // split_at[r]; nullptr = cut in the middle
+  // split_at[r]; -1 = not cut, run whole as piece 0; -2 = not cut, run whole
+  // as piece 1; nullptr = every row cut in the middle
   const int32_t* split_at;
+  int rows_per_unit;   // table rows that read one KV head's pages together
 };
 
 constexpr int kXcds = 8;   // MI355X: 8 accelerator complex dies, 32 CUs and one L2 each
@@ -292,9 +294,25 @@ __global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnA
     rowid = (sp ? x + kXcds - 1 : x) % kXcds + kXcds * (j / a.n_qtiles);
     qt = j % a.n_qtiles;
   } else {
-    sp = bid % a.splits;
-    qt = (bid / a.splits) % a.n_qtiles;
-    rowid = bid / (a.splits * a.n_qtiles);
+    // XCD x holds the units u with u % 8 = x when the units spread evenly (a
+    // unit = the table rows that read one KV head's pages: one group row, or
+    // the heads of one KV group in the per-(head, Q-block) layout), so that
+    // sequences of different lengths share every XCD; otherwise rows in order
+    const int per_row = a.splits * a.n_qtiles;
+    const int U = a.rows_per_unit;
+    const int units = nwg / per_row / U;
+    int rest;
+    if ((nwg & 7) == 0 && units % kXcds == 0) {
+      const int per_xcd = nwg / kXcds, per_unit = U * per_row;
+      const int x = bid / per_xcd, j = bid % per_xcd;
+      rowid = (x + kXcds * (j / per_unit)) * U + (j % per_unit) / per_row;
+      rest = j % per_row;
+    } else {
+      rowid = bid / per_row;
+      rest = bid % per_row;
+    }
+    sp = rest % a.splits;
+    qt = rest / a.splits;
   }
   const int b = rowid / a.G;
   const int g = rowid % a.G;
@@ -329,9 +347,15 @@ __global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnA
     len = a.kv_indptr[trow + 1] - tbase;
   }
   int e0, e1;
+  bool whole = a.splits == 1;   // the piece is the whole row: final output
   if (a.split_at != nullptr) {
     int cut = a.split_at[rowid];
-    cut = cut < 0 ? 0 : (cut > len ? len : cut);
+    if (cut < 0) {              // the row is not cut: one piece runs it, the other nothing
+      if (sp != (cut == -1 ? 0 : 1)) return;
+      whole = true;
+      cut = sp ? 0 : len;
+    }
+    cut = cut > len ? len : cut;
     e0 = sp ? cut : 0;
     e1 = sp ? len : cut;
   } else {
@@ -683,7 +707,7 @@ __global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnA
     const float lse_val = l_tot > 0.f ? (m_run[c] + log2f(l_tot)) * kLn2 : -INFINITY;
     const size_t qrow_idx = ((size_t)b * a.Hq + head[c]) * a.C + tq[c];
     if (!valid[c]) continue;
-    if (a.splits == 1) {
+    if (whole) {
       uint16_t* orow = a.out + (((size_t)b * a.C + tq[c]) * a.Hq + head[c]) * D;
 #pragma unroll
       for (int x = 0; x < NDT; ++x) {
@@ -778,11 +802,17 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
                                                       const float* __restrict__ part_lse,
                                                       uint16_t* __restrict__ out,
                                                       float* __restrict__ lse, int B, int Hq,
-                                                      int C, int splits) {
+                                                      int C, int splits,
+                                                      const int32_t* __restrict__ split_at,
+                                                      int G, int group_size) {
   constexpr int PER = D / 32;
   const size_t nrows = (size_t)B * Hq * C;
   const size_t row = (size_t)blockIdx.x * 8 + (threadIdx.x >> 5);
   if (row >= nrows) return;
+  if (split_at != nullptr) {   // a table row that was not cut wrote its output already
+    const int hh = (int)((row / C) % Hq), bb = (int)(row / ((size_t)C * Hq));
+    if (split_at[bb * G + hh / group_size] < 0) return;
+  }
   const int sub = threadIdx.x & 31;
   float mx = -INFINITY;
   for (int i = 0; i < splits; ++i) mx = fmaxf(mx, part_lse[(size_t)i * nrows + row]);
@@ -851,7 +881,9 @@ __global__ __launch_bounds__(256) void xcd_split_kernel(const int32_t* __restric
       lo = lo > -D8[x] ? lo : -D8[x];
       hi = hi < 8 * L[x] - D8[x] ? hi : 8 * L[x] - D8[x];
     }
-    const long long c0 = (lo + hi) / 2;   // lo > hi: no exact balance, clamped below
+    // any feasible C_0 balances; the largest keeps the most entries on their
+    // own XCD, and rows with C_x = L_x (or 0) are not cut at all
+    const long long c0 = lo <= hi ? hi : (lo + hi) / 2;   // lo > hi: clamped below
     for (int x = 0; x < kXcds; ++x) {
       long long cx = (c0 + D8[x]) / 8;
       Cx[x] = cx < 0 ? 0 : (cx > L[x] ? L[x] : cx);
@@ -865,7 +897,8 @@ __global__ __launch_bounds__(256) void xcd_split_kernel(const int32_t* __restric
       const long long len = row_len(r);
       const long long a0 = L[t] > 0 ? (before * Cx[t]) / L[t] : 0;
       const long long a1 = L[t] > 0 ? ((before + len) * Cx[t]) / L[t] : 0;
-      split_at[r] = (int32_t)(a1 - a0);
+      const long long c = a1 - a0;
+      split_at[r] = c >= len ? -1 : (c <= 0 ? -2 : (int32_t)c);
       before += len;
     }
   }
@@ -933,6 +966,7 @@ hipError_t launch_attention(const Dims& d, const AttnLaunch& L, hipStream_t st) 
   a.packed_pages = L.packed_pages;
   a.scale_log2 = L.sm_scale * kLog2e;
   a.split_at = nullptr;
+  a.rows_per_unit = L.table_mode == kTablesPerQTile ? d.Hq / d.Hkv : 1;
   if (L.xcd_balanced) {
     const int R = d.B * a.G;
     int32_t* cut = reinterpret_cast<int32_t*>(static_cast<char*>(L.ws) + attn_ws_bytes(d, 2));
@@ -956,10 +990,10 @@ hipError_t launch_attention(const Dims& d, const AttnLaunch& L, hipStream_t st) 
   const int cgrid = (int)((rows + 7) / 8);
   if (d.D == 128)
     combine_kernel<128><<<cgrid, 256, 0, st>>>(a.part_o, a.part_lse, L.out, L.lse, d.B, d.Hq,
-                                               d.C, L.splits);
+                                               d.C, L.splits, a.split_at, a.G, L.group_size);
   else
     combine_kernel<64><<<cgrid, 256, 0, st>>>(a.part_o, a.part_lse, L.out, L.lse, d.B, d.Hq,
-                                              d.C, L.splits);
+                                              d.C, L.splits, a.split_at, a.G, L.group_size);
   return hipGetLastError();
 }
 
