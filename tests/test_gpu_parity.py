@@ -500,6 +500,24 @@ def test_attention_matched_density_tables_sampled(density, workload_inputs):
     print(density, compare_attention(got, lse, ref, ref_lse, rows))
 
 
+@pytest.mark.parametrize("splits", [1, 2])
+def test_attention_batched_explicit_splits(splits, workload_inputs, oracle_estimate):
+    """Explicit uniform splits on the batched workload: its 32 table rows run in
+    the XCD-interleaved order (row r on XCD r % 8), sampled rows vs the oracle."""
+    name = "batched_ragged_4seq"
+    d = workload_inputs(name)
+    w = d["workload"]
+    p = _problem(w)
+    x = device_inputs(d)
+    masks, _ = oracle_estimate(name)
+    T, csr = _oracle_tables(masks, w)
+    got, lse = _run_attention(p, x, csr, w.group_size, w.sm_scale, num_splits=splits)
+    rows = sample_rows(w.batch, w.num_q_heads, w.chunk_len, seed=w.seed + 13, heads_per_b=2,
+                       n_random=6)
+    ref, ref_lse = _oracle_rows(d, T, w.group_size, w.sm_scale, rows)
+    print(splits, compare_attention(got, lse, ref, ref_lse, rows))
+
+
 def test_attention_xcd_split_unbalanceable_tables(workload_inputs):
     """Tables no cut can balance over the XCDs (group 7 holds every cached
     block, the others only the chunk): the automatic two-piece split clamps its
