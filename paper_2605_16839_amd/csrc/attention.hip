@@ -293,6 +293,7 @@ __global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnA
     if (sp) j -= own;
     rowid = (sp ? x + kXcds - 1 : x) % kXcds + kXcds * (j / a.n_qtiles);
     qt = j % a.n_qtiles;
+    if (sp) qt = a.n_qtiles - 1 - qt;   // second pieces in mirrored tile order
   } else {
     // XCD x holds the units u with u % 8 = x when the units spread evenly (a
     // unit = the table rows that read one KV head's pages: one group row, or
@@ -354,6 +355,18 @@ __global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnA
       if (sp != (cut == -1 ? 0 : 1)) return;
       whole = true;
       cut = sp ? 0 : len;
+    }
+    if (!whole) {
+      // Tile q sees the chunk's blocks up to j_last(q), so its second piece
+      // (which holds them) is longer for later tiles.  The first piece of tile
+      // q moves by (j_last(q) - j_last(mirror q)) / 4 entries: the CUs that
+      // finish their first pieces early take the long second pieces (mirrored
+      // order above), and with the chunk's evenly growing j_last every CU of
+      // the XCD ends together.
+      const int qm = a.n_qtiles - 1 - qt;
+      const int qm_end = (qm + 1) * QT < a.C ? (qm + 1) * QT : a.C;
+      cut += (j_last - (cl + qm_end - 1) / kPage) / 4;
+      cut = cut < 0 ? 0 : cut;
     }
     cut = cut > len ? len : cut;
     e0 = sp ? cut : 0;
