@@ -15,7 +15,7 @@
 //     the softmax statistics are in-lane plus one v_permlane32_swap; then
 //     O^T += V^T P^T with the V^T fragments read straight from the row-major
 //     V page by the gfx950 transpose read ds_read_b64_tr_b16;
-//   * pages go from HBM into LDS with 16-byte direct-to-LDS loads (no
+//   * pages go from HBM into LDS with 16-byte direct-to-LDS buffer loads (no
 //     register round trip) into XOR-swizzled tiles (conflict-free operand
 //     reads);
 //   * software pipeline: step i issues the copies of K(i+2) and V(i), the PV
@@ -26,7 +26,11 @@
 //     the pipeline, one at a time: their keys are compared by absolute
 //     position 64*j + r against cached_len + t (positions from the logical
 //     block id, App. B.2); entries past the tile's last visible block are
-//     dropped (tables are ascending).
+//     dropped (tables are ascending);
+//   * the workgroups of one table row run on one of the 8 XCDs and share its
+//     L2, so each page comes from HBM once; by default every row is cut in
+//     two so that the XCDs carry equal loads (xcd_split_kernel), the two
+//     pieces merged by combine_kernel.
 #include <type_traits>
 #include <utility>
 
