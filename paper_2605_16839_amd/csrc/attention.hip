@@ -524,6 +524,7 @@ __global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnA
     __syncthreads();
     qk_page(SA, k_s0);
     __syncthreads();
+    fence_sp(SA, PB);   // S(0) and the zero P are read by the first step's first slots
   }
 
   // Step i: DMA K(i+2) -> k[i%2], V(i) -> v[i%2]; PV(i-1) from v[(i-1)%2] and
@@ -542,7 +543,9 @@ __global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnA
     const int i2 = i + 2 < n_pipe ? i + 2 : n_pipe - 1;
     const uint16_t* const k_src = page_ptr(a.k_pool, i2);
     const uint16_t* const v_src = page_ptr(a.v_pool, i);
-    fence_sp(sc, po);
+    // No hazard fence here: the last MFMA writing S (slot 62 or 63) and the
+    // last pack writing P come at least ~25 instructions (end of step, barrier,
+    // page pointers) before their first readers in this step (slot 0 and later).
     float mx[2] = {-INFINITY, -INFINITY}, alpha[2] = {1.f, 1.f}, nmb[2] = {0.f, 0.f};
     float ps[2] = {0.f, 0.f};
     bool rb_any = false;
