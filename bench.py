@@ -349,7 +349,7 @@ def chunk_sweep(ca, stream, ev):
     for C in (512, 1024, 2048):
         n = total // C
         seq = synth.make_sweep_sequence(replace(base, chunk_len=C), n_chunks=n)
-        kd, vd = bf(seq.k_pool), bf(seq.v_pool)
+        kd, vd = bf(seq.k_pool), bf(synth.v_pages_transposed(seq.v_pool))
         k_mean = torch.zeros((1, base.num_kv_heads, base.max_kv_blocks, base.head_dim),
                              dtype=torch.float32, device=dev)
         cb = C // base.page_size
@@ -489,7 +489,7 @@ def main():
     d = synth.make_inputs(w)
     dev = "cuda"
     bf = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
-    q, kp, vp = bf(d["q"]), bf(d["k_pool"]), bf(d["v_pool"])
+    q, kp, vp = bf(d["q"]), bf(d["k_pool"]), bf(synth.v_pages_transposed(d["v_pool"]))
     pt = torch.from_numpy(d["page_table"]).to(dev)
     p = ca.Problem.from_workload(w, device=dev)
     gs = w.group_size

@@ -26,9 +26,13 @@
  *   row-major (C order) with the shapes given below.
  * - KV cache: KV-head-major pages (Sec. 3.3, Fig. 4).  Logical block j of
  *   (sequence b, KV head kvh) is physical page page_table[b, kvh, j] of
- *   k_pool / v_pool, each [P, page_size, head_dim]; one page id addresses the
- *   K page and the V page.  page_table is int32 [B, Hkv, max_kv_blocks];
- *   entries at j >= nKB_b are ignored.
+ *   k_pool and v_pool; one page id addresses the K page and the V page.
+ *   k_pool is [P, page_size, head_dim] (token-major pages, as the paper's
+ *   cache).  v_pool is [P, head_dim, page_size]: every V page is stored
+ *   transposed, dimension-major with the page's tokens contiguous (the
+ *   layout of vLLM's original paged V cache), so that the attention kernel
+ *   reads each V^T operand fragment with one 16-byte LDS read.  page_table
+ *   is int32 [B, Hkv, max_kv_blocks]; entries at j >= nKB_b are ignored.
  * - Per sequence b: cached_len[b] tokens are already in the cache and the
  *   chunk adds chunk_len tokens (any lengths).  Chunk token t sits at
  *   absolute position cached_len[b] + t, key r of block j at
@@ -36,11 +40,11 @@
  *   full of cached tokens (the candidates of the selector); the sequence
  *   occupies nKB_b = ceil((cached_len[b] + chunk_len) / page_size) blocks.
  *   A block holding both cached and chunk tokens counts as a chunk block.
- *   The rows of a sequence's last page past its end (cached_len[b] +
- *   chunk_len) are not part of it and may hold anything, NaN included:
- *   pooling does not read them and attention gives them no weight.  Every
- *   page of the pool is nevertheless read whole, so it must be allocated
- *   whole (page_size rows).
+ *   The tokens of a sequence's last page past its end (cached_len[b] +
+ *   chunk_len: K rows, V columns) are not part of it and may hold anything,
+ *   NaN included: pooling does not read them and attention gives them no
+ *   weight.  Every page of the pool is nevertheless read whole, so it must
+ *   be allocated whole (page_size tokens).
  * - Query head h belongs to KV head h / (Hq / Hkv) and to execution group
  *   h / group_size (contiguous heads, Sec. 3.2 and App. B.1: the KV group by
  *   default, or 4-head sub-groups of a larger KV group).  group_size must
@@ -69,7 +73,7 @@
 extern "C" {
 #endif
 
-#define CA_ABI_VERSION 3
+#define CA_ABI_VERSION 4
 
 typedef enum ca_status {
   CA_OK = 0,
@@ -302,8 +306,9 @@ ca_status ca_block_sparse_chunk_attention(const ca_problem* p, const uint16_t* q
  *    contiguous pools, then attention runs on them.
  *    ca_gather_selected_pages: packed page p (0 <= p < kv_indptr[B*G]) gets
  *    K_pool / V_pool page page_table[b, kvh, kv_indices[p]] of the row that
- *    owns entry p; k_packed and v_packed are bf16 [capacity_pages, page, D]
- *    and capacity_pages must be >= kv_indptr[B*G] (B*G*max_kv_blocks always
+ *    owns entry p; k_packed is bf16 [capacity_pages, page, D] and v_packed
+ *    [capacity_pages, D, page] (pages copied whole, in the pools' layouts);
+ *    capacity_pages must be >= kv_indptr[B*G] (B*G*max_kv_blocks always
  *    is; entries beyond the capacity are not copied).  Invalid entries
  *    (kv_indices outside [0, max_kv_blocks)) are skipped.
  *    ca_packed_chunk_attention: the section 3 result for the same tables,

@@ -376,7 +376,10 @@ def chunk_attention(p: Problem, q_chunk: torch.Tensor, kv_pool: Tuple[torch.Tens
                     group_size: int, sm_scale: float, num_splits: int = 0,
                     out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
                     ws: Optional[torch.Tensor] = None, stream=None):
-    """Attention of the chunk over its groups' tables; returns (out bf16, lse fp32 or None)."""
+    """Attention of the chunk over its groups' tables; returns (out bf16, lse fp32 or None).
+
+    ``kv_pool`` = (k_pool ``[P, page, D]``, v_pool ``[P, D, page]``: V pages
+    transposed, see ``synth.v_pages_transposed``)."""
     k_pool, v_pool = kv_pool
     if out is None:
         out = torch.empty_like(q_chunk)
@@ -458,9 +461,10 @@ def gather_selected_pages(p: Problem, kv_pool: Tuple[torch.Tensor, torch.Tensor]
     if capacity_pages is None:
         capacity_pages = p.batch * p.n_groups(group_size) * p.max_kv_blocks
     if out is None:
-        shape = (capacity_pages,) + tuple(k_pool.shape[1:])
-        out = (torch.empty(shape, dtype=k_pool.dtype, device=k_pool.device),
-               torch.empty(shape, dtype=v_pool.dtype, device=v_pool.device))
+        out = (torch.empty((capacity_pages,) + tuple(k_pool.shape[1:]), dtype=k_pool.dtype,
+                           device=k_pool.device),
+               torch.empty((capacity_pages,) + tuple(v_pool.shape[1:]), dtype=v_pool.dtype,
+                           device=v_pool.device))
     _check(load().ca_gather_selected_pages(p.ref, _ptr(k_pool), _ptr(v_pool), _ptr(page_table),
                                            _ptr(tables[0]), _ptr(tables[1]), group_size,
                                            _ptr(out[0]), _ptr(out[1]), capacity_pages,

@@ -13,8 +13,9 @@
 //     LDS traffic per flop of a 32-row wave;
 //   * S^T = K Q^T (keys x queries): every lane holds one query column, so
 //     the softmax statistics are in-lane plus one v_permlane32_swap; then
-//     O^T += V^T P^T with the V^T fragments read straight from the row-major
-//     V page by the gfx950 transpose read ds_read_b64_tr_b16;
+//     O^T += V^T P^T with each V^T fragment one 16-byte read: V pages are
+//     stored transposed (D rows x 64 keys) and the lanes read K rows in an
+//     order that gives every lane 8 consecutive keys of P^T;
 //   * pages go from HBM into LDS with 16-byte direct-to-LDS buffer loads (no
 //     register round trip) into XOR-swizzled tiles (conflict-free operand
 //     reads);
@@ -71,22 +72,25 @@ constexpr int kXcds = 8;   // MI355X: 8 accelerator complex dies, 32 CUs and one
 
 // Swizzled position (16-byte chunk) of chunk c of row r in an LDS page tile.
 // gfx950 LDS has 64 banks of 4 bytes; a 16-byte read is served 16 lanes per
-// cycle and an 8-byte read 32 lanes per cycle.
-// K is read 16 bytes per lane by 16 consecutive rows at one chunk: the 16
-// rows must land on 16 different 16-byte bank slots of the 256-byte bank
-// window (a D = 64 row is half a window, so rows pair up).
-// V is read 8 bytes per lane by the transpose read, 32 lanes covering 4
-// consecutive rows x 4 chunks: each row's aligned group of 4 chunks must
-// move to a different aligned group of the window.
-// Both swizzles leave a row's pattern unchanged under +8 and +16 rows, so
-// the operand reads of one lane differ only by immediate offsets.
+// cycle, so the 16 rows that a read touches at one chunk must land on 16
+// different 16-byte bank slots of the 256-byte bank window.
+// K tiles are 64 key rows x D (a D = 64 row is half a window, so rows pair
+// up); V^T tiles are D rows x 64 keys (128 bytes, two rows per window).
+// Both swizzles leave a row's pattern unchanged under +32 rows (and the K
+// one under +8 and +16), so the operand reads of one lane differ only by
+// immediate offsets.
 template <int D>
 __device__ __forceinline__ int k_swz(int r, int c) {
   return D == 128 ? (c ^ (r & 15)) : (c ^ ((r >> 1) & 7));
 }
-template <int D>
-__device__ __forceinline__ int v_swz(int r, int c) {
-  return D == 128 ? (c ^ ((r & 3) << 2)) : (c ^ (((r >> 1) & 1) << 2));
+__device__ __forceinline__ int vt_swz(int r, int c) { return c ^ ((r >> 1) & 7); }
+
+// Key row that lane column `col` reads from a K tile: bits 2 and 3 of the
+// key index swapped.  With it the S^T accumulator rows that one lane packs
+// into a P^T fragment are 8 consecutive keys, so the matching V^T fragment
+// is one contiguous 16-byte read of a V^T row.
+__device__ __forceinline__ int key_of_row(int r) {
+  return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);
 }
 
 // 2^x with a single v_exp_f32 (results below the normal range flush to 0,
@@ -94,8 +98,6 @@ __device__ __forceinline__ int v_swz(int r, int c) {
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 typedef __attribute__((address_space(3))) void lds_void;
-typedef short i16x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 // Raw buffer resource of one page (64 rows x D bf16).  The page copies use
 // buffer loads to LDS rather than global_load_lds: while a global_load_lds is
@@ -108,23 +110,29 @@ constexpr int kRawBufferWord3 = 0x00020000;   // gfx9 raw buffer, 32-bit data fo
   __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(page), 0, kPage * (D) * 2,      \
                                     kRawBufferWord3)
 
-// Copy one page (64 rows x D bf16, contiguous in HBM) into an LDS tile with
-// direct-to-LDS loads.  Each wave instruction fills 1 KB of the tile, lane l
-// writing bytes [16l, 16l+16); the lane's source is the chunk that the
-// swizzle maps there (the swizzles are involutions).  NW waves share a page.
+// Copy one page (16 KB at D = 128, contiguous in HBM: a K page is 64 rows
+// x D, a V page D rows x 64 keys) into an LDS tile with direct-to-LDS loads.
+// Each wave instruction fills 1 KB of the tile, lane l writing bytes
+// [16l, 16l+16); the lane's source is the chunk that the swizzle maps there
+// (the swizzles are involutions).  NW waves share a page.
+template <int D, bool IS_V>
+__device__ __forceinline__ uint32_t copy_src_offset(int inst, int lane) {
+  constexpr int RL = IS_V ? kPage : D;   // elements per row
+  constexpr int CPR = RL / 8;            // 16-byte chunks per row
+  constexpr int ROWS_PER_INST = 64 / CPR;
+  const int r = inst * ROWS_PER_INST + lane / CPR;
+  const int cpos = lane % CPR;
+  const int c = IS_V ? vt_swz(r, cpos) : k_swz<D>(r, cpos);
+  return (uint32_t)(r * RL + c * 8);   // unsigned: scalar base + 32-bit offset
+}
 template <int D, int NW, bool IS_V>
 __device__ __forceinline__ void page_to_lds(const uint16_t* __restrict__ src, uint16_t* tile,
                                             int wv, int lane) {
-  constexpr int CPR = D / 8;                               // 16-byte chunks per row
-  constexpr int ROWS_PER_INST = 64 / CPR;                  // rows per 1 KB instruction
   constexpr int INST_PER_WAVE = (64 * D * 2) / 1024 / NW;
 #pragma unroll
   for (int m = 0; m < INST_PER_WAVE; ++m) {
     const int inst = wv * INST_PER_WAVE + m;
-    const int r = inst * ROWS_PER_INST + lane / CPR;
-    const int cpos = lane % CPR;
-    const int c = IS_V ? v_swz<D>(r, cpos) : k_swz<D>(r, cpos);
-    const uint32_t off = (uint32_t)(r * D + c * 8);   // unsigned: scalar base + 32-bit offset
+    const uint32_t off = copy_src_offset<D, IS_V>(inst, lane);
     __builtin_amdgcn_raw_ptr_buffer_load_lds(CA_PAGE_RSRC(src, D), (lds_void*)(tile + inst * 512),
                                              16, 2 * off, 0, 0, 0);
   }
@@ -135,14 +143,9 @@ __device__ __forceinline__ void page_to_lds(const uint16_t* __restrict__ src, ui
 template <int D, int NW, bool IS_V>
 __device__ __forceinline__ void page_part_to_lds(const uint16_t* __restrict__ src, uint16_t* tile,
                                                  int wv, int lane, int m) {
-  constexpr int CPR = D / 8;
-  constexpr int ROWS_PER_INST = 64 / CPR;
   constexpr int INST_PER_WAVE = (64 * D * 2) / 1024 / NW;
   const int inst = wv * INST_PER_WAVE + m;
-  const int r = inst * ROWS_PER_INST + lane / CPR;
-  const int cpos = lane % CPR;
-  const int c = IS_V ? v_swz<D>(r, cpos) : k_swz<D>(r, cpos);
-  const uint32_t off = (uint32_t)(r * D + c * 8);
+  const uint32_t off = copy_src_offset<D, IS_V>(inst, lane);
   __builtin_amdgcn_raw_ptr_buffer_load_lds(CA_PAGE_RSRC(src, D), (lds_void*)(tile + inst * 512),
                                            16, 2 * off, 0, 0, 0);
 }
@@ -184,8 +187,9 @@ __device__ __forceinline__ float halves_sum(float x) {
 }
 
 // S^T tiles of one page for the wave's two column tiles: s[c][h] holds keys
-// 32h .. 32h+31 of column tile c; key of accumulator slot v (lane half hf):
-// 32h + 8*(v/4) + 4*hf + v%4.
+// 32h .. 32h+31 of column tile c; accumulator slot v of lane half hf is row
+// 8*(v/4) + 4*hf + v%4 of the tile, i.e. key
+// 32h + 16*(v/8) + 8*hf + 4*((v/4)%2) + v%4 (key_of_row).
 struct SPage {
   f32x16 s[2][2];
 };
@@ -245,6 +249,22 @@ template <typename T>
 __device__ __forceinline__ void pin(const T& v) {
   asm volatile("" : : "v"(v));
 }
+
+// Softmax schedule of one page: 66 element ops (op j: score of element j,
+// exp of element j-1, sum of element j-2, for the 64 weights a lane holds)
+// and 8 packs, the pack of unit u (elements 8u .. 8u+7) right after element
+// op 8u+8.  soft_op(o) is j for an element op, -1-u for a pack.
+constexpr int kSoftOps = 74;
+constexpr int soft_op(int o) {
+  int op = 0;
+  for (int j = 0; j <= 65; ++j) {
+    if (op++ == o) return j;
+    if (j >= 8 && j <= 64 && (j - 8) % 8 == 0 && op++ == o) return -1 - (j - 8) / 8;
+  }
+  return 1 << 20;
+}
+static_assert(soft_op(kSoftOps - 1) == 65 && soft_op(9) == -1 && soft_op(kSoftOps - 2) == -8,
+              "softmax op table");
 
 // Calls f(integral_constant<int, I>) for I = 0 .. N-1 (compile-time indices).
 template <typename F, int... I>
@@ -455,33 +475,26 @@ __global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnA
   };
 
   // Per-lane byte offsets of the MFMA operand reads inside a page tile; the
-  // buffer, the 16-key block of a PV step and the upper 32 keys of a QK step
-  // are immediates.
-  uint32_t kofs[NKS], vofs[NDT];
+  // buffer, the d tile of a PV step and the upper 32 keys of a QK step are
+  // immediates.  Lane column col reads key row key_of_row(col) of K, so its
+  // P^T fragment kk holds keys 16kk + 8*half .. +7, read from V^T row
+  // 32x + col as one 16-byte chunk.
+  uint32_t kofs[NKS], vofs[4];
 #pragma unroll
-  for (int x = 0; x < NKS; ++x)
-    kofs[x] = (uint32_t)(col * D * 2 + 16 * k_swz<D>(col, 2 * x + half));
-  {
-    const int grp = lane >> 4, sl = lane & 15;
-    const int m = sl >> 2, q = sl & 3;
-    const int r0 = 4 * (grp >> 1) + m;
-#pragma unroll
-    for (int x = 0; x < NDT; ++x) {
-      const int d = 32 * x + 16 * (grp & 1) + 4 * q;
-      vofs[x] = (uint32_t)(r0 * D * 2 + 16 * v_swz<D>(r0, d >> 3) + 2 * (d & 7));
-    }
+  for (int x = 0; x < NKS; ++x) {
+    const int kr = key_of_row(col);
+    kofs[x] = (uint32_t)(kr * D * 2 + 16 * k_swz<D>(kr, 2 * x + half));
   }
-  // fragment F of a step: F < NPV is V^T fragment (kk = F / NDT, x = F % NDT),
-  // otherwise K fragment (k-step (F - NPV) / 2, keys 32 * ((F - NPV) % 2) ..)
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) vofs[kk] = (uint32_t)(col * kPage * 2 + 16 * vt_swz(col, 2 * kk + half));
+  // fragment F of a step: F < NPV is V^T fragment (kk = F / NDT, d tile
+  // x = F % NDT), otherwise K fragment (k-step (F - NPV) / 2, keys
+  // 32 * ((F - NPV) % 2) ..)
   auto load_frag = [&](int F, const uint16_t* vt, const uint16_t* kt) -> bf16x8 {
     if (F < NPV) {
       const int kk = F / NDT, x = F % NDT;
-      const char* p = reinterpret_cast<const char*>(vt) + vofs[x] + 16 * kk * D * 2;
-      const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p);
-      const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 8 * D * 2));
-      const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
-      const u32x4 w = {l2[0], l2[1], h2[0], h2[1]};
-      return __builtin_bit_cast(bf16x8, w);
+      const char* p = reinterpret_cast<const char*>(vt) + vofs[kk] + 32 * kPage * 2 * x;
+      return *reinterpret_cast<const bf16x8*>(p);
     }
     const int G2 = F - NPV;
     const char* p = reinterpret_cast<const char*>(kt) + kofs[G2 / 2] + (G2 % 2) * 32 * D * 2;
@@ -546,7 +559,8 @@ __global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnA
     // No hazard fence here: the last MFMA writing S (slot 62 or 63) and the
     // last pack writing P come at least ~25 instructions (end of step, barrier,
     // page pointers) before their first readers in this step (slot 0 and later).
-    float mx[2] = {-INFINITY, -INFINITY}, alpha[2] = {1.f, 1.f}, nmb[2] = {0.f, 0.f};
+    float mx[2][2] = {{-INFINITY, -INFINITY}, {-INFINITY, -INFINITY}};
+    float alpha[2] = {1.f, 1.f}, nmb[2] = {0.f, 0.f};
     float ps[2] = {0.f, 0.f};
     bool rb_any = false;
     bf16x8 fr[NFRAG];
@@ -576,13 +590,17 @@ __global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnA
       }
       // softmax work of this slot
       if constexpr (s < 8) {
+        // two independent max chains per column tile (half the dependent latency)
         constexpr int cc = s / 4, k0 = 4 * (s % 4);
-#pragma unroll
-        for (int k = k0; k < k0 + 4; ++k) mx[cc] = max3(mx[cc], sc.s[cc][0][k], sc.s[cc][1][k]);
-        pin(mx[cc]);
+        mx[cc][0] = max3(mx[cc][0], sc.s[cc][0][k0], sc.s[cc][1][k0]);
+        mx[cc][1] = max3(mx[cc][1], sc.s[cc][0][k0 + 1], sc.s[cc][1][k0 + 1]);
+        mx[cc][0] = max3(mx[cc][0], sc.s[cc][0][k0 + 2], sc.s[cc][1][k0 + 2]);
+        mx[cc][1] = max3(mx[cc][1], sc.s[cc][0][k0 + 3], sc.s[cc][1][k0 + 3]);
+        pin(mx[cc][0]);
+        pin(mx[cc][1]);
       } else if constexpr (s < MAXS) {
         constexpr int cc = s - 8;
-        const float m = halves_max(mx[cc]) * a.scale_log2;
+        const float m = halves_max(fmaxf(mx[cc][0], mx[cc][1])) * a.scale_log2;
         const bool rebase = m > m_run[cc] + kRescaleSlack;
         alpha[cc] = rebase ? fast_exp2(m_run[cc] - m) : 1.0f;
         m_run[cc] = rebase ? m : m_run[cc];
@@ -591,20 +609,36 @@ __global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnA
         pin(nmb[cc]);
         pin(alpha[cc]);
       } else {
-        constexpr int NOPS = 72;
-        constexpr int lo = ((s - MAXS) * NOPS) / (NSLOT - MAXS);
-        constexpr int hi = ((s - MAXS + 1) * NOPS) / (NSLOT - MAXS);
+        // Weights of the page, software-pipelined over the remaining slots so
+        // that no instruction waits on the one before it: element op j does
+        // the scaled score of element j, the exp of element j-1 and the row
+        // sum of element j-2 (elements in unit order, unit u = 8 weights of
+        // one P^T fragment); unit u is packed to bf16 after element op 8u+8.
+        constexpr int lo = ((s - MAXS) * kSoftOps) / (NSLOT - MAXS);
+        constexpr int hi = ((s - MAXS + 1) * kSoftOps) / (NSLOT - MAXS);
         static_for<hi - lo>([&](auto otag) __attribute__((always_inline)) {
-          constexpr int op = lo + decltype(otag)::value;
-          constexpr int u = op / 9, k = op % 9, cc = u / 4, kk = u % 4;
-          f32x16& sv = sc.s[cc][kk / 2];
-          if constexpr (k < 8) {
-            constexpr int v = 8 * (kk % 2) + k;
-            const float e = fast_exp2(fmaf(sv[v], a.scale_log2, nmb[cc]));
-            sv[v] = e;
-            ps[cc] += e;
-            pin(ps[cc]);
+          constexpr int op = soft_op(lo + decltype(otag)::value);
+          if constexpr (op >= 0) {
+            if constexpr (op < 64) {
+              constexpr int u = op / 8, cc = u / 4, kk = u % 4, v = 8 * (kk % 2) + op % 8;
+              f32x16& sv = sc.s[cc][kk / 2];
+              sv[v] = fmaf(sv[v], a.scale_log2, nmb[cc]);
+              pin(sv[v]);
+            }
+            if constexpr (op >= 1 && op <= 64) {
+              constexpr int e = op - 1, u = e / 8, cc = u / 4, kk = u % 4, v = 8 * (kk % 2) + e % 8;
+              f32x16& sv = sc.s[cc][kk / 2];
+              sv[v] = fast_exp2(sv[v]);
+              pin(sv[v]);
+            }
+            if constexpr (op >= 2) {
+              constexpr int e = op - 2, u = e / 8, cc = u / 4, kk = u % 4, v = 8 * (kk % 2) + e % 8;
+              ps[cc] += sc.s[cc][kk / 2][v];
+              pin(ps[cc]);
+            }
           } else {
+            constexpr int u = -1 - op, cc = u / 4, kk = u % 4;
+            const f32x16& sv = sc.s[cc][kk / 2];
 #pragma unroll
             for (int x = 0; x < 8; ++x) pn.p[cc][kk][x] = (__bf16)sv[8 * (kk % 2) + x];
             pin(pn.p[cc][kk]);
@@ -652,13 +686,16 @@ __global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnA
     copies_landed(k_s0, v_s0);
     __syncthreads();
     if (i >= n_main) {
-      // The rows of a sequence's last page past its end are not part of it
-      // and may hold anything: their weights are exactly 0, so their V rows
-      // are zeroed to keep 0 * NaN out of O (their K scores are masked).
+      // The tokens of a sequence's last page past its end are not part of it
+      // and may hold anything: their weights are exactly 0, so their V
+      // entries (the last `past` keys of every V^T row) are zeroed to keep
+      // 0 * NaN out of O (their K scores are masked).
       const int past = kPage * id_of(blk_cur, blk_nxt, i) + kPage - (cl + a.C);
       if (past > 0) {
-        uint4* vz = reinterpret_cast<uint4*>(v_s0 + (kPage - past) * D);
-        for (int x = t; x < past * D / 8; x += 64 * NW) vz[x] = make_uint4(0u, 0u, 0u, 0u);
+        for (int x = t; x < past * D; x += 64 * NW) {
+          const int r = x / past, key = kPage - past + x % past;
+          v_s0[r * kPage + 8 * vt_swz(r, key >> 3) + (key & 7)] = 0;
+        }
         __syncthreads();
       }
     }
@@ -668,10 +705,10 @@ __global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnA
       const int j = id_of(blk_cur, blk_nxt, i);
 #pragma unroll
       for (int c = 0; c < 2; ++c) {
-        const int lim = qpos[c] - kPage * j - 4 * half;
+        const int lim = qpos[c] - kPage * j - 8 * half;
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          const int kp = 8 * (v >> 2) + (v & 3);
+          const int kp = 16 * (v >> 3) + 4 * ((v >> 2) & 1) + (v & 3);   // key - 8*half
           if (kp > lim) SA.s[c][0][v] = -INFINITY;
           if (kp + 32 > lim) SA.s[c][1][v] = -INFINITY;
         }

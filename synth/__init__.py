@@ -12,7 +12,8 @@ unions, no attention).  Everything it returns is a plain NumPy array:
   ``page_table[b, kvh, j]`` of ``k_pool`` / ``v_pool`` (``[P, page, D]``),
   which is the layout of the paper's zero-copy execution (Sec. 3.3, Fig. 4
   and App. B.2: one contiguous ``[block, D]`` region per
-  (batch, KV head, block) triple);
+  (batch, KV head, block) triple); the GPU library takes V pages
+  transposed (``v_pages_transposed``: ``[P, D, page]``);
 * physical page ids are a seeded permutation of all (b, kvh, j) triples, so
   the pool holds exactly the pages the workload needs.
 
@@ -30,4 +31,5 @@ from .gen import (  # noqa: F401
     random_masks,
     random_tables,
     tied_scores,
+    v_pages_transposed,
 )

@@ -200,6 +200,16 @@ def _apply_needle(kb: np.ndarray, j: int, u: np.ndarray, beta: float) -> None:
 BF16_QNAN = np.uint16(0x7FC0)
 
 
+def v_pages_transposed(v_pool: np.ndarray) -> np.ndarray:
+    """The V pool in the GPU library's page layout: every page transposed to
+    ``[D, page]`` (head dimension major, tokens contiguous), the same values.
+
+    The seeded V data and the oracle use token-major pages ``[page, D]``;
+    the attention kernel reads V^T pages (one 16-byte LDS read per operand
+    fragment), so GPU callers hand over this copy."""
+    return np.ascontiguousarray(v_pool.transpose(0, 2, 1))
+
+
 def poison_past_end(w: Workload, k_pool: np.ndarray, v_pool: np.ndarray,
                     pt: np.ndarray) -> None:
     """NaN in every K and V row of a sequence's last page past its end.

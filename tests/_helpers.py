@@ -3,6 +3,7 @@ import numpy as np
 import torch
 
 import oracle
+import synth
 
 # Tolerances on bf16 attention outputs against the fp64 oracle.
 MAX_ABS = 2e-2      # per element
@@ -34,7 +35,8 @@ def bf16_host_f64(t: torch.Tensor) -> np.ndarray:
 
 
 def device_inputs(d: dict) -> dict:
-    return dict(q=bf16_dev(d["q"]), k=bf16_dev(d["k_pool"]), v=bf16_dev(d["v_pool"]),
+    return dict(q=bf16_dev(d["q"]), k=bf16_dev(d["k_pool"]),
+                v=bf16_dev(synth.v_pages_transposed(d["v_pool"])),
                 pt=i32_dev(d["page_table"]))
 
 

@@ -71,7 +71,7 @@ def test_copy_arm_gather_and_bitexact(name, workload_inputs, oracle_estimate):
     vh = vp[torch.as_tensor(pick, device="cuda")].view(torch.int16).cpu().numpy()
     # bit patterns (NaN rows past a sequence end are copied as they are)
     assert np.array_equal(kh.view(np.uint16), d["k_pool"][src[pick]])
-    assert np.array_equal(vh.view(np.uint16), d["v_pool"][src[pick]])
+    assert np.array_equal(vh.view(np.uint16), synth.v_pages_transposed(d["v_pool"][src[pick]]))
     for splits in (1, 0):
         lse_z = torch.empty((p.batch, p.num_q_heads, p.chunk_len), dtype=torch.float32,
                             device="cuda")

@@ -607,7 +607,7 @@ def test_sweep_all_chunks():
     page = base.page_size
     full_nkb = seq.page_table_full.shape[2]
     km_all = oracle.k_block_means(seq.k_pool, seq.page_table_full, [full_nkb])
-    k_dev, v_dev = bf16_dev(seq.k_pool), bf16_dev(seq.v_pool)
+    k_dev, v_dev = bf16_dev(seq.k_pool), bf16_dev(synth.v_pages_transposed(seq.v_pool))
     k_mean = torch.zeros((1, base.num_kv_heads, base.max_kv_blocks, base.head_dim),
                          dtype=torch.float32, device="cuda")
     attn_chunks = {0, 1, 31, 62, 63}

@@ -137,3 +137,18 @@ def test_unaligned_workload_shapes_and_poisoned_tails(workload_inputs):
                 assert np.isfinite(last[:valid]).all() and np.isnan(last[valid:]).all()
                 before = synth.bf16_bits_to_f32(pool[d["page_table"][b, kvh, :n - 1]])
                 assert np.isfinite(before).all()
+
+
+def test_v_pages_transposed_layout(workload_inputs):
+    """The GPU copy of the V pool holds page p's token t, dimension c at
+    [p, c, t]: the same bits, every page transposed."""
+    d = workload_inputs("tiny_unaligned")
+    v = d["v_pool"]
+    vt = synth.v_pages_transposed(v)
+    P, page, D = v.shape
+    assert vt.shape == (P, D, page) and vt.dtype == v.dtype and vt.flags.c_contiguous
+    rng = np.random.default_rng(5)
+    for _ in range(200):
+        p, t, c = rng.integers(P), rng.integers(page), rng.integers(D)
+        assert vt[p, c, t] == v[p, t, c]
+    assert np.array_equal(synth.v_pages_transposed(vt), v)
