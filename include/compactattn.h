@@ -23,7 +23,11 @@
  *   caller allocates and owns every buffer; the library allocates nothing
  *   and keeps no state besides a thread-local error string.
  * - bf16 tensors are passed as uint16_t bit patterns.  All tensors are dense
- *   row-major (C order) with the shapes given below.
+ *   row-major (C order) with the shapes given below.  The bf16 and fp32
+ *   tensors (q, k_pool, v_pool, out, q_mean, k_mean, scores, packed pools)
+ *   must start on a 16-byte boundary (CA_ERR_UNALIGNED otherwise; any
+ *   hipMalloc or torch allocation does), and so must the attention
+ *   workspace (CA_ERR_WORKSPACE).
  * - KV cache: KV-head-major pages (Sec. 3.3, Fig. 4).  Logical block j of
  *   (sequence b, KV head kvh) is physical page page_table[b, kvh, j] of
  *   k_pool and v_pool; one page id addresses the K page and the V page.
@@ -79,7 +83,7 @@ typedef enum ca_status {
   CA_OK = 0,
   CA_ERR_NULL = 1,          /* a required pointer is NULL                       */
   CA_ERR_SHAPE = 2,         /* a size is out of range or inconsistent           */
-  CA_ERR_UNALIGNED = 3,     /* no longer returned: any lengths are accepted     */
+  CA_ERR_UNALIGNED = 3,     /* a tensor pointer is not 16-byte aligned          */
   CA_ERR_GROUP = 4,         /* group_size does not divide Hq / Hkv              */
   CA_ERR_WORKSPACE = 5,     /* workspace missing or too small                   */
   CA_ERR_UNSUPPORTED = 6,   /* head_dim / page_size / q_block not built for     */

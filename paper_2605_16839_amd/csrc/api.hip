@@ -137,6 +137,16 @@ bool xcd_balance_ok(const ca::Dims& d, const ca_problem* p, int group_size, int 
   return true;
 }
 
+// The kernels read and write the bf16 and fp32 tensors with 16-byte vector
+// accesses, so each must start on a 16-byte boundary (every hipMalloc or torch
+// allocation does; a view that starts mid-row may not).  NULL passes here: the
+// NULL checks report it.
+template <typename... T>
+ca_status need_aligned16(const char* names, const T*... ptrs) {
+  const bool ok = ((reinterpret_cast<uintptr_t>(ptrs) % 16 == 0) && ...);
+  return ok ? CA_OK : fail(CA_ERR_UNALIGNED, "%s must be 16-byte aligned", names);
+}
+
 ca_status run_attention(const ca_problem* p, const uint16_t* q, const uint16_t* k_pool,
                         const uint16_t* v_pool, const int32_t* page_table,
                         const int32_t* kv_indptr, const int32_t* kv_indices, int32_t group_size,
@@ -149,6 +159,7 @@ ca_status run_attention(const ca_problem* p, const uint16_t* q, const uint16_t* 
   if ((s = need_device(p)) != CA_OK) return s;
   if (!q || !k_pool || !v_pool || !out || (!page_table && table_mode != ca::kTablesPacked))
     return fail(CA_ERR_NULL, "q, k_pool, v_pool, page_table and out are required");
+  if ((s = need_aligned16("q, k_pool, v_pool and out", q, k_pool, v_pool, out)) != CA_OK) return s;
   if (table_mode == ca::kTablesPerQTile &&
       ca::attn_query_tile(group_size, table_mode) != d.q_block)
     return fail(CA_ERR_UNSUPPORTED,
@@ -173,6 +184,8 @@ ca_status run_attention(const ca_problem* p, const uint16_t* q, const uint16_t* 
     if (ws == nullptr || ws_bytes < need)
       return fail(CA_ERR_WORKSPACE, "attention with %d splits needs %zu workspace bytes, got %zu",
                   splits, need, ws == nullptr ? (size_t)0 : ws_bytes);
+    if (reinterpret_cast<uintptr_t>(ws) % 16 != 0)
+      return fail(CA_ERR_WORKSPACE, "workspace must be 16-byte aligned");
   }
   ca::AttnLaunch L;
   L.q = q;
@@ -228,6 +241,7 @@ ca_status ca_pool_q_blocks(const ca_problem* p, const uint16_t* q, float* q_mean
   ca_status s = check(p, 0, &d);
   if (s != CA_OK) return s;
   if (!q || !q_mean) return fail(CA_ERR_NULL, "q and q_mean are required");
+  if ((s = need_aligned16("q and q_mean", q, q_mean)) != CA_OK) return s;
   return hip_status(ca::launch_pool_q(d, q, q_mean, static_cast<hipStream_t>(stream)),
                     "pool_q launch");
 }
@@ -241,6 +255,7 @@ ca_status ca_pool_k_blocks(const ca_problem* p, const uint16_t* k_pool,
   if ((s = need_device(p)) != CA_OK) return s;
   if (!k_pool || !page_table || !k_mean)
     return fail(CA_ERR_NULL, "k_pool, page_table and k_mean are required");
+  if ((s = need_aligned16("k_pool and k_mean", k_pool, k_mean)) != CA_OK) return s;
   if (first_block < 0) return fail(CA_ERR_SHAPE, "first_block must be >= 0");
   return hip_status(ca::launch_pool_k(d, k_pool, page_table, p->cached_len, first_block,
                                       k_mean, static_cast<hipStream_t>(stream)),
@@ -255,6 +270,7 @@ ca_status ca_block_scores(const ca_problem* p, const float* q_mean, const float*
   if ((s = need_device(p)) != CA_OK) return s;
   if (!q_mean || !k_mean || !scores)
     return fail(CA_ERR_NULL, "q_mean, k_mean and scores are required");
+  if ((s = need_aligned16("q_mean, k_mean and scores", q_mean, k_mean, scores)) != CA_OK) return s;
   return hip_status(ca::launch_scores(d, q_mean, k_mean, p->cached_len, scores,
                                       static_cast<hipStream_t>(stream)),
                     "scores launch");
@@ -299,7 +315,10 @@ ca_status ca_estimate_masks(const ca_problem* p, const uint16_t* q, const uint16
   if (sink_blocks < 0 || local_blocks < 0)
     return fail(CA_ERR_SHAPE, "sink_blocks and local_blocks must be >= 0");
   if (!masks) return fail(CA_ERR_NULL, "masks is required");
-  ca_status s = ca_pool_q_blocks(p, q, q_mean, stream);
+  ca_status s = need_aligned16("q, k_pool, q_mean, k_mean and scores", q, k_pool, q_mean, k_mean,
+                               scores);
+  if (s != CA_OK) return s;
+  s = ca_pool_q_blocks(p, q, q_mean, stream);
   if (s != CA_OK) return s;
   if ((s = ca_pool_k_blocks(p, k_pool, page_table, k_mean_first_block, k_mean, stream)) != CA_OK)
     return s;
@@ -322,6 +341,9 @@ ca_status ca_estimate_tables(const ca_problem* p, const uint16_t* q, const uint1
     return fail(CA_ERR_NULL,
                 "q, k_pool, page_table, q_mean, k_mean, scores, kv_indptr and kv_indices are "
                 "required");
+  if ((s = need_aligned16("q, k_pool, q_mean, k_mean and scores", q, k_pool, q_mean, k_mean,
+                          scores)) != CA_OK)
+    return s;
   if (!(top_frac >= 0.f && top_frac <= 1.f))
     return fail(CA_ERR_SHAPE, "top_frac must be in [0, 1]");
   if (sink_blocks < 0 || local_blocks < 0)
@@ -387,6 +409,9 @@ ca_status ca_estimate_masks_threshold(const ca_problem* p, const uint16_t* q,
   ca_status s = check_threshold(alpha, temperature, sm_scale, sink_blocks, local_blocks);
   if (s != CA_OK) return s;
   if (!masks) return fail(CA_ERR_NULL, "masks is required");
+  if ((s = need_aligned16("q, k_pool, q_mean, k_mean and scores", q, k_pool, q_mean, k_mean,
+                          scores)) != CA_OK)
+    return s;
   s = ca_pool_q_blocks(p, q, q_mean, stream);
   if (s != CA_OK) return s;
   if ((s = ca_pool_k_blocks(p, k_pool, page_table, k_mean_first_block, k_mean, stream)) != CA_OK)
@@ -521,6 +546,9 @@ ca_status ca_gather_selected_pages(const ca_problem* p, const uint16_t* k_pool,
   if (s != CA_OK) return s;
   if (!k_pool || !v_pool || !page_table || !kv_indptr || !kv_indices || !k_packed || !v_packed)
     return fail(CA_ERR_NULL, "pools, page_table, tables and packed pools are required");
+  if ((s = need_aligned16("k_pool, v_pool, k_packed and v_packed", k_pool, v_pool, k_packed,
+                          v_packed)) != CA_OK)
+    return s;
   const long long cap_max = (long long)d.B * (d.Hq / group_size) * d.max_kv_blocks;
   if (capacity_pages < 1 || capacity_pages > cap_max)
     return fail(CA_ERR_SHAPE, "capacity_pages %lld out of range [1, %lld]",

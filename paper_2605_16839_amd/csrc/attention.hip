@@ -884,8 +884,16 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
       const float wgt = expf(li - mx);
       wsum += wgt;
       const float* po = part_o + ((size_t)i * nrows + row) * D + sub * PER;
+      float v[PER];
+      if constexpr (PER == 4) {
+        const float4 f = *reinterpret_cast<const float4*>(po);
+        v[0] = f.x, v[1] = f.y, v[2] = f.z, v[3] = f.w;
+      } else {
+        const float2 f = *reinterpret_cast<const float2*>(po);
+        v[0] = f.x, v[1] = f.y;
+      }
 #pragma unroll
-      for (int x = 0; x < PER; ++x) acc[x] = fmaf(wgt, po[x], acc[x]);
+      for (int x = 0; x < PER; ++x) acc[x] = fmaf(wgt, v[x], acc[x]);
     }
   }
   const float inv = wsum > 0.f ? 1.0f / wsum : 0.f;
@@ -894,8 +902,11 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
   const int h = (int)((row / C) % Hq);
   const int b = (int)(row / ((size_t)C * Hq));
   uint16_t* orow = out + (((size_t)b * C + tq) * Hq + h) * D + sub * PER;
+  uint32_t pk[PER / 2];
 #pragma unroll
-  for (int x = 0; x < PER; ++x) orow[x] = float_to_bf16_bits(acc[x] * inv);
+  for (int x = 0; x < PER / 2; ++x) pk[x] = pack_bf16x2(acc[2 * x] * inv, acc[2 * x + 1] * inv);
+  if constexpr (PER == 4) *reinterpret_cast<uint2*>(orow) = make_uint2(pk[0], pk[1]);
+  else *reinterpret_cast<uint32_t*>(orow) = pk[0];
   if (lse != nullptr && sub == 0) lse[row] = wsum > 0.f ? mx + logf(wsum) : -INFINITY;
 }
 

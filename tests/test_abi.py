@@ -177,3 +177,37 @@ def test_fused_tables_validation(lib):
     assert call(nbytes=8) == "CA_ERR_WORKSPACE"
     assert call(ws=ctypes.c_void_p(0x1004)) == "CA_ERR_WORKSPACE"
 
+
+
+def test_unaligned_tensors_rejected(lib):
+    """Every entry point rejects a bf16 / fp32 tensor that does not start on a
+    16-byte boundary, on the host, before anything is enqueued (fake device
+    pointers, never dereferenced)."""
+    fake = ctypes.c_void_p(0x1000)
+    odd = ctypes.c_void_p(0x1008)     # 8-byte aligned only
+    p = _prob()
+    p.c.cached_len = fake.value
+    st = lambda s: lib.ca_status_string(s).decode()
+    assert st(lib.ca_pool_q_blocks(p.ref, odd, fake, None)) == "CA_ERR_UNALIGNED"
+    assert st(lib.ca_pool_k_blocks(p.ref, fake, fake, 0, odd, None)) == "CA_ERR_UNALIGNED"
+    assert st(lib.ca_block_scores(p.ref, fake, fake, odd, None)) == "CA_ERR_UNALIGNED"
+    assert st(lib.ca_estimate_masks(p.ref, fake, odd, fake, 0.05, 1, 4, 0, fake, fake, fake,
+                                    fake, None)) == "CA_ERR_UNALIGNED"
+    assert st(lib.ca_estimate_masks_threshold(p.ref, fake, fake, fake, 0.9, 1.0, 0.1, 1, 4, 0,
+                                              odd, fake, fake, fake, None)) == "CA_ERR_UNALIGNED"
+    need = lib.ca_tables_workspace_bytes(p.ref, 4)
+    assert st(lib.ca_estimate_tables(p.ref, fake, fake, fake, 0.05, 1, 4, 0, 4, fake, fake, odd,
+                                     fake, fake, fake, need, None)) == "CA_ERR_UNALIGNED"
+    for args in ((odd, fake, fake, fake), (fake, odd, fake, fake), (fake, fake, odd, fake),
+                 (fake, fake, fake, odd)):
+        q, k, v, out = args
+        assert st(lib.ca_chunk_attention(p.ref, q, k, v, fake, fake, fake, 4, 0.1, 1, out, None,
+                                         None, 0, None)) == "CA_ERR_UNALIGNED"
+    assert st(lib.ca_dense_paged_chunk_attention(p.ref, fake, fake, odd, fake, 0.1, 1, fake, None,
+                                                 None, 0, None)) == "CA_ERR_UNALIGNED"
+    assert st(lib.ca_gather_selected_pages(p.ref, fake, fake, fake, fake, fake, 4, fake, odd, 10,
+                                           None)) == "CA_ERR_UNALIGNED"
+    # the split-KV workspace holds fp32 partial rows written 16 bytes at a time
+    ws = lib.ca_attention_workspace_bytes(p.ref, 4, 2)
+    assert st(lib.ca_chunk_attention(p.ref, fake, fake, fake, fake, fake, fake, 4, 0.1, 2, fake,
+                                     None, odd, ws, None)) == "CA_ERR_WORKSPACE"
