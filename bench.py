@@ -119,6 +119,30 @@ def selected_flops(w, ip: np.ndarray, ix: np.ndarray) -> float:
     return tot * 4 * w.head_dim
 
 
+def stage_bytes(w, ip: np.ndarray, ix: np.ndarray) -> dict:
+    """Algorithmic HBM bytes of each stage of one step (each byte once).
+
+    estimate: the cached K pages pooled (all of them: nothing is carried over
+    between chunks) and Q read, the fp32 block means and scores written and
+    read back, the mask words written; tables: the mask words read and the
+    CSR written; attention: every selected K and V page once per execution
+    group, Q read, O and lse written."""
+    D, page, B, Hq, Hkv, C = (w.head_dim, w.page_size, w.batch, w.num_q_heads, w.num_kv_heads,
+                              w.chunk_len)
+    nc = [w.n_cached_blocks(b) for b in range(B)]
+    q_bytes = B * C * Hq * D * 2
+    kmean = sum(nc) * Hkv * D * 4
+    qmean = B * Hq * w.n_qblocks * D * 4
+    scores = B * Hq * w.n_qblocks * max(nc + [1]) * 4
+    masks = B * Hq * w.n_qblocks * w.words * 8
+    nnz = int(ip[-1])
+    return {
+        "estimate": sum(nc) * Hkv * page * D * 2 + q_bytes + 2 * (kmean + qmean + scores) + masks,
+        "tables": masks + 4 * (len(ip) + nnz),
+        "attention": nnz * page * D * 2 * 2 + 2 * q_bytes + B * Hq * C * 4,
+    }
+
+
 def percentiles(v) -> dict:
     return {"median": round(float(np.median(v)), 4), "p10": round(float(np.percentile(v, 10)), 4),
             "p90": round(float(np.percentile(v, 90)), 4)}
@@ -650,6 +674,9 @@ def main():
                    "cached_tokens": list(w.cached_lens), "chunk_len": w.chunk_len,
                    "top_frac": w.top_frac, "rho": w.rho, "group_size": gs},
         "stage_ms": {k: round(v, 4) for k, v in st_ms.items()},
+        # algorithmic bytes / stage time (attention: the back-to-back launch time)
+        "stage_GBps": {k: round(v / ((attn_ms if k == "attention" else st_ms[k]) * 1e-3) / 1e9, 1)
+                       for k, v in stage_bytes(w, ip, ix).items()},
         "fused_step_ms": round(fused_ms, 4),
         "fused_estimate_tables_ms": round(fused_est_ms, 4),
         "dense_ms": round(dense_ms, 4),
