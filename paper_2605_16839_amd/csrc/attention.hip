@@ -866,32 +866,57 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
   const size_t nrows = (size_t)B * Hq * C;
   const size_t row = (size_t)blockIdx.x * 8 + (threadIdx.x >> 5);
   if (row >= nrows) return;
-  if (split_at != nullptr) {   // a table row that was not cut wrote its output already
-    const int hh = (int)((row / C) % Hq), bb = (int)(row / ((size_t)C * Hq));
-    if (split_at[bb * G + hh / group_size] < 0) return;
-  }
   const int sub = threadIdx.x & 31;
-  float mx = -INFINITY;
-  for (int i = 0; i < splits; ++i) mx = fmaxf(mx, part_lse[(size_t)i * nrows + row]);
+  auto load_part = [&](int i, float (&v)[PER]) {
+    const float* po = part_o + ((size_t)i * nrows + row) * D + sub * PER;
+    if constexpr (PER == 4) {
+      const float4 f = *reinterpret_cast<const float4*>(po);
+      v[0] = f.x, v[1] = f.y, v[2] = f.z, v[3] = f.w;
+    } else {
+      const float2 f = *reinterpret_cast<const float2*>(po);
+      v[0] = f.x, v[1] = f.y;
+    }
+  };
   float acc[PER];
 #pragma unroll
   for (int x = 0; x < PER; ++x) acc[x] = 0.f;
-  float wsum = 0.f;
-  if (mx != -INFINITY) {
+  float wsum = 0.f, mx = -INFINITY;
+  if (splits == 2) {
+    // Two pieces (the XCD-balanced split): every load is issued before any
+    // result is needed, so the row costs one memory latency instead of three.
+    // The slots of an uncut row are stale; they are loaded but never used.
+    float v0[PER], v1[PER];
+    const int cut = split_at != nullptr
+        ? split_at[(int)(row / ((size_t)C * Hq)) * G + (int)((row / C) % Hq) / group_size]
+        : 0;
+    const float l0 = part_lse[row], l1 = part_lse[nrows + row];
+    load_part(0, v0);
+    load_part(1, v1);
+    if (cut < 0) return;   // a table row that was not cut wrote its output already
+    mx = fmaxf(l0, l1);
+    if (mx != -INFINITY) {
+      const float w0 = l0 == -INFINITY ? 0.f : expf(l0 - mx);
+      const float w1 = l1 == -INFINITY ? 0.f : expf(l1 - mx);
+      wsum = w0 + w1;
+#pragma unroll
+      for (int x = 0; x < PER; ++x)
+        acc[x] = (w0 > 0.f ? w0 * v0[x] : 0.f) + (w1 > 0.f ? w1 * v1[x] : 0.f);
+    }
+  } else {
+    if (split_at != nullptr) {   // a table row that was not cut wrote its output already
+      const int hh = (int)((row / C) % Hq), bb = (int)(row / ((size_t)C * Hq));
+      if (split_at[bb * G + hh / group_size] < 0) return;
+    }
+    for (int i = 0; i < splits; ++i) mx = fmaxf(mx, part_lse[(size_t)i * nrows + row]);
+  }
+  if (splits != 2 && mx != -INFINITY) {
     for (int i = 0; i < splits; ++i) {
       const float li = part_lse[(size_t)i * nrows + row];
       if (li == -INFINITY) continue;
       const float wgt = expf(li - mx);
       wsum += wgt;
-      const float* po = part_o + ((size_t)i * nrows + row) * D + sub * PER;
       float v[PER];
-      if constexpr (PER == 4) {
-        const float4 f = *reinterpret_cast<const float4*>(po);
-        v[0] = f.x, v[1] = f.y, v[2] = f.z, v[3] = f.w;
-      } else {
-        const float2 f = *reinterpret_cast<const float2*>(po);
-        v[0] = f.x, v[1] = f.y;
-      }
+      load_part(i, v);
 #pragma unroll
       for (int x = 0; x < PER; ++x) acc[x] = fmaf(wgt, v[x], acc[x]);
     }
