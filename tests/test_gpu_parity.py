@@ -393,7 +393,7 @@ def test_attention_tiny_groups_and_sharp(gs, scale_mult, workload_inputs):
         print(compare_attention(got, lse, ref, ref_lse))
 
 
-@pytest.mark.parametrize("splits", [1, 3, 0])
+@pytest.mark.parametrize("splits", [1, 2, 3, 0])
 def test_attention_unaligned_full(splits, workload_inputs, oracle_estimate):
     """Every output row on three sequences of 1000 / 37 / 0 cached tokens + a
     200-token chunk (partial last query tile and page, a block shared by cache
@@ -457,8 +457,9 @@ def test_attention_first_chunk_no_cache():
     got, lse = _run_attention(p, x, csr, w.group_size, w.sm_scale, num_splits=1)
     compare_attention(got, lse, ref, ref_lse)
     # dense with splits: the early query tiles see fewer blocks than later
-    # splits start at (those splits are empty)
-    for splits in (1, 3):
+    # splits start at (those splits are empty; with 2 pieces the combine's
+    # two-piece path meets an empty piece next to stale partial slots)
+    for splits in (1, 2, 3):
         got, lse = _run_attention(p, x, None, w.group_size, w.sm_scale, num_splits=splits,
                                   dense=True)
         compare_attention(got, lse, ref, ref_lse)
