@@ -50,7 +50,14 @@ def parse():
                     help="also run the alpha-threshold selector at several (alpha, temperature)")
     ap.add_argument("--no-arms", action="store_true",
                     help="skip the copy and block-sparse execution arms")
-    ap.add_argument("--cpu-sample-queries", type=int, default=1024)
+    ap.add_argument("--v-layout", choices=("transposed", "token_major"), default="transposed",
+                    help="V page layout of the timed pool: transposed [P, D, 64] or the "
+                         "paper's token-major [P, 64, D]; the attention kernel is timed in "
+                         "the other layout as well")
+    ap.add_argument("--no-c5", action="store_true",
+                    help="skip the cumulative 64-chunk prefill of one 128K sequence")
+    ap.add_argument("--no-iid", action="store_true",
+                    help="skip the literal-iid (rho = 0) reading of the inputs")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of 256 MiB (to scale HBM counters)")
     return ap.parse_args()
@@ -215,15 +222,33 @@ def density_sweep(ca, p, w, q, kp, vp, pt, dense_ms, args, stream, ev):
     return res
 
 
-def cpu_baseline(w, d, tables_T, sample_queries: int):
-    """Oracle on the host: full estimator and tables, attention on a sample of
-    queries of one group scaled to the whole chunk (ms for one full step)."""
-    import oracle
+def host_cpu() -> dict:
+    """CPU model, logical CPUs and BLAS threads of the host the oracle runs on."""
+    model = platform.processor() or platform.machine()
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
     try:
         from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        blas = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:  # pragma: no cover
-        threads = os.cpu_count() or 1
+        blas = os.cpu_count() or 1
+    return {"cpu_model": model, "os_cpu_count": os.cpu_count(), "blas_threads": int(blas),
+            "omp_num_threads": os.environ.get("OMP_NUM_THREADS")}
+
+
+def cpu_baseline(w, d):
+    """The oracle on the host over one whole step of the workload, unscaled:
+    fp64 estimator (pooling, scores, top-k selection), set-logic tables and
+    fp64 attention of every query head and chunk query over the gathered
+    selected pages (ms for the step, per stage)."""
+    import oracle
+    host = host_cpu()
     params = oracle.EstimatorParams(w.top_frac, w.sink_blocks, w.local_blocks)
     t0 = time.perf_counter()
     masks = oracle.estimate_masks(d["q"], d["k_pool"], d["page_table"], d["cached_len"],
@@ -231,22 +256,20 @@ def cpu_baseline(w, d, tables_T, sample_queries: int):
     t1 = time.perf_counter()
     T = oracle.block_tables(masks, w.group_size, [w.n_kv_blocks(b) for b in range(w.batch)])
     t2 = time.perf_counter()
-    rng = np.random.default_rng(0)
-    qs = np.sort(rng.choice(w.chunk_len, size=min(sample_queries, w.chunk_len), replace=False))
-    heads = [(0, h) for h in range(w.group_size)]           # group 0 of sequence 0
     oracle.chunk_attention(d["q"], d["k_pool"], d["v_pool"], d["page_table"], d["cached_len"],
-                           T, w.group_size, w.sm_scale, heads=heads, queries=qs)
+                           T, w.group_size, w.sm_scale)
     t3 = time.perf_counter()
-    scale = (w.batch * w.num_q_heads * w.chunk_len) / (len(heads) * len(qs))
-    total_ms = 1e3 * ((t1 - t0) + (t2 - t1) + (t3 - t2) * scale)
+    total_ms = 1e3 * (t3 - t0)
     return {
-        "value": round(total_ms, 1), "unit": "ms", "cores": int(threads), "kind": "oracle",
-        "sample": (f"estimator + tables on the full chunk; fp64 attention on {len(qs)} queries x "
-                   f"{len(heads)} heads of group 0, scaled x{scale:.0f} to all queries"),
+        "value": round(total_ms, 1), "unit": "ms", "cores": host["blas_threads"],
+        "kind": "oracle",
+        "sample": (f"one whole step, unscaled: estimator + tables + fp64 attention of all "
+                   f"{w.batch * w.num_q_heads} query heads x {w.chunk_len} queries "
+                   "(matrix products on the BLAS threads; exp, set logic and gathers on "
+                   "one thread)"),
         "stage_ms": {"estimate": round(1e3 * (t1 - t0), 1), "tables": round(1e3 * (t2 - t1), 1),
-                     "attention_scaled": round(1e3 * (t3 - t2) * scale, 1)},
-        "host": platform.processor() or platform.machine(),
-        "os_cpu_count": os.cpu_count(),
+                     "attention": round(1e3 * (t3 - t2), 1)},
+        **host,
     }
 
 
@@ -354,12 +377,14 @@ def strategy_arms(ca, p, w, q, kp, vp, pt, masks, tables, ip, args, stream, ev):
     return res
 
 
-def chunk_sweep(ca, stream, ev):
-    """Chunked prefill of one 131072-token sequence at chunk sizes 512, 1024 and
-    2048 (Sec. 4.3 / Table 5 sizes): per chunk the incremental estimator (only
-    the newly cached blocks are pooled), the tables and the attention, against
-    the dense paged attention of the same chunk.  One layer, one timed pass per
-    chunk; the sums are the cumulative attention-side prefill cost."""
+def chunk_sweep(ca, stream, ev, sizes=(512, 1024, 2048), v_layout=None):
+    """Chunked prefill of one 131072-token sequence at the given chunk sizes
+    (512 / 1024 / 2048 are the sizes of Sec. 4.3, Table 5; 2048 alone is the
+    64-chunk sweep workload): per chunk the incremental estimator (only the
+    newly cached blocks are pooled), the tables and the attention, against the
+    dense paged attention of the same chunk.  One layer, one timed pass per
+    chunk; the sums are the cumulative attention-side prefill cost (Sec. 2.1:
+    the pattern search is paid again at every chunk)."""
     import torch
     from dataclasses import replace
 
@@ -369,11 +394,14 @@ def chunk_sweep(ca, stream, ev):
     total = base.chunk_len * synth.configs.SWEEP_CHUNKS
     dev = "cuda"
     bf = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
+    if v_layout is None:
+        v_layout = ca.V_TRANSPOSED
     res = {}
-    for C in (512, 1024, 2048):
+    for C in sizes:
         n = total // C
         seq = synth.make_sweep_sequence(replace(base, chunk_len=C), n_chunks=n)
-        kd, vd = bf(seq.k_pool), bf(synth.v_pages_transposed(seq.v_pool))
+        vpool = synth.v_pages_transposed(seq.v_pool) if v_layout == ca.V_TRANSPOSED else seq.v_pool
+        kd, vd = bf(seq.k_pool), bf(vpool)
         k_mean = torch.zeros((1, base.num_kv_heads, base.max_kv_blocks, base.head_dim),
                              dtype=torch.float32, device=dev)
         cb = C // base.page_size
@@ -385,7 +413,7 @@ def chunk_sweep(ca, stream, ev):
         for c in range(-1, n):          # c = -1: untimed warm-up on chunk 0
             d = seq.inputs(max(c, 0))
             w = d["workload"]
-            p = ca.Problem.from_workload(w, device=dev)
+            p = ca.Problem.from_workload(w, device=dev, v_layout=v_layout)
             q, pt = bf(d["q"]), torch.from_numpy(d["page_table"]).to(dev)
             m = [ev() for _ in range(8)]
             torch.cuda.synchronize()
@@ -436,6 +464,73 @@ def host_ahead(torch):
     enqueued before the GPU reaches them: stage timings between events then
     measure GPU time, not the host's launch overhead."""
     torch.cuda._sleep(1_000_000)
+
+
+def literal_iid(ca, w, args, stream, ev, v_layout):
+    """The same step on literal iid N(0, 1) inputs (rho = 0, the other reading
+    of the configs' "bf16 N(0,1) Q/K/V"): mean-pooled block scores are then
+    nearly independent across Q-blocks and heads, and the two unions of
+    Sec. 3.2 reopen most of the cache.  Reported beside the calibrated
+    reading: densities, whole-step time and speedup against dense."""
+    import torch
+    from dataclasses import replace
+
+    import synth
+
+    w0 = replace(w, rho=0.0)
+    d0 = synth.make_inputs(w0)
+    dev = "cuda"
+    bf = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
+    vpool = synth.v_pages_transposed(d0["v_pool"]) if v_layout == ca.V_TRANSPOSED else d0["v_pool"]
+    q, kp, vp = bf(d0["q"]), bf(d0["k_pool"]), bf(vpool)
+    pt = torch.from_numpy(d0["page_table"]).to(dev)
+    p = ca.Problem.from_workload(w0, device=dev, v_layout=v_layout)
+    gs = w0.group_size
+    G = w0.num_q_heads // gs
+    R = w0.batch * G
+    bufs = {}
+    tables = (torch.empty(R + 1, dtype=torch.int32, device=dev),
+              torch.empty(R * w0.max_kv_blocks, dtype=torch.int32, device=dev))
+    tws = torch.empty(max(ca.tables_workspace_bytes(p, gs), 1), dtype=torch.uint8, device=dev)
+    aws_n = ca.attention_workspace_bytes(p, gs, 0)
+    aws = torch.empty(aws_n, dtype=torch.uint8, device=dev) if aws_n else None
+    out = torch.empty_like(q)
+
+    def step():
+        masks, _ = ca.estimate_masks(p, q, kp, pt, w0.top_frac, w0.sink_blocks,
+                                     w0.local_blocks, bufs=bufs)
+        ca.build_block_tables(p, masks, gs, out=tables, ws=tws)
+        ca.chunk_attention(p, q, (kp, vp), pt, tables, gs, w0.sm_scale, num_splits=0, out=out,
+                           ws=aws)
+
+    def timed(fn):
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        a0, a1 = ev(), ev()
+        a0.record(stream)
+        for _ in range(args.steps):
+            fn()
+        a1.record(stream)
+        torch.cuda.synchronize()
+        return a0.elapsed_time(a1) / args.steps
+
+    step_ms = timed(step)
+    attn_ms = timed(lambda: ca.chunk_attention(p, q, (kp, vp), pt, tables, gs, w0.sm_scale,
+                                               num_splits=0, out=out, ws=aws))
+    dense_ms = timed(lambda: ca.dense_paged_chunk_attention(p, q, (kp, vp), pt, w0.sm_scale,
+                                                            out=out))
+    ip, ix = tables[0].cpu().numpy(), tables[1].cpu().numpy()
+    ncached = sum(w0.n_cached_blocks(b) for b in range(w0.batch)) * G
+    sel = sum(int(np.count_nonzero(ix[ip[r]:ip[r + 1]] < w0.n_cached_blocks(r // G)))
+              for r in range(R))
+    bits = np.unpackbits(bufs["masks"].cpu().numpy().view(np.uint8), axis=-1,
+                         bitorder="little").astype(bool)
+    return {"rho": 0.0, "ms_per_step": round(step_ms, 4), "attention_kernel_ms": round(attn_ms, 4),
+            "dense_ms": round(dense_ms, 4), "speedup_vs_dense": round(dense_ms / step_ms, 3),
+            "speedup_vs_dense_kernel_only": round(dense_ms / attn_ms, 3),
+            "densities": stage_densities(w0, bits),
+            "executed_cached_density": round(sel / max(ncached, 1), 4)}
 
 
 THRESHOLD_POINTS = ((16.0, 0.01), (16.0, 0.03), (16.0, 0.06), (16.0, 0.1), (8.0, 0.06))
@@ -513,9 +608,12 @@ def main():
     d = synth.make_inputs(w)
     dev = "cuda"
     bf = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
-    q, kp, vp = bf(d["q"]), bf(d["k_pool"]), bf(synth.v_pages_transposed(d["v_pool"]))
+    v_layout = ca.V_TRANSPOSED if args.v_layout == "transposed" else ca.V_TOKEN_MAJOR
+    v_of = lambda lay: bf(synth.v_pages_transposed(d["v_pool"]) if lay == ca.V_TRANSPOSED
+                          else d["v_pool"])
+    q, kp, vp = bf(d["q"]), bf(d["k_pool"]), v_of(v_layout)
     pt = torch.from_numpy(d["page_table"]).to(dev)
-    p = ca.Problem.from_workload(w, device=dev)
+    p = ca.Problem.from_workload(w, device=dev, v_layout=v_layout)
     gs = w.group_size
     G = w.num_q_heads // gs
     R = w.batch * G
@@ -624,6 +722,23 @@ def main():
     a1.record(stream)
     torch.cuda.synchronize()
     attn_ms = a0.elapsed_time(a1) / args.steps
+    # the same launches on a pool in the other V page layout (bit-identical output)
+    other = ca.V_TOKEN_MAJOR if v_layout == ca.V_TRANSPOSED else ca.V_TRANSPOSED
+    p_o = ca.Problem.from_workload(w, device=dev, v_layout=other)
+    vp_o = v_of(other)
+    run_o = lambda: ca.chunk_attention(p_o, q, (kp, vp_o), pt, tables, gs, w.sm_scale,
+                                       num_splits=0, out=out, lse=lse, ws=aws)
+    for _ in range(args.warmup):
+        run_o()
+    torch.cuda.synchronize()
+    a0o, a1o = ev(), ev()
+    a0o.record(stream)
+    for _ in range(args.steps):
+        run_o()
+    a1o.record(stream)
+    torch.cuda.synchronize()
+    attn_ms_other = a0o.elapsed_time(a1o) / args.steps
+    del vp_o
     # the same launch one at a time: warm caches, then after a 512 MiB overwrite
     one = lambda: ca.chunk_attention(p, q, (kp, vp), pt, tables, gs, w.sm_scale, num_splits=0,
                                      out=out, lse=lse, ws=aws)
@@ -672,7 +787,8 @@ def main():
         "config": {"workload": w.name, "batch": w.batch, "num_q_heads": w.num_q_heads,
                    "num_kv_heads": w.num_kv_heads, "head_dim": w.head_dim,
                    "cached_tokens": list(w.cached_lens), "chunk_len": w.chunk_len,
-                   "top_frac": w.top_frac, "rho": w.rho, "group_size": gs},
+                   "top_frac": w.top_frac, "rho": w.rho, "group_size": gs,
+                   "v_layout": args.v_layout},
         "stage_ms": {k: round(v, 4) for k, v in st_ms.items()},
         # algorithmic bytes / stage time (attention: the back-to-back launch time)
         "stage_GBps": {k: round(v / ((attn_ms if k == "attention" else st_ms[k]) * 1e-3) / 1e9, 1)
@@ -683,6 +799,9 @@ def main():
         "speedup_vs_dense": round(dense_ms / ms_per_step, 3),
         "speedup_vs_dense_kernel_only": round(dense_ms / attn_ms, 3),
         "attention_kernel_ms": round(attn_ms, 4),
+        "attention_kernel_ms_by_v_layout": {
+            args.v_layout: round(attn_ms, 4),
+            ("token_major" if other == ca.V_TOKEN_MAJOR else "transposed"): round(attn_ms_other, 4)},
         "attention_kernel_single_launch_ms": {"warm": percentiles(warm_each),
                                               "flushed": percentiles(flushed_each)},
         "executed_cached_density": round(density, 4),
@@ -705,10 +824,16 @@ def main():
     if args.threshold_sweep:
         res["threshold_sweep"] = threshold_sweep(ca, p, w, q, kp, vp, pt, dense_ms, args,
                                                  stream, ev)
+    if not args.no_iid and w.rho != 0.0:
+        res["literal_iid"] = literal_iid(ca, w, args, stream, ev, v_layout)
     if args.chunk_sweep:
-        res["chunk_sweep"] = chunk_sweep(ca, stream, ev)
+        res["chunk_sweep"] = chunk_sweep(ca, stream, ev, v_layout=v_layout)
+    elif not args.no_c5:
+        # the 64-chunk prefill of one 131072-token sequence (2048-token chunks)
+        res["cumulative_sweep_128k_64chunks"] = chunk_sweep(ca, stream, ev, sizes=(2048,),
+                                                            v_layout=v_layout)["2048"]
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(w, d, None, args.cpu_sample_queries)
+        res["cpu_baseline"] = cpu_baseline(w, d)
     print(json.dumps(res), flush=True)
 
 

@@ -28,15 +28,22 @@
  *   must start on a 16-byte boundary (CA_ERR_UNALIGNED otherwise; any
  *   hipMalloc or torch allocation does), and so must the attention
  *   workspace (CA_ERR_WORKSPACE).
- * - KV cache: KV-head-major pages (Sec. 3.3, Fig. 4).  Logical block j of
- *   (sequence b, KV head kvh) is physical page page_table[b, kvh, j] of
- *   k_pool and v_pool; one page id addresses the K page and the V page.
- *   k_pool is [P, page_size, head_dim] (token-major pages, as the paper's
- *   cache).  v_pool is [P, head_dim, page_size]: every V page is stored
- *   transposed, dimension-major with the page's tokens contiguous (the
- *   layout of vLLM's original paged V cache), so that the attention kernel
- *   reads each V^T operand fragment with one 16-byte LDS read.  page_table
- *   is int32 [B, Hkv, max_kv_blocks]; entries at j >= nKB_b are ignored.
+ * - KV cache: KV-head-major pages (Sec. 3.3, Fig. 4; App. B.2).  Logical
+ *   block j of (sequence b, KV head kvh) is physical page
+ *   page_table[b, kvh, j] of k_pool and v_pool; one page id addresses the K
+ *   page and the V page.  k_pool is [P, page_size, head_dim] (token-major
+ *   pages, one [block, D] region per page, as the paper's cache).  v_pool
+ *   has the layout named by ca_problem.v_layout:
+ *     CA_V_TOKEN_MAJOR (0, the default of a zeroed struct): [P, page_size,
+ *       head_dim], the same token-major pages as K (the paper's layout; a
+ *       cache writer appends a token's V as one contiguous row).  The kernel
+ *       reads each V^T operand fragment with two gfx950 transpose reads;
+ *     CA_V_TRANSPOSED (1): [P, head_dim, page_size], every V page stored
+ *       dimension-major with the page's tokens contiguous (the layout of
+ *       vLLM's original paged V cache); each V^T fragment is one 16-byte
+ *       LDS read.
+ *   Only the attention entry points read v_pool.  page_table is int32
+ *   [B, Hkv, max_kv_blocks]; entries at j >= nKB_b are ignored.
  * - Per sequence b: cached_len[b] tokens are already in the cache and the
  *   chunk adds chunk_len tokens (any lengths).  Chunk token t sits at
  *   absolute position cached_len[b] + t, key r of block j at
@@ -77,7 +84,7 @@
 extern "C" {
 #endif
 
-#define CA_ABI_VERSION 4
+#define CA_ABI_VERSION 5
 
 typedef enum ca_status {
   CA_OK = 0,
@@ -102,7 +109,12 @@ typedef struct ca_problem {
   int32_t max_kv_blocks;     /* row stride of page_table, >= max_b nKB_b, <= 16384 */
   const int32_t* cached_len_host; /* HOST [B]: >= 0, any length                 */
   const int32_t* cached_len;      /* DEVICE [B]: the same values                */
+  int32_t v_layout;          /* CA_V_TOKEN_MAJOR or CA_V_TRANSPOSED (v_pool)   */
 } ca_problem;
+
+/* ca_problem.v_layout: layout of the V pages of v_pool (see the file header). */
+#define CA_V_TOKEN_MAJOR 0   /* [P, page_size, head_dim], as the K pages        */
+#define CA_V_TRANSPOSED 1    /* [P, head_dim, page_size]                         */
 
 int ca_abi_version(void);
 const char* ca_status_string(ca_status s);
@@ -311,10 +323,11 @@ ca_status ca_block_sparse_chunk_attention(const ca_problem* p, const uint16_t* q
  *    ca_gather_selected_pages: packed page p (0 <= p < kv_indptr[B*G]) gets
  *    K_pool / V_pool page page_table[b, kvh, kv_indices[p]] of the row that
  *    owns entry p; k_packed is bf16 [capacity_pages, page, D] and v_packed
- *    [capacity_pages, D, page] (pages copied whole, in the pools' layouts);
- *    capacity_pages must be >= kv_indptr[B*G] (B*G*max_kv_blocks always
- *    is; entries beyond the capacity are not copied).  Invalid entries
- *    (kv_indices outside [0, max_kv_blocks)) are skipped.
+ *    has capacity_pages pages in the layout of v_pool (ca_problem.v_layout;
+ *    pages are copied whole); capacity_pages must be >= kv_indptr[B*G]
+ *    (B*G*max_kv_blocks always is; entries beyond the capacity are not
+ *    copied).  Invalid entries (kv_indices outside [0, max_kv_blocks)) are
+ *    skipped.
  *    ca_packed_chunk_attention: the section 3 result for the same tables,
  *    reading table entry p from packed page p (no page_table); the same
  *    kernel, so the output is bit-identical to ca_chunk_attention.

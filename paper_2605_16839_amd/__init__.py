@@ -12,4 +12,6 @@ from .binding import (  # noqa: F401
     packed_chunk_attention, estimate_masks_threshold, select_blocks_threshold, estimate_tables,
     EXPORTED,
     LIB_PATH,
+    V_TOKEN_MAJOR,
+    V_TRANSPOSED,
 )

@@ -43,7 +43,14 @@ class CAProblem(ctypes.Structure):
         ("max_kv_blocks", ctypes.c_int32),
         ("cached_len_host", _c_i32p),
         ("cached_len", ctypes.c_void_p),
+        ("v_layout", ctypes.c_int32),
     ]
+
+
+# ca_problem.v_layout: V pages token-major [P, page, D] (the paper's layout, as
+# the K pages) or transposed [P, D, page]
+V_TOKEN_MAJOR = 0
+V_TRANSPOSED = 1
 
 
 class CAError(RuntimeError):
@@ -136,15 +143,17 @@ class Problem:
 
     Holds the ca_problem struct, the host copy of cached_len that it points
     to, and the device copy (on ``device``; None for host-only validation).
+    ``v_layout`` names the layout of the V pages the attention calls read.
     """
 
     def __init__(self, batch: int, num_q_heads: int, num_kv_heads: int, head_dim: int,
                  q_block: int, chunk_len: int, max_kv_blocks: int,
                  cached_len: Sequence[int], page_size: int = 64,
-                 device: Optional[str] = "cuda"):
+                 device: Optional[str] = "cuda", v_layout: int = V_TOKEN_MAJOR):
         self.batch, self.num_q_heads, self.num_kv_heads = batch, num_q_heads, num_kv_heads
         self.head_dim, self.q_block, self.chunk_len = head_dim, q_block, chunk_len
         self.page_size, self.max_kv_blocks = page_size, max_kv_blocks
+        self.v_layout = v_layout
         self._host = (ctypes.c_int32 * len(cached_len))(*[int(c) for c in cached_len])
         self.cached_len = [int(c) for c in cached_len]
         self.cached_len_dev = (torch.tensor(self.cached_len, dtype=torch.int32, device=device)
@@ -152,12 +161,14 @@ class Problem:
         self.c = CAProblem(batch, num_q_heads, num_kv_heads, head_dim, page_size, q_block,
                            chunk_len, max_kv_blocks,
                            ctypes.cast(self._host, _c_i32p),
-                           self.cached_len_dev.data_ptr() if self.cached_len_dev is not None else None)
+                           self.cached_len_dev.data_ptr() if self.cached_len_dev is not None else None,
+                           v_layout)
 
     @classmethod
-    def from_workload(cls, w, device: Optional[str] = "cuda") -> "Problem":
+    def from_workload(cls, w, device: Optional[str] = "cuda",
+                      v_layout: int = V_TOKEN_MAJOR) -> "Problem":
         return cls(w.batch, w.num_q_heads, w.num_kv_heads, w.head_dim, w.q_block, w.chunk_len,
-                   w.max_kv_blocks, w.cached_lens, w.page_size, device)
+                   w.max_kv_blocks, w.cached_lens, w.page_size, device, v_layout)
 
     @property
     def ref(self):
@@ -378,8 +389,8 @@ def chunk_attention(p: Problem, q_chunk: torch.Tensor, kv_pool: Tuple[torch.Tens
                     ws: Optional[torch.Tensor] = None, stream=None):
     """Attention of the chunk over its groups' tables; returns (out bf16, lse fp32 or None).
 
-    ``kv_pool`` = (k_pool ``[P, page, D]``, v_pool ``[P, D, page]``: V pages
-    transposed, see ``synth.v_pages_transposed``)."""
+    ``kv_pool`` = (k_pool ``[P, page, D]``, v_pool ``[P, page, D]``, or
+    ``[P, D, page]`` when ``p.v_layout == V_TRANSPOSED``)."""
     k_pool, v_pool = kv_pool
     if out is None:
         out = torch.empty_like(q_chunk)

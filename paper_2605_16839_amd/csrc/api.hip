@@ -53,6 +53,9 @@ ca_status check(const ca_problem* p, int32_t group_size, ca::Dims* d) {
   if (p->q_block != 64 && p->q_block != 128)
     return fail(CA_ERR_UNSUPPORTED, "q_block %d not supported (64, 128)", p->q_block);
   if (p->chunk_len < 1) return fail(CA_ERR_SHAPE, "chunk_len must be >= 1");
+  if (p->v_layout != CA_V_TOKEN_MAJOR && p->v_layout != CA_V_TRANSPOSED)
+    return fail(CA_ERR_SHAPE, "v_layout %d is not CA_V_TOKEN_MAJOR (0) or CA_V_TRANSPOSED (1)",
+                p->v_layout);
   if (p->max_kv_blocks < 1 || p->max_kv_blocks > ca::kMaxKvBlocks)
     return fail(CA_ERR_SHAPE, "max_kv_blocks %d out of range [1, %d]", p->max_kv_blocks,
                 ca::kMaxKvBlocks);
@@ -169,6 +172,10 @@ ca_status run_attention(const ca_problem* p, const uint16_t* q, const uint16_t* 
     return fail(CA_ERR_SHAPE, "capacity_pages must be >= 1");
   if (!dense && (!kv_indptr || !kv_indices))
     return fail(CA_ERR_NULL, "kv_indptr and kv_indices are required");
+  // softmax(sm_scale * q.k): a zero, negative or non-finite scale would turn the
+  // masked (-inf) scores into NaN or +inf weights
+  if (!(sm_scale > 0.f) || !std::isfinite(sm_scale))
+    return fail(CA_ERR_SHAPE, "sm_scale must be finite and > 0, got %g", (double)sm_scale);
   if ((s = attention_tile_ok(group_size, table_mode)) != CA_OK) return s;
   if (num_splits < 0 || num_splits > 64)
     return fail(CA_ERR_SHAPE, "num_splits %d out of range [0, 64]", num_splits);
@@ -205,6 +212,7 @@ ca_status run_attention(const ca_problem* p, const uint16_t* q, const uint16_t* 
   L.dense = dense;
   L.table_mode = table_mode;
   L.packed_pages = packed_pages;
+  L.v_layout = p->v_layout == CA_V_TRANSPOSED ? ca::kVTransposed : ca::kVTokenMajor;
   return hip_status(ca::launch_attention(d, L, static_cast<hipStream_t>(stream)),
                     dense ? "dense paged attention launch" : "chunk attention launch");
 }
@@ -441,6 +449,8 @@ ca_status ca_build_block_tables(const ca_problem* p, const uint64_t* masks, int3
   if (ws == nullptr || ws_bytes < need)
     return fail(CA_ERR_WORKSPACE, "tables need %zu workspace bytes, got %zu", need,
                 ws == nullptr ? (size_t)0 : ws_bytes);
+  if (reinterpret_cast<uintptr_t>(ws) % sizeof(uint64_t) != 0)
+    return fail(CA_ERR_WORKSPACE, "workspace must be 8-byte aligned (it holds uint64 words)");
   return hip_status(ca::launch_tables(d, masks, p->cached_len, group_size, kv_indptr,
                                       kv_indices, ws, static_cast<hipStream_t>(stream)),
                     "tables launch");
@@ -513,6 +523,8 @@ ca_status ca_build_block_sparse_tables(const ca_problem* p, const uint64_t* mask
   if (ws == nullptr || ws_bytes < need)
     return fail(CA_ERR_WORKSPACE, "block-sparse tables need %zu workspace bytes, got %zu", need,
                 ws == nullptr ? (size_t)0 : ws_bytes);
+  if (reinterpret_cast<uintptr_t>(ws) % sizeof(uint64_t) != 0)
+    return fail(CA_ERR_WORKSPACE, "workspace must be 8-byte aligned (it holds uint64 words)");
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (group_size > 0)
     return hip_status(ca::launch_union_rows(d, masks, p->cached_len, group_size, kv_indptr,

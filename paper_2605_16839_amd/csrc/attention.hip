@@ -2,27 +2,34 @@
 // App. B.2), bf16 MFMA with fp32 online softmax, and the split-KV
 // log-sum-exp combine.
 //
-// Work decomposition: one workgroup = NW wavefronts, one per SIMD (each wave
-// holds up to 512 registers), 64 (head, query) rows per wave:
+// Work decomposition: one workgroup = NW wavefronts; a wave owns 32*CT
+// (head, query) rows, CT 32-column MFMA tiles:
 //   * a table row r = b*G + g serves the group_size query heads of group g;
 //     all of them read the same KV pages, so a workgroup packs rows of every
-//     head of the group (group_size heads x 64*NW/group_size chunk queries)
-//     and each KV page staged in LDS feeds all of them;
-//   * a wave's 64 rows are two 32-column MFMA tiles, so every K and V
-//     fragment it reads from LDS feeds two v_mfma_f32_32x32x16_bf16: half the
-//     LDS traffic per flop of a 32-row wave;
+//     head of the group (group_size heads x 32*CT*NW/group_size chunk
+//     queries) and each KV page staged in LDS feeds all of them;
+//   * the kernels run CT = 2: one wave per SIMD holding up to 512 registers
+//     (the O^T accumulators and Q^T fragments in AGPRs), and every K and V
+//     fragment a wave reads from LDS feeds two v_mfma_f32_32x32x16_bf16 (one
+//     per column tile), half the LDS traffic per flop of a 32-column wave.
+//     CT = 1 (two waves per SIMD, 32 columns and at most 256 registers each,
+//     all VGPRs) also compiles: it keeps the matrix cores busier per cycle,
+//     but doubles the LDS reads and per-page scalar work per flop, and on
+//     MI355X it ran at a lower clock, for no gain in time;
 //   * S^T = K Q^T (keys x queries): every lane holds one query column, so
 //     the softmax statistics are in-lane plus one v_permlane32_swap; then
-//     O^T += V^T P^T with each V^T fragment one 16-byte read: V pages are
-//     stored transposed (D rows x 64 keys) and the lanes read K rows in an
-//     order that gives every lane 8 consecutive keys of P^T;
+//     O^T += V^T P^T.  Lanes read the K rows in an order (key_of_row) that
+//     gives every lane 8 consecutive keys of its P^T fragment, so the
+//     matching V^T fragment is one 16-byte read of a transposed V page
+//     ([D, 64], VL = kVTransposed) or two gfx950 transpose reads
+//     (ds_read_b64_tr_b16) of a token-major page ([64, D], the paper's
+//     layout, VL = kVTokenMajor);
 //   * pages go from HBM into LDS with 16-byte direct-to-LDS buffer loads (no
 //     register round trip) into XOR-swizzled tiles (conflict-free operand
 //     reads);
 //   * software pipeline: step i issues the copies of K(i+2) and V(i), the PV
 //     MFMAs of page i-1 and the QK MFMAs of page i+1, and between them (one
-//     MFMA per slot) the softmax of page i, so the matrix cores and the VALU
-//     of one wave work side by side; one barrier per page;
+//     MFMA per slot) the softmax of page i; one barrier per page;
 //   * the causally masked diagonal pages (and an odd leftover page) run after
 //     the pipeline, one at a time: their keys are compared by absolute
 //     position 64*j + r against cached_len + t (positions from the logical
@@ -40,8 +47,12 @@
 
 namespace ca {
 
-constexpr int kWavesGroup = 4;   // waves per workgroup, per-group tables
-constexpr int kWavesQTile = 2;   // waves per workgroup, one head x 128 queries
+// Per-group tables: 4 waves of 64 columns (one wave per SIMD).  Block-sparse
+// tiles (one head x 128 queries): 2 waves of 64 columns, two workgroups per CU.
+constexpr int kWavesGroup = 4;
+constexpr int kWavesQTile = 2;
+constexpr int kColTiles = 2;     // 32-column MFMA tiles per wave
+constexpr int kWavesPerCu = 4;   // resident waves per CU (1 per SIMD)
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -70,25 +81,45 @@ struct AttnArgs {
 
 constexpr int kXcds = 8;   // MI355X: 8 accelerator complex dies, 32 CUs and one L2 each
 
+// LDS page tiles: K pages and token-major V pages are 64 key rows x D; a
+// transposed V page is D rows x 64 keys.
+constexpr int kTileK = 0;
+constexpr int kTileVT = 1;   // transposed V page
+constexpr int kTileVR = 2;   // token-major V page
+
 // Swizzled position (16-byte chunk) of chunk c of row r in an LDS page tile.
 // gfx950 LDS has 64 banks of 4 bytes; a 16-byte read is served 16 lanes per
-// cycle, so the 16 rows that a read touches at one chunk must land on 16
-// different 16-byte bank slots of the 256-byte bank window.
-// K tiles are 64 key rows x D (a D = 64 row is half a window, so rows pair
-// up); V^T tiles are D rows x 64 keys (128 bytes, two rows per window).
-// Both swizzles leave a row's pattern unchanged under +32 rows (and the K
-// one under +8 and +16), so the operand reads of one lane differ only by
-// immediate offsets.
+// cycle and an 8-byte read 32 lanes per cycle.
+// K tiles are read 16 bytes per lane by 16 rows at one chunk: the 16 rows
+// must land on 16 different 16-byte bank slots of the 256-byte bank window
+// (a D = 64 row is half a window, so rows pair up).
+// Transposed V tiles (128-byte rows, two per window) are read the same way.
+// Token-major V tiles are read 8 bytes per lane by the transpose read, 32
+// lanes covering 4 consecutive rows x 64 bytes: each row's aligned group of
+// 4 chunks must move to a different aligned group of the window.
+// Every swizzle leaves a row's pattern unchanged under +32 rows (K also under
+// +8 and +16, token-major V under +4 and +16), so the operand reads of one
+// lane differ only by immediate offsets.
 template <int D>
 __device__ __forceinline__ int k_swz(int r, int c) {
   return D == 128 ? (c ^ (r & 15)) : (c ^ ((r >> 1) & 7));
 }
 __device__ __forceinline__ int vt_swz(int r, int c) { return c ^ ((r >> 1) & 7); }
+template <int D>
+__device__ __forceinline__ int vr_swz(int r, int c) {
+  return D == 128 ? (c ^ ((r & 3) << 2)) : (c ^ (((r >> 1) & 1) << 2));
+}
+template <int D, int TILE>
+__device__ __forceinline__ int tile_swz(int r, int c) {
+  if constexpr (TILE == kTileVT) return vt_swz(r, c);
+  else if constexpr (TILE == kTileVR) return vr_swz<D>(r, c);
+  else return k_swz<D>(r, c);
+}
 
 // Key row that lane column `col` reads from a K tile: bits 2 and 3 of the
 // key index swapped.  With it the S^T accumulator rows that one lane packs
 // into a P^T fragment are 8 consecutive keys, so the matching V^T fragment
-// is one contiguous 16-byte read of a V^T row.
+// is one contiguous run of keys.
 __device__ __forceinline__ int key_of_row(int r) {
   return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);
 }
@@ -98,6 +129,8 @@ __device__ __forceinline__ int key_of_row(int r) {
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 typedef __attribute__((address_space(3))) void lds_void;
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 // Raw buffer resource of one page (64 rows x D bf16).  The page copies use
 // buffer loads to LDS rather than global_load_lds: while a global_load_lds is
@@ -110,29 +143,28 @@ constexpr int kRawBufferWord3 = 0x00020000;   // gfx9 raw buffer, 32-bit data fo
   __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(page), 0, kPage * (D) * 2,      \
                                     kRawBufferWord3)
 
-// Copy one page (16 KB at D = 128, contiguous in HBM: a K page is 64 rows
-// x D, a V page D rows x 64 keys) into an LDS tile with direct-to-LDS loads.
-// Each wave instruction fills 1 KB of the tile, lane l writing bytes
-// [16l, 16l+16); the lane's source is the chunk that the swizzle maps there
-// (the swizzles are involutions).  NW waves share a page.
-template <int D, bool IS_V>
+// Copy one page (16 KB at D = 128, contiguous in HBM) into an LDS tile with
+// direct-to-LDS loads.  Each wave instruction fills 1 KB of the tile, lane l
+// writing bytes [16l, 16l+16); the lane's source is the chunk that the
+// swizzle maps there (the swizzles are involutions).  NW waves share a page.
+template <int D, int TILE>
 __device__ __forceinline__ uint32_t copy_src_offset(int inst, int lane) {
-  constexpr int RL = IS_V ? kPage : D;   // elements per row
-  constexpr int CPR = RL / 8;            // 16-byte chunks per row
+  constexpr int RL = TILE == kTileVT ? kPage : D;   // elements per row
+  constexpr int CPR = RL / 8;                       // 16-byte chunks per row
   constexpr int ROWS_PER_INST = 64 / CPR;
   const int r = inst * ROWS_PER_INST + lane / CPR;
   const int cpos = lane % CPR;
-  const int c = IS_V ? vt_swz(r, cpos) : k_swz<D>(r, cpos);
+  const int c = tile_swz<D, TILE>(r, cpos);
   return (uint32_t)(r * RL + c * 8);   // unsigned: scalar base + 32-bit offset
 }
-template <int D, int NW, bool IS_V>
+template <int D, int NW, int TILE>
 __device__ __forceinline__ void page_to_lds(const uint16_t* __restrict__ src, uint16_t* tile,
                                             int wv, int lane) {
   constexpr int INST_PER_WAVE = (64 * D * 2) / 1024 / NW;
 #pragma unroll
   for (int m = 0; m < INST_PER_WAVE; ++m) {
     const int inst = wv * INST_PER_WAVE + m;
-    const uint32_t off = copy_src_offset<D, IS_V>(inst, lane);
+    const uint32_t off = copy_src_offset<D, TILE>(inst, lane);
     __builtin_amdgcn_raw_ptr_buffer_load_lds(CA_PAGE_RSRC(src, D), (lds_void*)(tile + inst * 512),
                                              16, 2 * off, 0, 0, 0);
   }
@@ -140,12 +172,12 @@ __device__ __forceinline__ void page_to_lds(const uint16_t* __restrict__ src, ui
 
 // One of the 1 KB copy instructions of page_to_lds (instruction m of this
 // wave), so that a step can spread its copies between MFMAs.
-template <int D, int NW, bool IS_V>
+template <int D, int NW, int TILE>
 __device__ __forceinline__ void page_part_to_lds(const uint16_t* __restrict__ src, uint16_t* tile,
                                                  int wv, int lane, int m) {
   constexpr int INST_PER_WAVE = (64 * D * 2) / 1024 / NW;
   const int inst = wv * INST_PER_WAVE + m;
-  const uint32_t off = copy_src_offset<D, IS_V>(inst, lane);
+  const uint32_t off = copy_src_offset<D, TILE>(inst, lane);
   __builtin_amdgcn_raw_ptr_buffer_load_lds(CA_PAGE_RSRC(src, D), (lds_void*)(tile + inst * 512),
                                            16, 2 * off, 0, 0, 0);
 }
@@ -186,60 +218,88 @@ __device__ __forceinline__ float halves_sum(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// S^T tiles of one page for the wave's two column tiles: s[c][h] holds keys
+// S^T tiles of one page for the wave's column tiles: s[c][h] holds keys
 // 32h .. 32h+31 of column tile c; accumulator slot v of lane half hf is row
 // 8*(v/4) + 4*hf + v%4 of the tile, i.e. key
 // 32h + 16*(v/8) + 8*hf + 4*((v/4)%2) + v%4 (key_of_row).
+template <int CT>
 struct SPage {
-  f32x16 s[2][2];
+  f32x16 s[CT][2];
 };
 // P^T fragments (bf16) of one page: p[c][kk] covers keys 16kk .. 16kk+15.
+template <int CT>
 struct PFrag {
-  bf16x8 p[2][4];
+  bf16x8 p[CT][4];
 };
 
 // ---- MFMAs with explicit register classes (inline asm) ----
-// O^T accumulators and Q^T fragments live in AGPRs, S^T tiles and P^T
-// fragments in VGPRs.  The compiler cannot see the wait states these
-// instructions need, so the kernel places explicit s_nop fences where an
-// MFMA result is read by VALU code or a VALU result is read by an MFMA.
+// With one wave per SIMD (AG = true) the O^T accumulators and Q^T fragments
+// live in AGPRs and the S^T tiles and P^T fragments in VGPRs; with two waves
+// per SIMD everything is in VGPRs (a wave that uses AGPRs may only hold 128
+// VGPRs).  The compiler cannot see the wait states these instructions need,
+// so the kernel places explicit s_nop fences where an MFMA result is read by
+// VALU code or a VALU result is read by an MFMA.
+template <bool AG>
 __device__ __forceinline__ void mfma_o(f32x16& o, const bf16x8& a, const bf16x8& b) {
-  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(o) : "v"(a), "v"(b));
+  if constexpr (AG) asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(o) : "v"(a), "v"(b));
+  else asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(o) : "v"(a), "v"(b));
 }
+template <bool AG>
 __device__ __forceinline__ void mfma_s0(f32x16& s, const bf16x8& a, const bf16x8& b) {
-  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&v"(s) : "v"(a), "a"(b));
+  if constexpr (AG) asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&v"(s) : "v"(a), "a"(b));
+  else asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&v"(s) : "v"(a), "v"(b));
 }
+template <bool AG>
 __device__ __forceinline__ void mfma_s(f32x16& s, const bf16x8& a, const bf16x8& b) {
-  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(s) : "v"(a), "a"(b));
+  if constexpr (AG) asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(s) : "v"(a), "a"(b));
+  else asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(s) : "v"(a), "v"(b));
 }
 
 // Whole-tuple fence on the O^T accumulators: an MFMA result read or
 // overwritten by VALU code, or a VALU result read by an MFMA, needs wait
 // states the compiler cannot see through inline asm.
-template <int NDT>
-__device__ __forceinline__ void fence_o(f32x16 (&o)[2][NDT]) {
+template <bool AG, int CT, int NDT>
+__device__ __forceinline__ void fence_o(f32x16 (&o)[CT][NDT]) {
 #pragma unroll
-  for (int c = 0; c < 2; ++c)
+  for (int c = 0; c < CT; ++c)
 #pragma unroll
-    for (int x = 0; x < NDT; ++x) asm volatile("s_nop 7\n s_nop 7\n s_nop 7" : "+a"(o[c][x]));
+    for (int x = 0; x < NDT; ++x) {
+      if constexpr (AG) asm volatile("s_nop 7\n s_nop 7\n s_nop 7" : "+a"(o[c][x]));
+      else asm volatile("s_nop 7\n s_nop 7\n s_nop 7" : "+v"(o[c][x]));
+    }
 }
 
 // Fences on S^T tiles (MFMA results about to be read by the softmax) and on
 // P^T fragments (VALU results about to be read by MFMAs).
-__device__ __forceinline__ void fence_sp(SPage& s, PFrag& p) {
-  asm volatile("s_nop 7\n s_nop 7\n s_nop 4"
-               : "+v"(s.s[0][0]), "+v"(s.s[0][1]), "+v"(s.s[1][0]), "+v"(s.s[1][1]),
-                 "+v"(p.p[0][0]), "+v"(p.p[0][1]), "+v"(p.p[0][2]), "+v"(p.p[0][3]),
-                 "+v"(p.p[1][0]), "+v"(p.p[1][1]), "+v"(p.p[1][2]), "+v"(p.p[1][3]));
+template <int CT>
+__device__ __forceinline__ void fence_sp(SPage<CT>& s, PFrag<CT>& p) {
+  if constexpr (CT == 2)
+    asm volatile("s_nop 7\n s_nop 7\n s_nop 4"
+                 : "+v"(s.s[0][0]), "+v"(s.s[0][1]), "+v"(s.s[1][0]), "+v"(s.s[1][1]),
+                   "+v"(p.p[0][0]), "+v"(p.p[0][1]), "+v"(p.p[0][2]), "+v"(p.p[0][3]),
+                   "+v"(p.p[1][0]), "+v"(p.p[1][1]), "+v"(p.p[1][2]), "+v"(p.p[1][3]));
+  else
+    asm volatile("s_nop 7\n s_nop 7\n s_nop 4"
+                 : "+v"(s.s[0][0]), "+v"(s.s[0][1]), "+v"(p.p[0][0]), "+v"(p.p[0][1]),
+                   "+v"(p.p[0][2]), "+v"(p.p[0][3]));
 }
-__device__ __forceinline__ void fence_s(SPage& s) {
-  asm volatile("s_nop 7\n s_nop 7\n s_nop 5"
-               : "+v"(s.s[0][0]), "+v"(s.s[0][1]), "+v"(s.s[1][0]), "+v"(s.s[1][1]));
+template <int CT>
+__device__ __forceinline__ void fence_s(SPage<CT>& s) {
+  if constexpr (CT == 2)
+    asm volatile("s_nop 7\n s_nop 7\n s_nop 5"
+                 : "+v"(s.s[0][0]), "+v"(s.s[0][1]), "+v"(s.s[1][0]), "+v"(s.s[1][1]));
+  else
+    asm volatile("s_nop 7\n s_nop 7\n s_nop 5" : "+v"(s.s[0][0]), "+v"(s.s[0][1]));
 }
-__device__ __forceinline__ void fence_p(PFrag& p) {
-  asm volatile("s_nop 7\n s_nop 7\n s_nop 5"
-               : "+v"(p.p[0][0]), "+v"(p.p[0][1]), "+v"(p.p[0][2]), "+v"(p.p[0][3]),
-                 "+v"(p.p[1][0]), "+v"(p.p[1][1]), "+v"(p.p[1][2]), "+v"(p.p[1][3]));
+template <int CT>
+__device__ __forceinline__ void fence_p(PFrag<CT>& p) {
+  if constexpr (CT == 2)
+    asm volatile("s_nop 7\n s_nop 7\n s_nop 5"
+                 : "+v"(p.p[0][0]), "+v"(p.p[0][1]), "+v"(p.p[0][2]), "+v"(p.p[0][3]),
+                   "+v"(p.p[1][0]), "+v"(p.p[1][1]), "+v"(p.p[1][2]), "+v"(p.p[1][3]));
+  else
+    asm volatile("s_nop 7\n s_nop 7\n s_nop 5"
+                 : "+v"(p.p[0][0]), "+v"(p.p[0][1]), "+v"(p.p[0][2]), "+v"(p.p[0][3]));
 }
 
 // Forces v to be computed at this point of the instruction stream (an empty
@@ -250,20 +310,22 @@ __device__ __forceinline__ void pin(const T& v) {
   asm volatile("" : : "v"(v));
 }
 
-// Softmax schedule of one page: 66 element ops (op j: score of element j,
-// exp of element j-1, sum of element j-2, for the 64 weights a lane holds)
-// and 8 packs, the pack of unit u (elements 8u .. 8u+7) right after element
-// op 8u+8.  soft_op(o) is j for an element op, -1-u for a pack.
-constexpr int kSoftOps = 74;
-constexpr int soft_op(int o) {
+// Softmax schedule of one page for E weights per lane: E + 2 element ops
+// (op j: score of element j, exp of element j-1, sum of element j-2) and
+// E / 8 packs, the pack of unit u (elements 8u .. 8u+7) right after element
+// op 8u+8.  soft_op(o, E) is j for an element op, -1-u for a pack.
+constexpr int soft_ops(int E) { return E + 2 + E / 8; }
+constexpr int soft_op(int o, int E) {
   int op = 0;
-  for (int j = 0; j <= 65; ++j) {
+  for (int j = 0; j <= E + 1; ++j) {
     if (op++ == o) return j;
-    if (j >= 8 && j <= 64 && (j - 8) % 8 == 0 && op++ == o) return -1 - (j - 8) / 8;
+    if (j >= 8 && j <= E && (j - 8) % 8 == 0 && op++ == o) return -1 - (j - 8) / 8;
   }
   return 1 << 20;
 }
-static_assert(soft_op(kSoftOps - 1) == 65 && soft_op(9) == -1 && soft_op(kSoftOps - 2) == -8,
+static_assert(soft_op(soft_ops(64) - 1, 64) == 65 && soft_op(9, 64) == -1 &&
+                  soft_op(soft_ops(64) - 2, 64) == -8 && soft_op(soft_ops(32) - 1, 32) == 33 &&
+                  soft_op(soft_ops(32) - 2, 32) == -4,
               "softmax op table");
 
 // Calls f(integral_constant<int, I>) for I = 0 .. N-1 (compile-time indices).
@@ -276,19 +338,25 @@ __device__ __forceinline__ void static_for(F&& f) {
   static_for_impl(f, std::make_integer_sequence<int, N>{});
 }
 
-template <int D, int NW, bool DENSE>
-__global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnArgs a) {
+template <int D, int NW, int CT, bool DENSE, int VL>
+__global__ __launch_bounds__(64 * NW, CT == 1 ? 2 : 1) void paged_attention_kernel(const AttnArgs a) {
+  constexpr bool AG = CT == 2;         // O^T and Q^T in AGPRs (one wave per SIMD)
+  constexpr bool VTR = VL == kVTransposed;
+  constexpr int VTILE = VTR ? kTileVT : kTileVR;
   constexpr int NKS = D / 16;          // QK k-steps
   constexpr int NDT = D / 32;          // O^T d tiles
   constexpr int PAGE = 64 * D;
-  constexpr int ROWS = 64 * NW;
+  constexpr int ROWS = 32 * CT * NW;
   constexpr int NPV = 4 * NDT;         // V^T fragments per page
   constexpr int NQK = 2 * NKS;         // K fragments per page
   constexpr int NFRAG = NPV + NQK;
-  constexpr int NSLOT = 2 * NFRAG;     // one MFMA per slot
+  constexpr int NSLOT = CT * NFRAG;    // one MFMA per slot
+  constexpr int FD = CT == 1 ? 4 : 3;  // fragment prefetch distance (slots)
   constexpr int DMA_PER_STEP = 2 * (64 * D * 2) / 1024 / NW;   // copy instructions per wave
   constexpr int DMA_STRIDE = (NSLOT / 2) / DMA_PER_STEP > 0 ? (NSLOT / 2) / DMA_PER_STEP : 1;
-  constexpr int MAXS = 10;             // slots holding the max / rebase work
+  constexpr int MAXS = 5 * CT;         // slots holding the max / rebase work
+  constexpr int NE = 32 * CT;          // softmax weights per lane per page
+  constexpr int NSOFT = soft_ops(NE);
   __shared__ __attribute__((aligned(1024))) uint16_t k_s0[PAGE];
   __shared__ __attribute__((aligned(1024))) uint16_t k_s1[PAGE];
   __shared__ __attribute__((aligned(1024))) uint16_t v_s0[PAGE];
@@ -345,11 +413,11 @@ __global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnA
   const int QT = ROWS / gs;            // chunk queries per tile
   const int q0 = qt * QT;
   const int q_end = q0 + QT < a.C ? q0 + QT : a.C;   // the last tile may be partial
-  int head[2], tq[2];
-  bool valid[2];
+  int head[CT], tq[CT];
+  bool valid[CT];
 #pragma unroll
-  for (int c = 0; c < 2; ++c) {
-    const int r = wv * 64 + 32 * c + col;
+  for (int c = 0; c < CT; ++c) {
+    const int r = wv * 32 * CT + 32 * c + col;
     head[c] = g * gs + r / QT;
     tq[c] = q0 + r % QT;
     valid[c] = tq[c] < a.C;
@@ -358,7 +426,9 @@ __global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnA
   const int kvh = (g * gs) / (a.Hq / a.Hkv);
   const int cl = a.cached_len[b];
   const int nkb = blocks_for(cl + a.C);
-  const int qpos[2] = {cl + tq[0], cl + tq[1]};
+  int qpos[CT];
+#pragma unroll
+  for (int c = 0; c < CT; ++c) qpos[c] = cl + tq[c];
   const int j_last = (cl + q_end - 1) / kPage;     // last block any row can see
   const int mask_from = cl + q0;                   // keys beyond this need masking
 
@@ -401,27 +471,31 @@ __global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnA
   }
   const int32_t* ptab = a.page_table + ((size_t)b * a.Hkv + kvh) * a.max_kv_blocks;
 
-  bf16x8 qf[2][NKS];
+  bf16x8 qf[CT][NKS];
 #pragma unroll
-  for (int c = 0; c < 2; ++c) {
+  for (int c = 0; c < CT; ++c) {
     const uint16_t* qrow = a.q + (((size_t)b * a.C + tq[c]) * a.Hq + head[c]) * D + 8 * half;
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) {
       qf[c][ks] = *reinterpret_cast<const bf16x8*>(qrow + 16 * ks);
-      asm volatile("s_nop 2" : "+a"(qf[c][ks]));   // into AGPRs before the first MFMA
+      if constexpr (AG) asm volatile("s_nop 2" : "+a"(qf[c][ks]));   // into AGPRs
     }
   }
 
-  f32x16 o[2][NDT];
+  f32x16 o[CT][NDT];
 #pragma unroll
-  for (int c = 0; c < 2; ++c)
+  for (int c = 0; c < CT; ++c)
 #pragma unroll
     for (int x = 0; x < NDT; ++x)
 #pragma unroll
       for (int v = 0; v < 16; ++v) o[c][x][v] = 0.f;
-  fence_o<NDT>(o);
-  float m_run[2] = {-INFINITY, -INFINITY};
-  float l_run[2] = {0.f, 0.f};
+  fence_o<AG, CT, NDT>(o);
+  float m_run[CT], l_run[CT];
+#pragma unroll
+  for (int c = 0; c < CT; ++c) {
+    m_run[c] = -INFINITY;
+    l_run[c] = 0.f;
+  }
 
   int e_end = e1;
   if (DENSE) {
@@ -440,8 +514,8 @@ __global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnA
   // pages run by the software-pipelined loop: an even number of unmasked ones
   const int n_pipe = n_main & ~1;
 
-  SPage SA, SB;
-  PFrag PA, PB;
+  SPage<CT> SA, SB;
+  PFrag<CT> PA, PB;
   int base = 0, blk_cur = 0, pg_cur = 0, blk_nxt = 0, pg_nxt = 0;
   auto fetch = [&](int b0, int& blk, int& pg) {
     int idx = b0 + lane;
@@ -475,26 +549,49 @@ __global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnA
   };
 
   // Per-lane byte offsets of the MFMA operand reads inside a page tile; the
-  // buffer, the d tile of a PV step and the upper 32 keys of a QK step are
-  // immediates.  Lane column col reads key row key_of_row(col) of K, so its
-  // P^T fragment kk holds keys 16kk + 8*half .. +7, read from V^T row
-  // 32x + col as one 16-byte chunk.
-  uint32_t kofs[NKS], vofs[4];
+  // buffer, the d tile or 16-key block of a PV step and the upper 32 keys of
+  // a QK step are immediates.  Lane column col reads key row key_of_row(col)
+  // of K, so its P^T fragment kk holds keys 16kk + 8*half .. +7: in a
+  // transposed V tile one 16-byte chunk of V^T row 32x + col; in a
+  // token-major tile two transpose reads (keys +0..3 and +4..7; the 16 lanes
+  // of a transpose read address 4 key rows x 16 d and receive one d each).
+  constexpr int NVOFS = VTR ? 4 : NDT;
+  uint32_t kofs[NKS], vofs[NVOFS];
 #pragma unroll
   for (int x = 0; x < NKS; ++x) {
     const int kr = key_of_row(col);
     kofs[x] = (uint32_t)(kr * D * 2 + 16 * k_swz<D>(kr, 2 * x + half));
   }
+  if constexpr (VTR) {
 #pragma unroll
-  for (int kk = 0; kk < 4; ++kk) vofs[kk] = (uint32_t)(col * kPage * 2 + 16 * vt_swz(col, 2 * kk + half));
+    for (int kk = 0; kk < 4; ++kk)
+      vofs[kk] = (uint32_t)(col * kPage * 2 + 16 * vt_swz(col, 2 * kk + half));
+  } else {
+    const int grp = lane >> 4, sl = lane & 15;
+    const int r0 = 8 * (grp >> 1) + (sl >> 2);
+#pragma unroll
+    for (int x = 0; x < NDT; ++x) {
+      const int d = 32 * x + 16 * (grp & 1) + 4 * (sl & 3);
+      vofs[x] = (uint32_t)(r0 * D * 2 + 16 * vr_swz<D>(r0, d >> 3) + 2 * (d & 7));
+    }
+  }
   // fragment F of a step: F < NPV is V^T fragment (kk = F / NDT, d tile
   // x = F % NDT), otherwise K fragment (k-step (F - NPV) / 2, keys
   // 32 * ((F - NPV) % 2) ..)
   auto load_frag = [&](int F, const uint16_t* vt, const uint16_t* kt) -> bf16x8 {
     if (F < NPV) {
       const int kk = F / NDT, x = F % NDT;
-      const char* p = reinterpret_cast<const char*>(vt) + vofs[kk] + 32 * kPage * 2 * x;
-      return *reinterpret_cast<const bf16x8*>(p);
+      if constexpr (VTR) {
+        const char* p = reinterpret_cast<const char*>(vt) + vofs[kk] + 32 * kPage * 2 * x;
+        return *reinterpret_cast<const bf16x8*>(p);
+      } else {
+        const char* p = reinterpret_cast<const char*>(vt) + vofs[x] + 16 * kk * D * 2;
+        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p);
+        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 4 * D * 2));
+        const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
+        const u32x4 w = {l2[0], l2[1], h2[0], h2[1]};
+        return __builtin_bit_cast(bf16x8, w);
+      }
     }
     const int G2 = F - NPV;
     const char* p = reinterpret_cast<const char*>(kt) + kofs[G2 / 2] + (G2 % 2) * 32 * D * 2;
@@ -502,23 +599,23 @@ __global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnA
   };
 
   // Whole-page contractions (outside the pipelined loop).
-  auto qk_page = [&](SPage& st, const uint16_t* kt) __attribute__((always_inline)) {
+  auto qk_page = [&](SPage<CT>& st, const uint16_t* kt) __attribute__((always_inline)) {
     static_for<NQK>([&](auto gtag) __attribute__((always_inline)) {
       constexpr int G2 = decltype(gtag)::value, x = G2 / 2, h = G2 % 2;
       const bf16x8 kf = load_frag(NPV + G2, kt, kt);
 #pragma unroll
-      for (int c = 0; c < 2; ++c) {
-        if constexpr (x == 0) mfma_s0(st.s[c][h], kf, qf[c][x]);
-        else mfma_s(st.s[c][h], kf, qf[c][x]);
+      for (int c = 0; c < CT; ++c) {
+        if constexpr (x == 0) mfma_s0<AG>(st.s[c][h], kf, qf[c][x]);
+        else mfma_s<AG>(st.s[c][h], kf, qf[c][x]);
       }
     });
   };
-  auto pv_page = [&](const PFrag& pf, const uint16_t* vt) __attribute__((always_inline)) {
+  auto pv_page = [&](const PFrag<CT>& pf, const uint16_t* vt) __attribute__((always_inline)) {
     static_for<NPV>([&](auto ftag) __attribute__((always_inline)) {
       constexpr int F = decltype(ftag)::value;
       const bf16x8 vf = load_frag(F, vt, vt);
 #pragma unroll
-      for (int c = 0; c < 2; ++c) mfma_o(o[c][F % NDT], vf, pf.p[c][F / NDT]);
+      for (int c = 0; c < CT; ++c) mfma_o<AG>(o[c][F % NDT], vf, pf.p[c][F / NDT]);
     });
   };
 
@@ -526,18 +623,18 @@ __global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnA
   // step's PV reads, with a zero P: that PV adds nothing and every tile read
   // is initialised.  Then S(0).
 #pragma unroll
-  for (int c = 0; c < 2; ++c)
+  for (int c = 0; c < CT; ++c)
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) PB.p[c][kk] = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
   if (n_pipe > 0) {
-    page_to_lds<D, NW, false>(page_ptr(a.k_pool, 0), k_s0, wv, lane);
-    page_to_lds<D, NW, false>(page_ptr(a.k_pool, 1), k_s1, wv, lane);
-    page_to_lds<D, NW, true>(page_ptr(a.v_pool, 0), v_s1, wv, lane);
+    page_to_lds<D, NW, kTileK>(page_ptr(a.k_pool, 0), k_s0, wv, lane);
+    page_to_lds<D, NW, kTileK>(page_ptr(a.k_pool, 1), k_s1, wv, lane);
+    page_to_lds<D, NW, VTILE>(page_ptr(a.v_pool, 0), v_s1, wv, lane);
     copies_landed(k_s0, k_s1, v_s1);
     __syncthreads();
     qk_page(SA, k_s0);
     __syncthreads();
-    fence_sp(SA, PB);   // S(0) and the zero P are read by the first step's first slots
+    fence_sp<CT>(SA, PB);   // S(0) and the zero P are read by the first step's first slots
   }
 
   // Step i: DMA K(i+2) -> k[i%2], V(i) -> v[i%2]; PV(i-1) from v[(i-1)%2] and
@@ -545,10 +642,10 @@ __global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnA
   // per slot, the softmax work spread over the slots.
   auto step = [&](auto par, int i) __attribute__((always_inline)) {
     constexpr int P = decltype(par)::value;
-    SPage& sc = P ? SB : SA;
-    SPage& sn = P ? SA : SB;
-    PFrag& pn = P ? PB : PA;
-    PFrag& po = P ? PA : PB;
+    SPage<CT>& sc = P ? SB : SA;
+    SPage<CT>& sn = P ? SA : SB;
+    PFrag<CT>& pn = P ? PB : PA;
+    PFrag<CT>& po = P ? PA : PB;
     uint16_t* const k_dma = P ? k_s1 : k_s0;
     const uint16_t* const k_rd = P ? k_s0 : k_s1;
     uint16_t* const v_dma = P ? v_s1 : v_s0;
@@ -556,40 +653,44 @@ __global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnA
     const int i2 = i + 2 < n_pipe ? i + 2 : n_pipe - 1;
     const uint16_t* const k_src = page_ptr(a.k_pool, i2);
     const uint16_t* const v_src = page_ptr(a.v_pool, i);
-    // No hazard fence here: the last MFMA writing S (slot 62 or 63) and the
-    // last pack writing P come at least ~25 instructions (end of step, barrier,
-    // page pointers) before their first readers in this step (slot 0 and later).
-    float mx[2][2] = {{-INFINITY, -INFINITY}, {-INFINITY, -INFINITY}};
-    float alpha[2] = {1.f, 1.f}, nmb[2] = {0.f, 0.f};
-    float ps[2] = {0.f, 0.f};
+    // No hazard fence here: the last MFMA writing S and the last pack writing
+    // P come well before their first readers in this step (end of step,
+    // barrier, page pointers); the hazard test checks the distance.
+    float mx[CT][2], alpha[CT], nmb[CT], ps[CT];
+#pragma unroll
+    for (int c = 0; c < CT; ++c) {
+      mx[c][0] = mx[c][1] = -INFINITY;
+      alpha[c] = 1.f;
+      nmb[c] = 0.f;
+      ps[c] = 0.f;
+    }
     bool rb_any = false;
     bf16x8 fr[NFRAG];
-    fr[0] = load_frag(0, v_rd, k_rd);
-    fr[1] = load_frag(1, v_rd, k_rd);
-    fr[2] = load_frag(2, v_rd, k_rd);
+#pragma unroll
+    for (int f = 0; f < FD; ++f) fr[f] = load_frag(f, v_rd, k_rd);
     static_for<NSLOT>([&](auto stag) __attribute__((always_inline)) {
       constexpr int s = decltype(stag)::value;
-      constexpr int F = s / 2, c = s % 2;
-      if constexpr (c == 0 && F + 3 < NFRAG) fr[F + 3] = load_frag(F + 3, v_rd, k_rd);
+      constexpr int F = s / CT, c = s % CT;
+      if constexpr (c == 0 && F + FD < NFRAG) fr[F + FD] = load_frag(F + FD, v_rd, k_rd);
       // the copies of K(i+2) and V(i), one instruction every DMA_STRIDE slots
       // over the first half of the step (issued all at once they queue in
       // the address unit and stall the wave)
       if constexpr (s % DMA_STRIDE == 0 && s / DMA_STRIDE < DMA_PER_STEP) {
         constexpr int m = s / DMA_STRIDE;
         if constexpr (m < DMA_PER_STEP / 2)
-          page_part_to_lds<D, NW, false>(k_src, k_dma, wv, lane, m);
+          page_part_to_lds<D, NW, kTileK>(k_src, k_dma, wv, lane, m);
         else
-          page_part_to_lds<D, NW, true>(v_src, v_dma, wv, lane, m - DMA_PER_STEP / 2);
+          page_part_to_lds<D, NW, VTILE>(v_src, v_dma, wv, lane, m - DMA_PER_STEP / 2);
       }
       if constexpr (F < NPV) {
-        mfma_o(o[c][F % NDT], fr[F], po.p[c][F / NDT]);
+        mfma_o<AG>(o[c][F % NDT], fr[F], po.p[c][F / NDT]);
       } else {
         constexpr int G2 = F - NPV, x = G2 / 2, h = G2 % 2;
-        if constexpr (x == 0) mfma_s0(sn.s[c][h], fr[F], qf[c][x]);
-        else mfma_s(sn.s[c][h], fr[F], qf[c][x]);
+        if constexpr (x == 0) mfma_s0<AG>(sn.s[c][h], fr[F], qf[c][x]);
+        else mfma_s<AG>(sn.s[c][h], fr[F], qf[c][x]);
       }
       // softmax work of this slot
-      if constexpr (s < 8) {
+      if constexpr (s < 4 * CT) {
         // two independent max chains per column tile (half the dependent latency)
         constexpr int cc = s / 4, k0 = 4 * (s % 4);
         mx[cc][0] = max3(mx[cc][0], sc.s[cc][0][k0], sc.s[cc][1][k0]);
@@ -599,7 +700,7 @@ __global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnA
         pin(mx[cc][0]);
         pin(mx[cc][1]);
       } else if constexpr (s < MAXS) {
-        constexpr int cc = s - 8;
+        constexpr int cc = s - 4 * CT;
         const float m = halves_max(fmaxf(mx[cc][0], mx[cc][1])) * a.scale_log2;
         const bool rebase = m > m_run[cc] + kRescaleSlack;
         alpha[cc] = rebase ? fast_exp2(m_run[cc] - m) : 1.0f;
@@ -614,18 +715,18 @@ __global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnA
         // the scaled score of element j, the exp of element j-1 and the row
         // sum of element j-2 (elements in unit order, unit u = 8 weights of
         // one P^T fragment); unit u is packed to bf16 after element op 8u+8.
-        constexpr int lo = ((s - MAXS) * kSoftOps) / (NSLOT - MAXS);
-        constexpr int hi = ((s - MAXS + 1) * kSoftOps) / (NSLOT - MAXS);
+        constexpr int lo = ((s - MAXS) * NSOFT) / (NSLOT - MAXS);
+        constexpr int hi = ((s - MAXS + 1) * NSOFT) / (NSLOT - MAXS);
         static_for<hi - lo>([&](auto otag) __attribute__((always_inline)) {
-          constexpr int op = soft_op(lo + decltype(otag)::value);
+          constexpr int op = soft_op(lo + decltype(otag)::value, NE);
           if constexpr (op >= 0) {
-            if constexpr (op < 64) {
+            if constexpr (op < NE) {
               constexpr int u = op / 8, cc = u / 4, kk = u % 4, v = 8 * (kk % 2) + op % 8;
               f32x16& sv = sc.s[cc][kk / 2];
               sv[v] = fmaf(sv[v], a.scale_log2, nmb[cc]);
               pin(sv[v]);
             }
-            if constexpr (op >= 1 && op <= 64) {
+            if constexpr (op >= 1 && op <= NE) {
               constexpr int e = op - 1, u = e / 8, cc = u / 4, kk = u % 4, v = 8 * (kk % 2) + e % 8;
               f32x16& sv = sc.s[cc][kk / 2];
               sv[v] = fast_exp2(sv[v]);
@@ -648,15 +749,15 @@ __global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnA
       __builtin_amdgcn_sched_barrier(0);
     });
 #pragma unroll
-    for (int c = 0; c < 2; ++c) l_run[c] = l_run[c] * alpha[c] + ps[c];
+    for (int c = 0; c < CT; ++c) l_run[c] = l_run[c] * alpha[c] + ps[c];
     const uint64_t any = __ballot(rb_any);
     if (any) {   // the exponent base moved on some lane: rescale O (rare)
-      fence_o<NDT>(o);
+      fence_o<AG, CT, NDT>(o);
 #pragma unroll
-      for (int c = 0; c < 2; ++c)
+      for (int c = 0; c < CT; ++c)
 #pragma unroll
         for (int x = 0; x < NDT; ++x) o[c][x] *= alpha[c];
-      fence_o<NDT>(o);
+      fence_o<AG, CT, NDT>(o);
     }
     copies_landed(k_dma, v_dma);
     __syncthreads();
@@ -671,7 +772,7 @@ __global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnA
       step(P1{}, i + 1);
     }
     // PV of page n_pipe - 1 (odd: its P is PB, its V in v_s1)
-    fence_p(PB);
+    fence_p<CT>(PB);
     pv_page(PB, v_s1);
     __syncthreads();
   }
@@ -681,30 +782,31 @@ __global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnA
   // mask, softmax, O += V^T P^T.
   for (int i = n_pipe; i < n; ++i) {
     advance(i);
-    page_to_lds<D, NW, false>(page_ptr(a.k_pool, i), k_s0, wv, lane);
-    page_to_lds<D, NW, true>(page_ptr(a.v_pool, i), v_s0, wv, lane);
+    page_to_lds<D, NW, kTileK>(page_ptr(a.k_pool, i), k_s0, wv, lane);
+    page_to_lds<D, NW, VTILE>(page_ptr(a.v_pool, i), v_s0, wv, lane);
     copies_landed(k_s0, v_s0);
     __syncthreads();
     if (i >= n_main) {
       // The tokens of a sequence's last page past its end are not part of it
       // and may hold anything: their weights are exactly 0, so their V
-      // entries (the last `past` keys of every V^T row) are zeroed to keep
+      // entries (the last `past` keys of the page) are zeroed to keep
       // 0 * NaN out of O (their K scores are masked).
       const int past = kPage * id_of(blk_cur, blk_nxt, i) + kPage - (cl + a.C);
       if (past > 0) {
         for (int x = t; x < past * D; x += 64 * NW) {
-          const int r = x / past, key = kPage - past + x % past;
-          v_s0[r * kPage + 8 * vt_swz(r, key >> 3) + (key & 7)] = 0;
+          const int r = x / past, key = kPage - past + x % past;   // r: the d index
+          if constexpr (VTR) v_s0[r * kPage + 8 * vt_swz(r, key >> 3) + (key & 7)] = 0;
+          else v_s0[key * D + 8 * vr_swz<D>(key, r >> 3) + (r & 7)] = 0;
         }
         __syncthreads();
       }
     }
     qk_page(SA, k_s0);
-    fence_s(SA);
+    fence_s<CT>(SA);
     if (i >= n_main) {
       const int j = id_of(blk_cur, blk_nxt, i);
 #pragma unroll
-      for (int c = 0; c < 2; ++c) {
+      for (int c = 0; c < CT; ++c) {
         const int lim = qpos[c] - kPage * j - 8 * half;
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
@@ -714,10 +816,10 @@ __global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnA
         }
       }
     }
-    float alpha[2];
+    float alpha[CT];
     bool rb_any = false;
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
+    for (int c = 0; c < CT; ++c) {
       float mx = -INFINITY;
 #pragma unroll
       for (int k = 0; k < 16; ++k) mx = max3(mx, SA.s[c][0][k], SA.s[c][1][k]);
@@ -743,22 +845,22 @@ __global__ __launch_bounds__(64 * NW, 1) void paged_attention_kernel(const AttnA
         for (int x = 0; x < 8; ++x) PA.p[c][kk][x] = (__bf16)SA.s[c][kk / 2][8 * (kk % 2) + x];
     }
     if (__ballot(rb_any)) {
-      fence_o<NDT>(o);
+      fence_o<AG, CT, NDT>(o);
 #pragma unroll
-      for (int c = 0; c < 2; ++c)
+      for (int c = 0; c < CT; ++c)
 #pragma unroll
         for (int x = 0; x < NDT; ++x) o[c][x] *= alpha[c];
-      fence_o<NDT>(o);
+      fence_o<AG, CT, NDT>(o);
     }
-    fence_p(PA);
+    fence_p<CT>(PA);
     pv_page(PA, v_s0);
     __syncthreads();
   }
-  fence_o<NDT>(o);
+  fence_o<AG, CT, NDT>(o);
 
   // epilogue
 #pragma unroll
-  for (int c = 0; c < 2; ++c) {
+  for (int c = 0; c < CT; ++c) {
     const float l_tot = halves_sum(l_run[c]);
     const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
     const float lse_val = l_tot > 0.f ? (m_run[c] + log2f(l_tot)) * kLn2 : -INFINITY;
@@ -998,7 +1100,7 @@ __global__ __launch_bounds__(256) void xcd_split_kernel(const int32_t* __restric
 }
 
 int attn_rows_per_workgroup(int table_mode) {
-  return 64 * (table_mode == kTablesPerQTile ? kWavesQTile : kWavesGroup);
+  return 32 * kColTiles * (table_mode == kTablesPerQTile ? kWavesQTile : kWavesGroup);
 }
 
 int attn_query_tile(int group_size, int table_mode) {
@@ -1011,8 +1113,8 @@ int attn_base_workgroups(const Dims& d, int group_size, int table_mode) {
 }
 
 int attn_resident_workgroups(int table_mode) {
-  // one wave per SIMD: 4 waves per CU on 256 CUs
-  return 256 * 4 / (attn_rows_per_workgroup(table_mode) / 64);
+  // kWavesPerCu waves per CU on 256 CUs
+  return 256 * kWavesPerCu / (table_mode == kTablesPerQTile ? kWavesQTile : kWavesGroup);
 }
 
 size_t attn_ws_bytes(const Dims& d, int splits) {
@@ -1025,10 +1127,16 @@ size_t attn_xcd_ws_bytes(const Dims& d, int group_size) {
   return attn_ws_bytes(d, 2) + (size_t)d.B * (d.Hq / group_size) * sizeof(int32_t);
 }
 
-template <int D, int NW>
+template <int D, int NW, int VL>
 static void launch_kernel(const AttnArgs& a, bool dense, int nwg, hipStream_t st) {
-  if (dense) paged_attention_kernel<D, NW, true><<<nwg, 64 * NW, 0, st>>>(a);
-  else paged_attention_kernel<D, NW, false><<<nwg, 64 * NW, 0, st>>>(a);
+  if (dense) paged_attention_kernel<D, NW, kColTiles, true, VL><<<nwg, 64 * NW, 0, st>>>(a);
+  else paged_attention_kernel<D, NW, kColTiles, false, VL><<<nwg, 64 * NW, 0, st>>>(a);
+}
+
+template <int D, int NW>
+static void launch_layout(const AttnArgs& a, bool dense, int v_layout, int nwg, hipStream_t st) {
+  if (v_layout == kVTransposed) launch_kernel<D, NW, kVTransposed>(a, dense, nwg, st);
+  else launch_kernel<D, NW, kVTokenMajor>(a, dense, nwg, st);
 }
 
 hipError_t launch_attention(const Dims& d, const AttnLaunch& L, hipStream_t st) {
@@ -1072,11 +1180,11 @@ hipError_t launch_attention(const Dims& d, const AttnLaunch& L, hipStream_t st) 
   const int nwg = attn_base_workgroups(d, L.group_size, L.table_mode) * L.splits;
   const bool qtile = L.table_mode == kTablesPerQTile;
   if (d.D == 128) {
-    if (qtile) launch_kernel<128, kWavesQTile>(a, L.dense, nwg, st);
-    else launch_kernel<128, kWavesGroup>(a, L.dense, nwg, st);
+    if (qtile) launch_layout<128, kWavesQTile>(a, L.dense, L.v_layout, nwg, st);
+    else launch_layout<128, kWavesGroup>(a, L.dense, L.v_layout, nwg, st);
   } else {
-    if (qtile) launch_kernel<64, kWavesQTile>(a, L.dense, nwg, st);
-    else launch_kernel<64, kWavesGroup>(a, L.dense, nwg, st);
+    if (qtile) launch_layout<64, kWavesQTile>(a, L.dense, L.v_layout, nwg, st);
+    else launch_layout<64, kWavesGroup>(a, L.dense, L.v_layout, nwg, st);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || L.splits == 1) return e;

@@ -50,6 +50,10 @@ constexpr int kTablesPerGroup = 0;   // row b*G + g, entries translated by page_
 constexpr int kTablesPerQTile = 1;   // row (b*Hq + h)*n_qtiles + tile (block-sparse arm)
 constexpr int kTablesPacked = 2;     // per-group rows; page of entry p is p (copy arm)
 
+// V page layouts of the pool (ca_problem.v_layout).
+constexpr int kVTokenMajor = 0;   // [P, page, D], like the K pages
+constexpr int kVTransposed = 1;   // [P, D, page]
+
 // Attention over per-group tables (dense = identity tables, no table read).
 struct AttnLaunch {
   const uint16_t* q;
@@ -71,6 +75,7 @@ struct AttnLaunch {
   // splits == 2 with the cut of every table row chosen so that the 8 XCDs
   // carry equal loads (needs B * G % 8 == 0 and attn_xcd_ws_bytes of ws)
   bool xcd_balanced = false;
+  int v_layout = kVTokenMajor;
 };
 int attn_rows_per_workgroup(int table_mode);             // (head, query) rows per workgroup
 int attn_query_tile(int group_size, int table_mode);     // chunk queries per workgroup

@@ -180,9 +180,15 @@ __global__ __launch_bounds__(256) void expand_union_kernel(const uint64_t* __res
   if (t == 0) counts[r] = red[0] + red[1] + red[2] + red[3];
 }
 
+// The per-row words follow the group-row workspace at the next 8-byte boundary
+// (the group-row part ends with one int32 count per row).
+static size_t union_rows_offset(const Dims& d, int group_size) {
+  return (tables_ws_bytes(d, group_size) + 7) & ~(size_t)7;
+}
+
 size_t union_rows_ws_bytes(const Dims& d, int group_size) {
   const size_t R = (size_t)d.B * d.Hq * d.nqb;
-  return tables_ws_bytes(d, group_size) + R * d.W * sizeof(uint64_t) + R * sizeof(int32_t);
+  return union_rows_offset(d, group_size) + R * d.W * sizeof(uint64_t) + R * sizeof(int32_t);
 }
 
 hipError_t launch_union_rows(const Dims& d, const uint64_t* masks, const int32_t* cached_len,
@@ -194,7 +200,7 @@ hipError_t launch_union_rows(const Dims& d, const uint64_t* masks, const int32_t
   uint64_t* gwords = static_cast<uint64_t*>(ws);
   int32_t* gcounts = reinterpret_cast<int32_t*>(gwords + (size_t)RG * d.W);
   uint64_t* rwords = reinterpret_cast<uint64_t*>(
-      static_cast<char*>(ws) + tables_ws_bytes(d, group_size));
+      static_cast<char*>(ws) + union_rows_offset(d, group_size));
   int32_t* rcounts = reinterpret_cast<int32_t*>(rwords + (size_t)R * d.W);
   union_kernel<<<RG, 256, 0, st>>>(masks, cached_len, gwords, gcounts, d.Hq, d.nqb, d.W,
                                    group_size, G, d.C);

@@ -12,8 +12,9 @@ unions, no attention).  Everything it returns is a plain NumPy array:
   ``page_table[b, kvh, j]`` of ``k_pool`` / ``v_pool`` (``[P, page, D]``),
   which is the layout of the paper's zero-copy execution (Sec. 3.3, Fig. 4
   and App. B.2: one contiguous ``[block, D]`` region per
-  (batch, KV head, block) triple); the GPU library takes V pages
-  transposed (``v_pages_transposed``: ``[P, D, page]``);
+  (batch, KV head, block) triple); the GPU library reads V pages in this
+  layout by default, or transposed (``v_pages_transposed``: ``[P, D, page]``)
+  when a caller selects that layout;
 * physical page ids are a seeded permutation of all (b, kvh, j) triples, so
   the pool holds exactly the pages the workload needs.
 

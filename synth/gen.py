@@ -201,12 +201,13 @@ BF16_QNAN = np.uint16(0x7FC0)
 
 
 def v_pages_transposed(v_pool: np.ndarray) -> np.ndarray:
-    """The V pool in the GPU library's page layout: every page transposed to
-    ``[D, page]`` (head dimension major, tokens contiguous), the same values.
+    """The V pool with every page transposed to ``[D, page]`` (head dimension
+    major, tokens contiguous), the same values: the library's optional
+    transposed V layout.
 
-    The seeded V data and the oracle use token-major pages ``[page, D]``;
-    the attention kernel reads V^T pages (one 16-byte LDS read per operand
-    fragment), so GPU callers hand over this copy."""
+    The seeded V data and the oracle use token-major pages ``[page, D]``, the
+    paper's layout and the library's default; a caller that selects the
+    transposed layout hands over this copy."""
     return np.ascontiguousarray(v_pool.transpose(0, 2, 1))
 
 

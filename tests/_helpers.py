@@ -34,9 +34,13 @@ def bf16_host_f64(t: torch.Tensor) -> np.ndarray:
     return oracle.bf16_to_f64(t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16))
 
 
-def device_inputs(d: dict) -> dict:
-    return dict(q=bf16_dev(d["q"]), k=bf16_dev(d["k_pool"]),
-                v=bf16_dev(synth.v_pages_transposed(d["v_pool"])),
+V_TOKEN_MAJOR, V_TRANSPOSED = 0, 1   # ca_problem.v_layout
+
+
+def device_inputs(d: dict, v_layout: int = V_TOKEN_MAJOR) -> dict:
+    """Q, K pool, V pool (token-major pages, or transposed ones) and page table on the GPU."""
+    v = d["v_pool"] if v_layout == V_TOKEN_MAJOR else synth.v_pages_transposed(d["v_pool"])
+    return dict(q=bf16_dev(d["q"]), k=bf16_dev(d["k_pool"]), v=bf16_dev(v),
                 pt=i32_dev(d["page_table"]))
 
 
@@ -73,6 +77,28 @@ def sample_rows(B, Hq, C, seed=0, heads_per_b=4, n_random=16):
         for h in heads:
             ts = sorted(set(fixed + rng.choice(C, size=n_random, replace=False).tolist()))
             rows += [(b, h, t) for t in ts]
+    return rows
+
+
+def tile_rows(B, Hq, C, group_size, seed=0, rows_per_tile=256, per_tile=2):
+    """(b, h, t) rows covering every (sequence, execution group, query tile) of
+    the attention kernel: a workgroup runs rows_per_tile (head, query) rows,
+    i.e. rows_per_tile / group_size queries of every head of its group.  Each
+    tile contributes per_tile queries (one on a tile edge, alternately the first
+    and the last query, the others at random) on one head of the group, the
+    head rotating from tile to tile so that every head of every group appears."""
+    rng = np.random.default_rng(seed)
+    qt = rows_per_tile // group_size
+    rows = []
+    for b in range(B):
+        for g in range(Hq // group_size):
+            for t in range(-(-C // qt)):
+                h = g * group_size + (t + b + g) % group_size
+                lo, hi = t * qt, min((t + 1) * qt, C)
+                ts = {lo if t % 2 == 0 else hi - 1}
+                while len(ts) < min(per_tile, hi - lo):
+                    ts.add(int(rng.integers(lo, hi)))
+                rows += [(b, h, x) for x in sorted(ts)]
     return rows
 
 

@@ -211,3 +211,62 @@ def test_unaligned_tensors_rejected(lib):
     ws = lib.ca_attention_workspace_bytes(p.ref, 4, 2)
     assert st(lib.ca_chunk_attention(p.ref, fake, fake, fake, fake, fake, fake, 4, 0.1, 2, fake,
                                      None, odd, ws, None)) == "CA_ERR_WORKSPACE"
+
+
+def test_sm_scale_rejected(lib):
+    """A zero, negative or non-finite softmax scale is rejected on the host by
+    every attention entry point (it would turn masked scores into NaN / +inf
+    weights); fake device pointers, never dereferenced."""
+    fake = ctypes.c_void_p(0x1000)
+    p = _prob()
+    p.c.cached_len = fake.value
+    st = lambda s: lib.ca_status_string(s).decode()
+    for sm in (0.0, -0.125, float("nan"), float("inf"), -float("inf")):
+        assert st(lib.ca_chunk_attention(p.ref, fake, fake, fake, fake, fake, fake, 4, sm, 1,
+                                         fake, None, None, 0, None)) == "CA_ERR_SHAPE", sm
+        assert st(lib.ca_dense_paged_chunk_attention(p.ref, fake, fake, fake, fake, sm, 1, fake,
+                                                     None, None, 0, None)) == "CA_ERR_SHAPE", sm
+        assert st(lib.ca_block_sparse_chunk_attention(p.ref, fake, fake, fake, fake, fake, fake,
+                                                      sm, 1, fake, None, None, 0,
+                                                      None)) == "CA_ERR_SHAPE", sm
+        assert st(lib.ca_packed_chunk_attention(p.ref, fake, fake, fake, fake, fake, 4, sm, 1, 10,
+                                                fake, None, None, 0, None)) == "CA_ERR_SHAPE", sm
+    assert lib.ca_last_error_detail().decode().startswith("sm_scale")
+
+
+def test_tables_workspace_alignment(lib):
+    """The table builders keep uint64 union words in their workspace: a
+    workspace that is not 8-byte aligned is rejected before any launch."""
+    fake = ctypes.c_void_p(0x1000)
+    odd = ctypes.c_void_p(0x1004)
+    p = _prob()
+    p.c.cached_len = fake.value
+    st = lambda s: lib.ca_status_string(s).decode()
+    need = lib.ca_tables_workspace_bytes(p.ref, 4)
+    assert st(lib.ca_build_block_tables(p.ref, fake, 4, fake, fake, odd, need, None)) == \
+        "CA_ERR_WORKSPACE"
+    for gs in (0, 4):
+        need = lib.ca_block_sparse_tables_workspace_bytes(p.ref, gs)
+        assert st(lib.ca_build_block_sparse_tables(p.ref, fake, gs, fake, fake, odd, need,
+                                                   None)) == "CA_ERR_WORKSPACE"
+
+
+def test_v_layout_field(lib):
+    """ca_problem.v_layout: 0 (token-major, the default) and 1 (transposed) are
+    accepted, anything else is CA_ERR_SHAPE."""
+    assert _status(_prob()) == 0
+    assert _status(_prob(v_layout=ca.V_TRANSPOSED)) == 0
+    for bad in (2, -1):
+        s = _status(_prob(v_layout=bad))
+        assert lib.ca_status_string(s).decode() == "CA_ERR_SHAPE"
+        assert "v_layout" in lib.ca_last_error_detail().decode()
+
+
+def test_block_sparse_workspace_one_group_row(lib):
+    """One group row (B = 1, a single group of 4 heads): its words and count take
+    12 bytes, so the per-(head, Q-block) words start at the next 8-byte boundary."""
+    tiny = _prob(num_q_heads=4, num_kv_heads=1, head_dim=64, q_block=64, chunk_len=256,
+                 max_kv_blocks=20, cached_len=[1024])
+    assert ca.tables_workspace_bytes(tiny, 4) == 1 * 8 + 1 * 4
+    rows = 4 * 4                         # heads x Q-blocks, one word each
+    assert ca.block_sparse_tables_workspace_bytes(tiny, 4) == 16 + rows * 8 + rows * 4

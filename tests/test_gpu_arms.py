@@ -46,13 +46,16 @@ def _bs_csr(bits, w):
     return np.array(indptr, dtype=np.int32), np.array(indices, dtype=np.int32)
 
 
-@pytest.mark.parametrize("name", ["tiny_gqa_1k", "llama8b_32k", "batched_ragged_4seq",
-                                  "tiny_unaligned", "llama8b_unaligned"])
-def test_copy_arm_gather_and_bitexact(name, workload_inputs, oracle_estimate):
+@pytest.mark.parametrize("name,v_layout", [("tiny_gqa_1k", 0), ("llama8b_32k", 0),
+                                           ("batched_ragged_4seq", 0), ("tiny_unaligned", 0),
+                                           ("llama8b_unaligned", 0), ("tiny_unaligned", 1),
+                                           ("llama8b_32k", 1)])
+def test_copy_arm_gather_and_bitexact(name, v_layout, workload_inputs, oracle_estimate):
+    """v_layout 0: token-major V pages, 1: transposed (the packed V pool keeps it)."""
     d = workload_inputs(name)
     w = d["workload"]
-    p = ca.Problem.from_workload(w)
-    x = device_inputs(d)
+    p = ca.Problem.from_workload(w, v_layout=v_layout)
+    x = device_inputs(d, v_layout)
     masks = d["masks"] if name == "tiny_gqa_1k" else oracle_estimate(name)[0]
     ip, ix = _csr(masks, w)
     tabs = (i32_dev(ip), i32_dev(ix))
@@ -71,7 +74,10 @@ def test_copy_arm_gather_and_bitexact(name, workload_inputs, oracle_estimate):
     vh = vp[torch.as_tensor(pick, device="cuda")].view(torch.int16).cpu().numpy()
     # bit patterns (NaN rows past a sequence end are copied as they are)
     assert np.array_equal(kh.view(np.uint16), d["k_pool"][src[pick]])
-    assert np.array_equal(vh.view(np.uint16), synth.v_pages_transposed(d["v_pool"][src[pick]]))
+    v_want = d["v_pool"][src[pick]]
+    if v_layout == 1:
+        v_want = synth.v_pages_transposed(v_want)
+    assert np.array_equal(vh.view(np.uint16), v_want)
     for splits in (1, 0):
         lse_z = torch.empty((p.batch, p.num_q_heads, p.chunk_len), dtype=torch.float32,
                             device="cuda")
@@ -100,12 +106,15 @@ def _union_rows_csr(masks, w):
     return np.array(indptr, dtype=np.int32), np.array(indices, dtype=np.int32), T
 
 
-@pytest.mark.parametrize("name", ["llama8b_32k", "batched_ragged_4seq", "llama8b_unaligned"])
+@pytest.mark.parametrize("name", ["llama8b_32k", "batched_ragged_4seq", "llama8b_unaligned",
+                                  "tiny_gqa_1k"])
 def test_block_sparse_tables_bitexact(name, workload_inputs, oracle_estimate):
+    """tiny_gqa_1k has a single group row (B = 1, one group of 4 heads): the
+    per-row words then start at an 8-byte boundary past an odd count array."""
     d = workload_inputs(name)
     w = d["workload"]
     p = ca.Problem.from_workload(w)
-    masks, _ = oracle_estimate(name)
+    masks = d["masks"] if w.mask_kind == "bernoulli" else oracle_estimate(name)[0]
     ip, ix = ca.build_block_sparse_tables(p, u64_dev(masks))          # raw mask rows
     torch.cuda.synchronize()
     rip, rix = _bs_csr(oracle.unpack_masks(masks), w)

@@ -109,7 +109,8 @@ def attention_asm(tmp_path_factory):
 
 def test_mfma_results_wait_before_use(attention_asm):
     kernels = list(_kernels(attention_asm))
-    assert len(kernels) == 8   # D in {64, 128} x waves in {2, 4} x {selected, dense}
+    # D in {64, 128} x waves in {2, 4} x {selected, dense} x V layout in {token-major, transposed}
+    assert len(kernels) == 16
     for name, lines, labels in kernels:
         n_mfma = 0
         for k, t in enumerate(lines):
@@ -128,7 +129,7 @@ def test_checker_flags_a_missing_fence(tmp_path):
     if not os.path.exists(HIPCC):
         pytest.skip("hipcc not available")
     src = open(SRC).read()
-    fenced = "    qk_page(SA, k_s0);\n    fence_s(SA);\n"
+    fenced = "    qk_page(SA, k_s0);\n    fence_s<CT>(SA);\n"
     assert src.count(fenced) == 1
     bad = tmp_path / "attention.hip"
     bad.write_text(src.replace(fenced, "    qk_page(SA, k_s0);\n"))
@@ -143,4 +144,4 @@ def test_checker_flags_a_missing_fence(tmp_path):
     flagged = {name for name, lines, labels in _kernels(out.read_text())
                for k, t in enumerate(lines) if t.startswith("v_mfma")
                and _shortest_use(lines, labels, k) is not None}
-    assert len(flagged) == 8, flagged
+    assert len(flagged) == 16, flagged

@@ -568,3 +568,56 @@ def test_threshold_kept_blocks_are_the_alpha_heavy_softmax_blocks():
         want = set(np.nonzero((ratio >= alpha) & clear)[0].tolist())
         assert {j for j in kept if clear[j]} == want
         assert 0 < len(want) < 500
+
+
+def _bits(word) -> set:
+    w = int(word)
+    return {j for j in range(64) if (w >> j) & 1}
+
+
+def test_threshold_masks_hand_built_case():
+    """masks_from_threshold on hand-picked float32 scores (10 cached blocks, a
+    128-token chunk of two 64-query Q-blocks, margin -0.75, one sink block, a
+    2-block local window); the kept blocks and the forced bits worked out by
+    hand: the kept set is {j : s_j >= max + margin} (ties at the cut and at the
+    maximum kept, -0.0 equal to +0.0), then the sink {0}, the local window
+    {8, 9} and the chunk-causal blocks {10} (Q-block 0) or {10, 11} (Q-block 1)."""
+    f = lambda *v: np.array(v, dtype=np.float32)
+    s = np.zeros((2, 2, 10), dtype=np.float32)
+    s[0, 0] = f(0, 1, 5, 2, 4.5, 0, 3, 5, 1, 0)                 # max 5, cut 4.25
+    s[0, 1] = f(-1, -0.5, -0.5, -4, -1.25, -2, -3, -1.5, -9, -1.0)   # cut -1.25, kept exactly
+    s[1, 0] = np.full(10, 7.0, dtype=np.float32)                  # all tie at the maximum
+    s[1, 1] = f(-0.0, 0.0, -5, -5, -5, -5, -5, -5, -5, -5)        # signed zeros at the maximum
+    masks = oracle.masks_from_threshold([s], [640], 128, 64, 64, 1, np.float32(-0.75),
+                                        sink_blocks=1, local_blocks=2)
+    assert masks.shape == (1, 2, 2, 1)
+    want = {(0, 0): {0, 2, 4, 7, 8, 9, 10},
+            (0, 1): {0, 1, 2, 4, 8, 9, 10, 11},
+            (1, 0): set(range(11)),
+            (1, 1): {0, 1, 8, 9, 10, 11}}
+    for (h, i), bits in want.items():
+        assert _bits(masks[0, h, i, 0]) == bits, (h, i)
+
+
+def test_threshold_masks_hand_built_unaligned():
+    """Three sequences with a 100-token chunk (Q-block 1 holds 36 queries):
+    340 cached tokens (5 full cached blocks; block 5 holds the last 20 cached
+    and the first 44 chunk tokens, so it is a chunk block, never a candidate),
+    an empty cache, and 63 cached tokens (no full cached block; block 0 is
+    shared).  Local window 3, sink 1, margin -0.75; every bit by hand."""
+    f = lambda *v: np.array(v, dtype=np.float32)
+    s0 = np.stack([f(1, 2, 3, 2.5, 0), f(9, 0, 0, 0, 0)])[None]  # [Hq=1, nQB=2, nC=5]
+    empty = np.zeros((1, 2, 0), dtype=np.float32)
+    masks = oracle.masks_from_threshold([s0, empty, empty], [340, 0, 63], 100, 64, 64, 1,
+                                        np.float32(-0.75), sink_blocks=1, local_blocks=3)
+    assert masks.shape == (3, 1, 2, 1)
+    # b = 0: kept {2, 3} / {0}; sink {0}; local {2, 3, 4}; chunk blocks 5, 6 for both
+    # Q-blocks (positions 340..403 and 404..439 end in block 6)
+    assert _bits(masks[0, 0, 0, 0]) == {0, 2, 3, 4, 5, 6}
+    assert _bits(masks[0, 0, 1, 0]) == {0, 2, 3, 4, 5, 6}
+    # b = 1: no cache: Q-block 0 (positions 0..63) sees block 0, Q-block 1 (64..99) 0..1
+    assert _bits(masks[1, 0, 0, 0]) == {0}
+    assert _bits(masks[1, 0, 1, 0]) == {0, 1}
+    # b = 2: 63 cached tokens: positions 63..126 -> blocks 0..1, 127..162 -> 0..2
+    assert _bits(masks[2, 0, 0, 0]) == {0, 1}
+    assert _bits(masks[2, 0, 1, 0]) == {0, 1, 2}
