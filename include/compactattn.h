@@ -211,6 +211,25 @@ ca_status ca_build_block_tables(const ca_problem* p, const uint64_t* masks,
                                 int32_t* kv_indices, void* ws, size_t ws_bytes,
                                 void* stream);
 
+/* 2a. Allocation-free ca_build_block_tables, for callers that cannot allocate
+ *    device memory (code under HIP graph capture, tight serving loops,
+ *    harnesses that forbid hipMalloc): the same kernels and the same tables,
+ *    bit for bit, with the union words and row counts in a scratch array of
+ *    CA_NOALLOC_SCRATCH_BYTES that the library holds on every GPU it runs on
+ *    until the process ends (looked up on the first call on each device, with
+ *    that device current; the stream must belong to the current device).  The
+ *    call allocates nothing.  It needs ca_tables_workspace_bytes(p, group_size)
+ *    <= CA_NOALLOC_SCRATCH_BYTES (B * G rows of ceil(max_kv_blocks / 64) 8-byte
+ *    words + one int32 count each: 511 rows at max_kv_blocks = 16384), else
+ *    CA_ERR_WORKSPACE before any launch.  Every call on one GPU uses that GPU's
+ *    one scratch array: calls that overlap on one GPU (different streams or
+ *    host threads without ordering) race and must not be issued. */
+#define CA_NOALLOC_SCRATCH_BYTES (1u << 20)
+
+ca_status ca_build_block_tables_noalloc(const ca_problem* p, const uint64_t* masks,
+                                        int32_t group_size, int32_t* kv_indptr,
+                                        int32_t* kv_indices, void* stream);
+
 /* 2b. Fused estimator-to-union (Sec. 3.2: the selected blocks of every head
  *    and Q-block of a group only matter through their union): the four
  *    estimator stages of ca_estimate_masks, except that each selection row

@@ -28,6 +28,7 @@ EXPORTED = (
     "ca_block_sparse_tables_workspace_bytes", "ca_build_block_sparse_tables",
     "ca_block_sparse_chunk_attention", "ca_gather_selected_pages", "ca_packed_chunk_attention",
     "ca_select_blocks_threshold", "ca_estimate_masks_threshold", "ca_estimate_tables",
+    "ca_build_block_tables_noalloc",
 )
 
 
@@ -89,6 +90,7 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
         "ca_estimate_masks": ([P, vp, vp, vp, f32, i32, i32, i32, vp, vp, vp, vp, vp], ctypes.c_int),
         "ca_tables_workspace_bytes": ([P, i32], sz),
         "ca_build_block_tables": ([P, vp, i32, vp, vp, vp, sz, vp], ctypes.c_int),
+        "ca_build_block_tables_noalloc": ([P, vp, i32, vp, vp, vp], ctypes.c_int),
         "ca_attention_workspace_bytes": ([P, i32, i32], sz),
         "ca_chunk_attention": ([P, vp, vp, vp, vp, vp, vp, i32, f32, i32, vp, vp, vp, sz, vp],
                                ctypes.c_int),
@@ -329,6 +331,20 @@ def build_block_tables(p: Problem, masks: torch.Tensor, group_size: int,
     _check(load().ca_build_block_tables(p.ref, _ptr(masks), group_size, _ptr(out[0]),
                                         _ptr(out[1]), _ptr(ws), ws.numel() * ws.element_size(),
                                         _stream(stream)))
+    return out
+
+
+def build_block_tables_noalloc(p: Problem, masks: torch.Tensor, group_size: int,
+                               out: Optional[Tuple[torch.Tensor, torch.Tensor]] = None,
+                               stream=None):
+    """build_block_tables without a workspace (the library's fixed scratch); the
+    caller still owns the output tables (allocated here when ``out`` is None)."""
+    R = p.batch * p.n_groups(group_size)
+    if out is None:
+        out = (torch.empty(R + 1, dtype=torch.int32, device=masks.device),
+               torch.empty(R * p.max_kv_blocks, dtype=torch.int32, device=masks.device))
+    _check(load().ca_build_block_tables_noalloc(p.ref, _ptr(masks), group_size, _ptr(out[0]),
+                                                _ptr(out[1]), _stream(stream)))
     return out
 
 

@@ -5,6 +5,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -215,6 +216,42 @@ ca_status run_attention(const ca_problem* p, const uint16_t* q, const uint16_t* 
   L.v_layout = p->v_layout == CA_V_TRANSPOSED ? ca::kVTransposed : ca::kVTokenMajor;
   return hip_status(ca::launch_attention(d, L, static_cast<hipStream_t>(stream)),
                     dense ? "dense paged attention launch" : "chunk attention launch");
+}
+
+}  // namespace
+
+// Scratch of the allocation-free table builder: the union words and row counts
+// that ca_build_block_tables keeps in the caller's workspace.  Every GPU the
+// library runs on holds its own copy until the process ends; host code never
+// uses this name as an address, only the pointer hipGetSymbolAddress returns
+// for the current device.
+static __device__ __align__(256) uint64_t scratch[CA_NOALLOC_SCRATCH_BYTES / sizeof(uint64_t)];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];   // device address of `scratch`, per device
+
+// Device address of the current device's scratch, looked up once per device
+// (with that device current) on the first call.
+ca_status scratch_ptr(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_status(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(CA_ERR_UNSUPPORTED, "device %d: the scratch table holds %d devices", dev,
+                kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_status(e, "hipGetSymbolAddress(scratch)");
+    if (ptr == nullptr) return fail(CA_ERR_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return CA_OK;
 }
 
 }  // namespace
@@ -454,6 +491,31 @@ ca_status ca_build_block_tables(const ca_problem* p, const uint64_t* masks, int3
   return hip_status(ca::launch_tables(d, masks, p->cached_len, group_size, kv_indptr,
                                       kv_indices, ws, static_cast<hipStream_t>(stream)),
                     "tables launch");
+}
+
+ca_status ca_build_block_tables_noalloc(const ca_problem* p, const uint64_t* masks,
+                                        int32_t group_size, int32_t* kv_indptr,
+                                        int32_t* kv_indices, void* stream) {
+  ca::Dims d;
+  if (group_size < 1) return fail(CA_ERR_GROUP, "group_size must be >= 1");
+  ca_status s = check(p, group_size, &d);
+  if (s != CA_OK) return s;
+  if ((s = need_device(p)) != CA_OK) return s;
+  if (!masks || !kv_indptr || !kv_indices)
+    return fail(CA_ERR_NULL, "masks, kv_indptr and kv_indices are required");
+  const size_t need = ca::tables_ws_bytes(d, group_size);
+  if (need > CA_NOALLOC_SCRATCH_BYTES)
+    return fail(CA_ERR_WORKSPACE,
+                "the tables need %zu scratch bytes (B * G rows x (W words + 1 count)), more than "
+                "the %zu bytes of the allocation-free entry point: use ca_build_block_tables",
+                need, (size_t)CA_NOALLOC_SCRATCH_BYTES);
+  void* ws = nullptr;
+  if ((s = scratch_ptr(&ws)) != CA_OK) return s;
+  // union_kernel writes every word and count that compact_kernel reads, so the
+  // previous call's contents need no clearing
+  return hip_status(ca::launch_tables(d, masks, p->cached_len, group_size, kv_indptr,
+                                      kv_indices, ws, static_cast<hipStream_t>(stream)),
+                    "tables launch (allocation-free)");
 }
 
 size_t ca_attention_workspace_bytes(const ca_problem* p, int32_t group_size, int32_t num_splits) {

@@ -270,3 +270,23 @@ def test_block_sparse_workspace_one_group_row(lib):
     assert ca.tables_workspace_bytes(tiny, 4) == 1 * 8 + 1 * 4
     rows = 4 * 4                         # heads x Q-blocks, one word each
     assert ca.block_sparse_tables_workspace_bytes(tiny, 4) == 16 + rows * 8 + rows * 4
+
+
+def test_noalloc_tables_size_limit(lib):
+    """The allocation-free table builder rejects, on the host and before any HIP
+    call, a problem whose union words and counts exceed its fixed scratch
+    (CA_NOALLOC_SCRATCH_BYTES); 512 group rows of 256 words need 1050624 bytes."""
+    m = re.search(r"#define CA_NOALLOC_SCRATCH_BYTES \(1u << (\d+)\)", open(HEADER).read())
+    limit = 1 << int(m.group(1))
+    fake = ctypes.c_void_p(0x1000)
+    big = _prob(batch=64, cached_len=[16384 * 64 - 2048] * 64, max_kv_blocks=16384)
+    big.c.cached_len = fake.value
+    assert ca.tables_workspace_bytes(big, 4) == 512 * (256 * 8 + 4) > limit
+    s = lib.ca_build_block_tables_noalloc(big.ref, fake, 4, fake, fake, None)
+    assert lib.ca_status_string(s).decode() == "CA_ERR_WORKSPACE"
+    assert "scratch" in lib.ca_last_error_detail().decode()
+    p = _prob()
+    p.c.cached_len = fake.value
+    st = lambda s: lib.ca_status_string(s).decode()
+    assert st(lib.ca_build_block_tables_noalloc(p.ref, fake, 3, fake, fake, None)) == "CA_ERR_GROUP"
+    assert st(lib.ca_build_block_tables_noalloc(p.ref, None, 4, fake, fake, None)) == "CA_ERR_NULL"
