@@ -2,28 +2,28 @@
 // App. B.2), bf16 MFMA with fp32 online softmax, and the split-KV
 // log-sum-exp combine.
 //
-// Work decomposition: one workgroup = NW wavefronts; a wave owns 32*CT
-// (head, query) rows, CT 32-column MFMA tiles:
+// Work decomposition: one workgroup = NW wavefronts, 16*NCT (head, query)
+// rows per wave: NCT = 2 runs two waves per SIMD (256 registers each), NCT = 4
+// one wave per SIMD (512 registers):
 //   * a table row r = b*G + g serves the group_size query heads of group g;
 //     all of them read the same KV pages, so a workgroup packs rows of every
-//     head of the group (group_size heads x 32*CT*NW/group_size chunk
+//     head of the group (group_size heads x 16*NCT*NW/group_size chunk
 //     queries) and each KV page staged in LDS feeds all of them;
-//   * the kernels run CT = 2: one wave per SIMD holding up to 512 registers
-//     (the O^T accumulators and Q^T fragments in AGPRs), and every K and V
-//     fragment a wave reads from LDS feeds two v_mfma_f32_32x32x16_bf16 (one
-//     per column tile), half the LDS traffic per flop of a 32-column wave.
-//     CT = 1 (two waves per SIMD, 32 columns and at most 256 registers each,
-//     all VGPRs) also compiles: it keeps the matrix cores busier per cycle,
-//     but doubles the LDS reads and per-page scalar work per flop, and on
-//     MI355X it ran at a lower clock, for no gain in time;
-//   * S^T = K Q^T (keys x queries): every lane holds one query column, so
-//     the softmax statistics are in-lane plus one v_permlane32_swap; then
-//     O^T += V^T P^T.  Lanes read the K rows in an order (key_of_row) that
-//     gives every lane 8 consecutive keys of its P^T fragment, so the
-//     matching V^T fragment is one 16-byte read of a transposed V page
-//     ([D, 64], VL = kVTransposed) or two gfx950 transpose reads
-//     (ds_read_b64_tr_b16) of a token-major page ([64, D], the paper's
-//     layout, VL = kVTokenMajor);
+//   * the contractions are v_mfma_f32_16x16x32_bf16: a wave's rows are NCT
+//     16-column tiles and a page's 64 keys four 16-key tiles, so every K and
+//     V fragment a wave reads from LDS feeds NCT MFMAs.  On MI355X this kernel
+//     runs at the board's power limit, and the 16x16x32 form moves half the
+//     accumulator data per flop of the 32x32x16 form: the same flops then
+//     cost less energy and the clock stays higher;
+//   * S^T = K Q^T (keys x queries): a lane holds one query column of each of
+//     its NCT column tiles and 4 keys of each 16-key tile; the softmax
+//     statistics are in-lane plus a reduction over the 4 lane groups
+//     (v_permlane16_swap, v_permlane32_swap); then O^T += V^T P^T.  Lanes read
+//     the K rows of a page in an order (key_of) that gives every lane 8
+//     consecutive keys of each 32-key P^T fragment, so the matching V^T
+//     fragment is one 16-byte read of a transposed V page ([D, 64],
+//     VL = kVTransposed) or two gfx950 transpose reads (ds_read_b64_tr_b16)
+//     of a token-major page ([64, D], the paper's layout, VL = kVTokenMajor);
 //   * pages go from HBM into LDS with 16-byte direct-to-LDS buffer loads (no
 //     register round trip) into XOR-swizzled tiles (conflict-free operand
 //     reads);
@@ -47,12 +47,16 @@
 
 namespace ca {
 
-// Per-group tables: 4 waves of 64 columns (one wave per SIMD).  Block-sparse
-// tiles (one head x 128 queries): 2 waves of 64 columns, two workgroups per CU.
-constexpr int kWavesGroup = 4;
-constexpr int kWavesQTile = 2;
-constexpr int kColTiles = 2;     // 32-column MFMA tiles per wave
-constexpr int kWavesPerCu = 4;   // resident waves per CU (1 per SIMD)
+#ifndef CA_COL_TILES
+#define CA_COL_TILES 2
+#endif
+// 16-column MFMA tiles per wave: 4 (one wave per SIMD, 512 registers) or 2
+// (two waves per SIMD, 256 registers each).  Per-group tables: 256 rows per
+// workgroup; block-sparse tiles (one head x 128 queries): 128 rows.
+constexpr int kColTiles = CA_COL_TILES;
+constexpr int kWavesGroup = 16 / kColTiles;
+constexpr int kWavesQTile = 8 / kColTiles;
+constexpr int kWavesPerCu = 16 / kColTiles;   // resident waves per CU
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -87,41 +91,46 @@ constexpr int kTileK = 0;
 constexpr int kTileVT = 1;   // transposed V page
 constexpr int kTileVR = 2;   // token-major V page
 
+// Key that row r (0..15) of 16-key tile kt (0..3) of a page stands for in the
+// QK contraction: 32*(kt/2) + 8*(r/4) + 4*(kt%2) + r%4.  The 16x16 result
+// gives lane group g (lanes 16g .. 16g+15) rows 4g .. 4g+3 of every tile, so
+// with this order the lane holds keys 32p + 8g .. 32p + 8g + 7 of each 32-key
+// step p (tiles 2p and 2p+1): the 8 consecutive keys that its P^T fragment of
+// that step covers.
+__host__ __device__ constexpr int key_of(int kt, int r) {
+  return 32 * (kt >> 1) + 8 * (r >> 2) + 4 * (kt & 1) + (r & 3);
+}
+
 // Swizzled position (16-byte chunk) of chunk c of row r in an LDS page tile.
 // gfx950 LDS has 64 banks of 4 bytes; a 16-byte read is served 16 lanes per
 // cycle and an 8-byte read 32 lanes per cycle.
-// K tiles are read 16 bytes per lane by 16 rows at one chunk: the 16 rows
-// must land on 16 different 16-byte bank slots of the 256-byte bank window
-// (a D = 64 row is half a window, so rows pair up).
-// Transposed V tiles (128-byte rows, two per window) are read the same way.
-// Token-major V tiles are read 8 bytes per lane by the transpose read, 32
-// lanes covering 4 consecutive rows x 64 bytes: each row's aligned group of
-// 4 chunks must move to a different aligned group of the window.
-// Every swizzle leaves a row's pattern unchanged under +32 rows (K also under
-// +8 and +16, token-major V under +4 and +16), so the operand reads of one
-// lane differ only by immediate offsets.
+// K tiles are read 16 bytes per lane by the 16 keys key_of(kt, 0..15) at one
+// chunk: bits 0, 1, 3, 4 of those keys differ, so XOR-ing them into the chunk
+// puts the 16 reads on 16 different 16-byte bank slots (D = 64: a row is half
+// a 256-byte bank window, rows pair up by bit 0, and bits 1, 3, 4 pick the
+// chunk).  Transposed V tiles (128-byte rows, two per window) are read 16
+// bytes per lane by 16 consecutive d rows at one chunk.  Token-major V tiles
+// are read 8 bytes per lane by the transpose read: 32 lanes cover keys
+// {0..3, 8..11} (+ multiples of 4 and 16) x 32 bytes, so bits 0, 1, 3 of the
+// key pick the 32-byte pair of chunks (D = 64: bit 0 picks the half window,
+// bits 1 and 3 the pair).  None of the swizzles depends on key bits 2 or 5, so
+// a lane's operand reads of the four key tiles differ only by immediates.
 template <int D>
 __device__ __forceinline__ int k_swz(int r, int c) {
-  return D == 128 ? (c ^ (r & 15)) : (c ^ ((r >> 1) & 7));
+  return D == 128 ? (c ^ ((r & 3) | (((r >> 3) & 3) << 2)))
+                  : (c ^ (((r >> 1) & 1) | (((r >> 3) & 3) << 1)));
 }
 __device__ __forceinline__ int vt_swz(int r, int c) { return c ^ ((r >> 1) & 7); }
 template <int D>
 __device__ __forceinline__ int vr_swz(int r, int c) {
-  return D == 128 ? (c ^ ((r & 3) << 2)) : (c ^ (((r >> 1) & 1) << 2));
+  return D == 128 ? (c ^ (((r & 3) | (((r >> 3) & 1) << 2)) << 1))
+                  : (c ^ ((((r >> 1) & 1) | (((r >> 3) & 1) << 1)) << 1));
 }
 template <int D, int TILE>
 __device__ __forceinline__ int tile_swz(int r, int c) {
   if constexpr (TILE == kTileVT) return vt_swz(r, c);
   else if constexpr (TILE == kTileVR) return vr_swz<D>(r, c);
   else return k_swz<D>(r, c);
-}
-
-// Key row that lane column `col` reads from a K tile: bits 2 and 3 of the
-// key index swapped.  With it the S^T accumulator rows that one lane packs
-// into a P^T fragment are 8 consecutive keys, so the matching V^T fragment
-// is one contiguous run of keys.
-__device__ __forceinline__ int key_of_row(int r) {
-  return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);
 }
 
 // 2^x with a single v_exp_f32 (results below the normal range flush to 0,
@@ -204,102 +213,118 @@ __device__ __forceinline__ float max3(float a, float b, float c) {
 // exponent base is only moved when a new score exceeds it by more than this,
 // so the weights stay <= 2^kRescaleSlack and most pages skip the O rescale.
 constexpr float kRescaleSlack = 8.0f;
+// Exponent base before the first page: finite and below any score, so the
+// first page with a finite score always moves it (its alpha exp2(kNoBase - m)
+// is 0, which clears the empty O and row sum), and no -inf test is needed.
+// A row that never sees a finite score keeps it with a zero row sum.
+constexpr float kNoBase = -1.0e30f;
 
-// max / sum of a value and its partner in the other half of the wave
-// (lanes l and l^32 hold the same query column).
-__device__ __forceinline__ float halves_max(float x) {
-  const uint32_t u = __float_as_uint(x);
-  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+// max / sum over the 4 lane groups (lanes l, l^16, l^32, l^48 hold the same
+// query column): rows 0<->1 and 2<->3 swap (v_permlane16_swap), then rows
+// {0,1}<->{2,3} (v_permlane32_swap); each swap hands both values back.
+__device__ __forceinline__ float max2(float a, float b) {
+  return __builtin_elementwise_maximum(a, b);   // v_maximum_f32: no quieting of the inputs
 }
-__device__ __forceinline__ float halves_sum(float x) {
-  const uint32_t u = __float_as_uint(x);
-  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+__device__ __forceinline__ float groups_max(float x) {
+  uint32_t u = __float_as_uint(x);
+  auto r = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  u = __float_as_uint(max2(__uint_as_float(r[0]), __uint_as_float(r[1])));
+  r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return max2(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float groups_sum(float x) {
+  uint32_t u = __float_as_uint(x);
+  auto r = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  u = __float_as_uint(__uint_as_float(r[0]) + __uint_as_float(r[1]));
+  r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// S^T tiles of one page for the wave's column tiles: s[c][h] holds keys
-// 32h .. 32h+31 of column tile c; accumulator slot v of lane half hf is row
-// 8*(v/4) + 4*hf + v%4 of the tile, i.e. key
-// 32h + 16*(v/8) + 8*hf + 4*((v/4)%2) + v%4 (key_of_row).
-template <int CT>
+// S^T of one page: s[kt][c] is 16-key tile kt of column tile c; value i of
+// lane group g holds key key_of(kt, 4g + i) of the lane's query column.
+template <int NCT>
 struct SPage {
-  f32x16 s[CT][2];
+  f32x4 s[4][NCT];
 };
-// P^T fragments (bf16) of one page: p[c][kk] covers keys 16kk .. 16kk+15.
-template <int CT>
+// P^T fragments (bf16) of one page: p[kp][c] covers the 32 keys of step kp,
+// lane group g holding keys 32kp + 8g .. 32kp + 8g + 7 (values 0..3 from
+// tile 2kp, 4..7 from tile 2kp + 1).
+template <int NCT>
 struct PFrag {
-  bf16x8 p[CT][4];
+  bf16x8 p[2][NCT];
 };
 
 // ---- MFMAs with explicit register classes (inline asm) ----
-// With one wave per SIMD (AG = true) the O^T accumulators and Q^T fragments
-// live in AGPRs and the S^T tiles and P^T fragments in VGPRs; with two waves
-// per SIMD everything is in VGPRs (a wave that uses AGPRs may only hold 128
-// VGPRs).  The compiler cannot see the wait states these instructions need,
-// so the kernel places explicit s_nop fences where an MFMA result is read by
-// VALU code or a VALU result is read by an MFMA.
+// O^T accumulators and Q^T fragments live in AGPRs, S^T tiles and P^T
+// fragments in VGPRs.  The compiler cannot see the wait states these
+// instructions need, so the kernel places explicit s_nop fences where an
+// MFMA result is read by VALU code or a VALU result is read by an MFMA.
+// With two waves per SIMD (AG = false) every value is in VGPRs: a wave that
+// uses AGPRs may then only hold 128 VGPRs.
 template <bool AG>
-__device__ __forceinline__ void mfma_o(f32x16& o, const bf16x8& a, const bf16x8& b) {
-  if constexpr (AG) asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(o) : "v"(a), "v"(b));
-  else asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(o) : "v"(a), "v"(b));
+__device__ __forceinline__ void mfma_o(f32x4& o, const bf16x8& a, const bf16x8& b) {
+  if constexpr (AG) asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(o) : "v"(a), "v"(b));
+  else asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+v"(o) : "v"(a), "v"(b));
 }
 template <bool AG>
-__device__ __forceinline__ void mfma_s0(f32x16& s, const bf16x8& a, const bf16x8& b) {
-  if constexpr (AG) asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&v"(s) : "v"(a), "a"(b));
-  else asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&v"(s) : "v"(a), "v"(b));
+__device__ __forceinline__ void mfma_s0(f32x4& s, const bf16x8& a, const bf16x8& b) {
+  if constexpr (AG) asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, 0" : "=&v"(s) : "v"(a), "a"(b));
+  else asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, 0" : "=&v"(s) : "v"(a), "v"(b));
 }
 template <bool AG>
-__device__ __forceinline__ void mfma_s(f32x16& s, const bf16x8& a, const bf16x8& b) {
-  if constexpr (AG) asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(s) : "v"(a), "a"(b));
-  else asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(s) : "v"(a), "v"(b));
+__device__ __forceinline__ void mfma_s(f32x4& s, const bf16x8& a, const bf16x8& b) {
+  if constexpr (AG) asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+v"(s) : "v"(a), "a"(b));
+  else asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+v"(s) : "v"(a), "v"(b));
 }
 
 // Whole-tuple fence on the O^T accumulators: an MFMA result read or
 // overwritten by VALU code, or a VALU result read by an MFMA, needs wait
 // states the compiler cannot see through inline asm.
-template <bool AG, int CT, int NDT>
-__device__ __forceinline__ void fence_o(f32x16 (&o)[CT][NDT]) {
+template <bool AG, int NDT, int NCT>
+__device__ __forceinline__ void fence_o(f32x4 (&o)[NDT][NCT]) {
 #pragma unroll
-  for (int c = 0; c < CT; ++c)
+  for (int x = 0; x < NDT; ++x)
 #pragma unroll
-    for (int x = 0; x < NDT; ++x) {
-      if constexpr (AG) asm volatile("s_nop 7\n s_nop 7\n s_nop 7" : "+a"(o[c][x]));
-      else asm volatile("s_nop 7\n s_nop 7\n s_nop 7" : "+v"(o[c][x]));
+    for (int c = 0; c < NCT; ++c) {
+      if constexpr (AG) asm volatile("s_nop 7\n s_nop 7\n s_nop 7" : "+a"(o[x][c]));
+      else asm volatile("s_nop 7\n s_nop 7\n s_nop 7" : "+v"(o[x][c]));
     }
 }
 
 // Fences on S^T tiles (MFMA results about to be read by the softmax) and on
 // P^T fragments (VALU results about to be read by MFMAs).
-template <int CT>
-__device__ __forceinline__ void fence_sp(SPage<CT>& s, PFrag<CT>& p) {
-  if constexpr (CT == 2)
-    asm volatile("s_nop 7\n s_nop 7\n s_nop 4"
-                 : "+v"(s.s[0][0]), "+v"(s.s[0][1]), "+v"(s.s[1][0]), "+v"(s.s[1][1]),
-                   "+v"(p.p[0][0]), "+v"(p.p[0][1]), "+v"(p.p[0][2]), "+v"(p.p[0][3]),
-                   "+v"(p.p[1][0]), "+v"(p.p[1][1]), "+v"(p.p[1][2]), "+v"(p.p[1][3]));
-  else
-    asm volatile("s_nop 7\n s_nop 7\n s_nop 4"
-                 : "+v"(s.s[0][0]), "+v"(s.s[0][1]), "+v"(p.p[0][0]), "+v"(p.p[0][1]),
-                   "+v"(p.p[0][2]), "+v"(p.p[0][3]));
-}
-template <int CT>
-__device__ __forceinline__ void fence_s(SPage<CT>& s) {
-  if constexpr (CT == 2)
+template <int NCT>
+__device__ __forceinline__ void fence_s(SPage<NCT>& s) {
+  if constexpr (NCT == 4)
     asm volatile("s_nop 7\n s_nop 7\n s_nop 5"
-                 : "+v"(s.s[0][0]), "+v"(s.s[0][1]), "+v"(s.s[1][0]), "+v"(s.s[1][1]));
+                 : "+v"(s.s[0][0]), "+v"(s.s[0][1]), "+v"(s.s[0][2]), "+v"(s.s[0][3]),
+                   "+v"(s.s[1][0]), "+v"(s.s[1][1]), "+v"(s.s[1][2]), "+v"(s.s[1][3]),
+                   "+v"(s.s[2][0]), "+v"(s.s[2][1]), "+v"(s.s[2][2]), "+v"(s.s[2][3]),
+                   "+v"(s.s[3][0]), "+v"(s.s[3][1]), "+v"(s.s[3][2]), "+v"(s.s[3][3]));
   else
-    asm volatile("s_nop 7\n s_nop 7\n s_nop 5" : "+v"(s.s[0][0]), "+v"(s.s[0][1]));
+    asm volatile("s_nop 7\n s_nop 7\n s_nop 5"
+                 : "+v"(s.s[0][0]), "+v"(s.s[0][1]), "+v"(s.s[1][0]), "+v"(s.s[1][1]),
+                   "+v"(s.s[2][0]), "+v"(s.s[2][1]), "+v"(s.s[3][0]), "+v"(s.s[3][1]));
 }
-template <int CT>
-__device__ __forceinline__ void fence_p(PFrag<CT>& p) {
-  if constexpr (CT == 2)
+template <int NCT>
+__device__ __forceinline__ void fence_p(PFrag<NCT>& p) {
+  if constexpr (NCT == 4)
     asm volatile("s_nop 7\n s_nop 7\n s_nop 5"
                  : "+v"(p.p[0][0]), "+v"(p.p[0][1]), "+v"(p.p[0][2]), "+v"(p.p[0][3]),
                    "+v"(p.p[1][0]), "+v"(p.p[1][1]), "+v"(p.p[1][2]), "+v"(p.p[1][3]));
   else
     asm volatile("s_nop 7\n s_nop 7\n s_nop 5"
-                 : "+v"(p.p[0][0]), "+v"(p.p[0][1]), "+v"(p.p[0][2]), "+v"(p.p[0][3]));
+                 : "+v"(p.p[0][0]), "+v"(p.p[0][1]), "+v"(p.p[1][0]), "+v"(p.p[1][1]));
+}
+template <int NCT>
+__device__ __forceinline__ void fence_sp(SPage<NCT>& s, PFrag<NCT>& p) {
+  fence_s<NCT>(s);
+  if constexpr (NCT == 4)
+    asm volatile(""
+                 : "+v"(p.p[0][0]), "+v"(p.p[0][1]), "+v"(p.p[0][2]), "+v"(p.p[0][3]),
+                   "+v"(p.p[1][0]), "+v"(p.p[1][1]), "+v"(p.p[1][2]), "+v"(p.p[1][3]));
+  else
+    asm volatile("" : "+v"(p.p[0][0]), "+v"(p.p[0][1]), "+v"(p.p[1][0]), "+v"(p.p[1][1]));
 }
 
 // Forces v to be computed at this point of the instruction stream (an empty
@@ -338,25 +363,31 @@ __device__ __forceinline__ void static_for(F&& f) {
   static_for_impl(f, std::make_integer_sequence<int, N>{});
 }
 
-template <int D, int NW, int CT, bool DENSE, int VL>
-__global__ __launch_bounds__(64 * NW, CT == 1 ? 2 : 1) void paged_attention_kernel(const AttnArgs a) {
-  constexpr bool AG = CT == 2;         // O^T and Q^T in AGPRs (one wave per SIMD)
+template <int D, int NW, int NCT, bool DENSE, int VL>
+__global__ __launch_bounds__(64 * NW, NCT == 4 ? 1 : 2) void paged_attention_kernel(const AttnArgs a) {
+  constexpr bool AG = NCT == 4;        // O^T and Q^T in AGPRs (one wave per SIMD)
   constexpr bool VTR = VL == kVTransposed;
   constexpr int VTILE = VTR ? kTileVT : kTileVR;
-  constexpr int NKS = D / 16;          // QK k-steps
-  constexpr int NDT = D / 32;          // O^T d tiles
+  constexpr int NKS = D / 32;          // QK k-steps (32 d each)
+  constexpr int NDT = D / 16;          // O^T d tiles
   constexpr int PAGE = 64 * D;
-  constexpr int ROWS = 32 * CT * NW;
-  constexpr int NPV = 4 * NDT;         // V^T fragments per page
-  constexpr int NQK = 2 * NKS;         // K fragments per page
+  constexpr int ROWS = 16 * NCT * NW;
+  constexpr int NPV = 2 * NDT;         // V^T fragments per page (2 key steps x d tiles)
+  constexpr int NQK = 4 * NKS;         // K fragments per page (4 key tiles x k-steps)
   constexpr int NFRAG = NPV + NQK;
-  constexpr int NSLOT = CT * NFRAG;    // one MFMA per slot
-  constexpr int FD = CT == 1 ? 4 : 3;  // fragment prefetch distance (slots)
+  constexpr int NSLOT = NCT * NFRAG;   // one MFMA per slot, every fragment feeds NCT
+  constexpr int FD = 3;                // fragment prefetch distance
   constexpr int DMA_PER_STEP = 2 * (64 * D * 2) / 1024 / NW;   // copy instructions per wave
   constexpr int DMA_STRIDE = (NSLOT / 2) / DMA_PER_STEP > 0 ? (NSLOT / 2) / DMA_PER_STEP : 1;
-  constexpr int MAXS = 5 * CT;         // slots holding the max / rebase work
-  constexpr int NE = 32 * CT;          // softmax weights per lane per page
+  // softmax slots: the page maximum (8 max3 per column over MAXA slots), then
+  // per column the reduction over the lane groups and the exponent-base
+  // decision (MAXB slots per column), then the weights over the remaining slots
+  constexpr int NE = 16 * NCT;         // softmax weights per lane per page
   constexpr int NSOFT = soft_ops(NE);
+  constexpr int MAXA = NSLOT / 8;
+  constexpr int MAXB = NSLOT / (8 * NCT);
+  constexpr int MAXS = MAXA + NCT * MAXB;
+  static_assert((8 * NCT) % MAXA == 0 && MAXB >= 2, "slot plan");
   __shared__ __attribute__((aligned(1024))) uint16_t k_s0[PAGE];
   __shared__ __attribute__((aligned(1024))) uint16_t k_s1[PAGE];
   __shared__ __attribute__((aligned(1024))) uint16_t v_s0[PAGE];
@@ -365,8 +396,8 @@ __global__ __launch_bounds__(64 * NW, CT == 1 ? 2 : 1) void paged_attention_kern
   const int t = threadIdx.x;
   const int wv = __builtin_amdgcn_readfirstlane(t >> 6);
   const int lane = t & 63;
-  const int col = lane & 31;
-  const int half = lane >> 5;
+  const int col = lane & 15;           // query column within a 16-column tile
+  const int grp = lane >> 4;           // lane group: keys 4*grp .. of each 16-key tile
 
   int bid = blockIdx.x;
   const int nwg = gridDim.x;
@@ -413,11 +444,11 @@ __global__ __launch_bounds__(64 * NW, CT == 1 ? 2 : 1) void paged_attention_kern
   const int QT = ROWS / gs;            // chunk queries per tile
   const int q0 = qt * QT;
   const int q_end = q0 + QT < a.C ? q0 + QT : a.C;   // the last tile may be partial
-  int head[CT], tq[CT];
-  bool valid[CT];
+  int head[NCT], tq[NCT];
+  bool valid[NCT];
 #pragma unroll
-  for (int c = 0; c < CT; ++c) {
-    const int r = wv * 32 * CT + 32 * c + col;
+  for (int c = 0; c < NCT; ++c) {
+    const int r = wv * 16 * NCT + 16 * c + col;
     head[c] = g * gs + r / QT;
     tq[c] = q0 + r % QT;
     valid[c] = tq[c] < a.C;
@@ -426,9 +457,9 @@ __global__ __launch_bounds__(64 * NW, CT == 1 ? 2 : 1) void paged_attention_kern
   const int kvh = (g * gs) / (a.Hq / a.Hkv);
   const int cl = a.cached_len[b];
   const int nkb = blocks_for(cl + a.C);
-  int qpos[CT];
+  int qpos[NCT];
 #pragma unroll
-  for (int c = 0; c < CT; ++c) qpos[c] = cl + tq[c];
+  for (int c = 0; c < NCT; ++c) qpos[c] = cl + tq[c];
   const int j_last = (cl + q_end - 1) / kPage;     // last block any row can see
   const int mask_from = cl + q0;                   // keys beyond this need masking
 
@@ -471,29 +502,30 @@ __global__ __launch_bounds__(64 * NW, CT == 1 ? 2 : 1) void paged_attention_kern
   }
   const int32_t* ptab = a.page_table + ((size_t)b * a.Hkv + kvh) * a.max_kv_blocks;
 
-  bf16x8 qf[CT][NKS];
+  // Q^T fragments: column tile c, k-step ks: d = 32ks + 8*grp .. +7 of the lane's query
+  bf16x8 qf[NCT][NKS];
 #pragma unroll
-  for (int c = 0; c < CT; ++c) {
-    const uint16_t* qrow = a.q + (((size_t)b * a.C + tq[c]) * a.Hq + head[c]) * D + 8 * half;
+  for (int c = 0; c < NCT; ++c) {
+    const uint16_t* qrow = a.q + (((size_t)b * a.C + tq[c]) * a.Hq + head[c]) * D + 8 * grp;
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) {
-      qf[c][ks] = *reinterpret_cast<const bf16x8*>(qrow + 16 * ks);
+      qf[c][ks] = *reinterpret_cast<const bf16x8*>(qrow + 32 * ks);
       if constexpr (AG) asm volatile("s_nop 2" : "+a"(qf[c][ks]));   // into AGPRs
     }
   }
 
-  f32x16 o[CT][NDT];
+  f32x4 o[NDT][NCT];
 #pragma unroll
-  for (int c = 0; c < CT; ++c)
+  for (int x = 0; x < NDT; ++x)
 #pragma unroll
-    for (int x = 0; x < NDT; ++x)
+    for (int c = 0; c < NCT; ++c)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) o[c][x][v] = 0.f;
-  fence_o<AG, CT, NDT>(o);
-  float m_run[CT], l_run[CT];
+      for (int v = 0; v < 4; ++v) o[x][c][v] = 0.f;
+  fence_o<AG>(o);
+  float m_run[NCT], l_run[NCT];
 #pragma unroll
-  for (int c = 0; c < CT; ++c) {
-    m_run[c] = -INFINITY;
+  for (int c = 0; c < NCT; ++c) {
+    m_run[c] = kNoBase;
     l_run[c] = 0.f;
   }
 
@@ -514,8 +546,8 @@ __global__ __launch_bounds__(64 * NW, CT == 1 ? 2 : 1) void paged_attention_kern
   // pages run by the software-pipelined loop: an even number of unmasked ones
   const int n_pipe = n_main & ~1;
 
-  SPage<CT> SA, SB;
-  PFrag<CT> PA, PB;
+  SPage<NCT> SA, SB;
+  PFrag<NCT> PA, PB;
   int base = 0, blk_cur = 0, pg_cur = 0, blk_nxt = 0, pg_nxt = 0;
   auto fetch = [&](int b0, int& blk, int& pg) {
     int idx = b0 + lane;
@@ -549,43 +581,43 @@ __global__ __launch_bounds__(64 * NW, CT == 1 ? 2 : 1) void paged_attention_kern
   };
 
   // Per-lane byte offsets of the MFMA operand reads inside a page tile; the
-  // buffer, the d tile or 16-key block of a PV step and the upper 32 keys of
-  // a QK step are immediates.  Lane column col reads key row key_of_row(col)
-  // of K, so its P^T fragment kk holds keys 16kk + 8*half .. +7: in a
-  // transposed V tile one 16-byte chunk of V^T row 32x + col; in a
-  // token-major tile two transpose reads (keys +0..3 and +4..7; the 16 lanes
-  // of a transpose read address 4 key rows x 16 d and receive one d each).
-  constexpr int NVOFS = VTR ? 4 : NDT;
+  // buffer, the key tile of a QK fragment and the d tile or key step of a PV
+  // fragment are immediates where the swizzle allows.  K fragment (kt, ks):
+  // row key_of(kt, col), chunk 4ks + grp.  V^T fragment (kp, dt): d rows
+  // 16dt + col, keys 32kp + 8grp .. +7: in a transposed tile one 16-byte chunk
+  // of row 16dt + col; in a token-major tile two transpose reads (keys +0..3
+  // and +4..7; the 16 lanes of a group address 4 key rows x 16 d and each
+  // receives 4 keys of one d).
+  constexpr int NVOFS = VTR ? 2 : NDT;
   uint32_t kofs[NKS], vofs[NVOFS];
 #pragma unroll
-  for (int x = 0; x < NKS; ++x) {
-    const int kr = key_of_row(col);
-    kofs[x] = (uint32_t)(kr * D * 2 + 16 * k_swz<D>(kr, 2 * x + half));
+  for (int ks = 0; ks < NKS; ++ks) {
+    const int kr = key_of(0, col);
+    kofs[ks] = (uint32_t)(kr * D * 2 + 16 * k_swz<D>(kr, 4 * ks + grp));
   }
   if constexpr (VTR) {
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk)
-      vofs[kk] = (uint32_t)(col * kPage * 2 + 16 * vt_swz(col, 2 * kk + half));
+    for (int kp = 0; kp < 2; ++kp)
+      vofs[kp] = (uint32_t)(col * kPage * 2 + 16 * vt_swz(col, 4 * kp + grp));
   } else {
-    const int grp = lane >> 4, sl = lane & 15;
-    const int r0 = 8 * (grp >> 1) + (sl >> 2);
+    const int r0 = 8 * grp + (col >> 2);
 #pragma unroll
     for (int x = 0; x < NDT; ++x) {
-      const int d = 32 * x + 16 * (grp & 1) + 4 * (sl & 3);
+      const int d = 16 * x + 4 * (col & 3);
       vofs[x] = (uint32_t)(r0 * D * 2 + 16 * vr_swz<D>(r0, d >> 3) + 2 * (d & 7));
     }
   }
-  // fragment F of a step: F < NPV is V^T fragment (kk = F / NDT, d tile
-  // x = F % NDT), otherwise K fragment (k-step (F - NPV) / 2, keys
-  // 32 * ((F - NPV) % 2) ..)
+  // fragment F of a step: F < NPV is V^T fragment (kp = F / NDT, d tile
+  // x = F % NDT), otherwise K fragment (key tile (F - NPV) / NKS, k-step
+  // (F - NPV) % NKS)
   auto load_frag = [&](int F, const uint16_t* vt, const uint16_t* kt) -> bf16x8 {
     if (F < NPV) {
-      const int kk = F / NDT, x = F % NDT;
+      const int kp = F / NDT, x = F % NDT;
       if constexpr (VTR) {
-        const char* p = reinterpret_cast<const char*>(vt) + vofs[kk] + 32 * kPage * 2 * x;
+        const char* p = reinterpret_cast<const char*>(vt) + vofs[kp] + 16 * kPage * 2 * x;
         return *reinterpret_cast<const bf16x8*>(p);
       } else {
-        const char* p = reinterpret_cast<const char*>(vt) + vofs[x] + 16 * kk * D * 2;
+        const char* p = reinterpret_cast<const char*>(vt) + vofs[x] + 32 * kp * D * 2;
         const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p);
         const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 4 * D * 2));
         const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
@@ -593,29 +625,30 @@ __global__ __launch_bounds__(64 * NW, CT == 1 ? 2 : 1) void paged_attention_kern
         return __builtin_bit_cast(bf16x8, w);
       }
     }
-    const int G2 = F - NPV;
-    const char* p = reinterpret_cast<const char*>(kt) + kofs[G2 / 2] + (G2 % 2) * 32 * D * 2;
+    const int G2 = F - NPV, kt4 = G2 / NKS, ks = G2 % NKS;
+    const char* p = reinterpret_cast<const char*>(kt) + kofs[ks] +
+                    (32 * (kt4 >> 1) + 4 * (kt4 & 1)) * D * 2;
     return *reinterpret_cast<const bf16x8*>(p);
   };
 
   // Whole-page contractions (outside the pipelined loop).
-  auto qk_page = [&](SPage<CT>& st, const uint16_t* kt) __attribute__((always_inline)) {
+  auto qk_page = [&](SPage<NCT>& st, const uint16_t* kt) __attribute__((always_inline)) {
     static_for<NQK>([&](auto gtag) __attribute__((always_inline)) {
-      constexpr int G2 = decltype(gtag)::value, x = G2 / 2, h = G2 % 2;
+      constexpr int G2 = decltype(gtag)::value, kt4 = G2 / NKS, ks = G2 % NKS;
       const bf16x8 kf = load_frag(NPV + G2, kt, kt);
 #pragma unroll
-      for (int c = 0; c < CT; ++c) {
-        if constexpr (x == 0) mfma_s0<AG>(st.s[c][h], kf, qf[c][x]);
-        else mfma_s<AG>(st.s[c][h], kf, qf[c][x]);
+      for (int c = 0; c < NCT; ++c) {
+        if constexpr (ks == 0) mfma_s0<AG>(st.s[kt4][c], kf, qf[c][ks]);
+        else mfma_s<AG>(st.s[kt4][c], kf, qf[c][ks]);
       }
     });
   };
-  auto pv_page = [&](const PFrag<CT>& pf, const uint16_t* vt) __attribute__((always_inline)) {
+  auto pv_page = [&](const PFrag<NCT>& pf, const uint16_t* vt) __attribute__((always_inline)) {
     static_for<NPV>([&](auto ftag) __attribute__((always_inline)) {
       constexpr int F = decltype(ftag)::value;
       const bf16x8 vf = load_frag(F, vt, vt);
 #pragma unroll
-      for (int c = 0; c < CT; ++c) mfma_o<AG>(o[c][F % NDT], vf, pf.p[c][F / NDT]);
+      for (int c = 0; c < NCT; ++c) mfma_o<AG>(o[F % NDT][c], vf, pf.p[F / NDT][c]);
     });
   };
 
@@ -623,9 +656,9 @@ __global__ __launch_bounds__(64 * NW, CT == 1 ? 2 : 1) void paged_attention_kern
   // step's PV reads, with a zero P: that PV adds nothing and every tile read
   // is initialised.  Then S(0).
 #pragma unroll
-  for (int c = 0; c < CT; ++c)
+  for (int kp = 0; kp < 2; ++kp)
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) PB.p[c][kk] = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
+    for (int c = 0; c < NCT; ++c) PB.p[kp][c] = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
   if (n_pipe > 0) {
     page_to_lds<D, NW, kTileK>(page_ptr(a.k_pool, 0), k_s0, wv, lane);
     page_to_lds<D, NW, kTileK>(page_ptr(a.k_pool, 1), k_s1, wv, lane);
@@ -634,7 +667,7 @@ __global__ __launch_bounds__(64 * NW, CT == 1 ? 2 : 1) void paged_attention_kern
     __syncthreads();
     qk_page(SA, k_s0);
     __syncthreads();
-    fence_sp<CT>(SA, PB);   // S(0) and the zero P are read by the first step's first slots
+    fence_sp<NCT>(SA, PB);   // S(0) and the zero P are read by the first step's first slots
   }
 
   // Step i: DMA K(i+2) -> k[i%2], V(i) -> v[i%2]; PV(i-1) from v[(i-1)%2] and
@@ -642,10 +675,10 @@ __global__ __launch_bounds__(64 * NW, CT == 1 ? 2 : 1) void paged_attention_kern
   // per slot, the softmax work spread over the slots.
   auto step = [&](auto par, int i) __attribute__((always_inline)) {
     constexpr int P = decltype(par)::value;
-    SPage<CT>& sc = P ? SB : SA;
-    SPage<CT>& sn = P ? SA : SB;
-    PFrag<CT>& pn = P ? PB : PA;
-    PFrag<CT>& po = P ? PA : PB;
+    SPage<NCT>& sc = P ? SB : SA;
+    SPage<NCT>& sn = P ? SA : SB;
+    PFrag<NCT>& pn = P ? PB : PA;
+    PFrag<NCT>& po = P ? PA : PB;
     uint16_t* const k_dma = P ? k_s1 : k_s0;
     const uint16_t* const k_rd = P ? k_s0 : k_s1;
     uint16_t* const v_dma = P ? v_s1 : v_s0;
@@ -656,12 +689,10 @@ __global__ __launch_bounds__(64 * NW, CT == 1 ? 2 : 1) void paged_attention_kern
     // No hazard fence here: the last MFMA writing S and the last pack writing
     // P come well before their first readers in this step (end of step,
     // barrier, page pointers); the hazard test checks the distance.
-    float mx[CT][2], alpha[CT], nmb[CT], ps[CT];
+    float mx[NCT][2], alpha[NCT], ps[NCT];
 #pragma unroll
-    for (int c = 0; c < CT; ++c) {
-      mx[c][0] = mx[c][1] = -INFINITY;
+    for (int c = 0; c < NCT; ++c) {
       alpha[c] = 1.f;
-      nmb[c] = 0.f;
       ps[c] = 0.f;
     }
     bool rb_any = false;
@@ -670,7 +701,7 @@ __global__ __launch_bounds__(64 * NW, CT == 1 ? 2 : 1) void paged_attention_kern
     for (int f = 0; f < FD; ++f) fr[f] = load_frag(f, v_rd, k_rd);
     static_for<NSLOT>([&](auto stag) __attribute__((always_inline)) {
       constexpr int s = decltype(stag)::value;
-      constexpr int F = s / CT, c = s % CT;
+      constexpr int F = s / NCT, c = s % NCT;
       if constexpr (c == 0 && F + FD < NFRAG) fr[F + FD] = load_frag(F + FD, v_rd, k_rd);
       // the copies of K(i+2) and V(i), one instruction every DMA_STRIDE slots
       // over the first half of the step (issued all at once they queue in
@@ -683,81 +714,97 @@ __global__ __launch_bounds__(64 * NW, CT == 1 ? 2 : 1) void paged_attention_kern
           page_part_to_lds<D, NW, VTILE>(v_src, v_dma, wv, lane, m - DMA_PER_STEP / 2);
       }
       if constexpr (F < NPV) {
-        mfma_o<AG>(o[c][F % NDT], fr[F], po.p[c][F / NDT]);
+        mfma_o<AG>(o[F % NDT][c], fr[F], po.p[F / NDT][c]);
       } else {
-        constexpr int G2 = F - NPV, x = G2 / 2, h = G2 % 2;
-        if constexpr (x == 0) mfma_s0<AG>(sn.s[c][h], fr[F], qf[c][x]);
-        else mfma_s<AG>(sn.s[c][h], fr[F], qf[c][x]);
+        constexpr int G2 = F - NPV, kt4 = G2 / NKS, ks = G2 % NKS;
+        if constexpr (ks == 0) mfma_s0<AG>(sn.s[kt4][c], fr[F], qf[c][ks]);
+        else mfma_s<AG>(sn.s[kt4][c], fr[F], qf[c][ks]);
       }
       // softmax work of this slot
-      if constexpr (s < 4 * CT) {
-        // two independent max chains per column tile (half the dependent latency)
-        constexpr int cc = s / 4, k0 = 4 * (s % 4);
-        mx[cc][0] = max3(mx[cc][0], sc.s[cc][0][k0], sc.s[cc][1][k0]);
-        mx[cc][1] = max3(mx[cc][1], sc.s[cc][0][k0 + 1], sc.s[cc][1][k0 + 1]);
-        mx[cc][0] = max3(mx[cc][0], sc.s[cc][0][k0 + 2], sc.s[cc][1][k0 + 2]);
-        mx[cc][1] = max3(mx[cc][1], sc.s[cc][0][k0 + 3], sc.s[cc][1][k0 + 3]);
-        pin(mx[cc][0]);
-        pin(mx[cc][1]);
+      if constexpr (s < MAXA) {
+        // the page maximum of every column, two independent chains per column
+        // (tiles 0, 1 and tiles 2, 3): 8 max3 per column over MAXA slots
+        constexpr int PER = 8 * NCT / MAXA;     // max3 per slot
+        static_for<PER>([&](auto xtag) __attribute__((always_inline)) {
+          constexpr int k = s * PER + decltype(xtag)::value;   // 0 .. 8 * NCT - 1
+          constexpr int cc = k / 8, ch = (k / 4) % 2, v = k % 4;
+          if constexpr (v == 0) mx[cc][ch] = max2(sc.s[2 * ch][cc][0], sc.s[2 * ch + 1][cc][0]);
+          else mx[cc][ch] = max3(mx[cc][ch], sc.s[2 * ch][cc][v], sc.s[2 * ch + 1][cc][v]);
+          pin(mx[cc][ch]);
+        });
       } else if constexpr (s < MAXS) {
-        constexpr int cc = s - 4 * CT;
-        const float m = halves_max(fmaxf(mx[cc][0], mx[cc][1])) * a.scale_log2;
-        const bool rebase = m > m_run[cc] + kRescaleSlack;
-        alpha[cc] = rebase ? fast_exp2(m_run[cc] - m) : 1.0f;
-        m_run[cc] = rebase ? m : m_run[cc];
-        rb_any |= rebase;
-        nmb[cc] = (m_run[cc] == -INFINITY) ? 0.f : -m_run[cc];
-        pin(nmb[cc]);
-        pin(alpha[cc]);
+        // per column: the maximum over the 4 lane groups, then the base decision
+        // (a dependent chain, spread over the column's slots)
+        constexpr int cc = (s - MAXA) / MAXB, part = (s - MAXA) % MAXB;
+        if constexpr (part == 0) {
+          mx[cc][0] = groups_max(max2(mx[cc][0], mx[cc][1]));
+          pin(mx[cc][0]);
+        }
+        if constexpr (part == 1) {
+          // the page maximum in log2 units; the base moves only past the slack,
+          // and alpha = exp2(old - new) is exactly 1 when it does not
+          const float m = mx[cc][0] * a.scale_log2;
+          const bool rebase = m > m_run[cc] + kRescaleSlack;
+          mx[cc][1] = rebase ? m : m_run[cc];
+          rb_any |= rebase;
+          pin(mx[cc][1]);
+        }
+        if constexpr (part == MAXB - 1) {
+          alpha[cc] = fast_exp2(m_run[cc] - mx[cc][1]);
+          m_run[cc] = mx[cc][1];
+          pin(alpha[cc]);
+          pin(m_run[cc]);
+        }
       } else {
         // Weights of the page, software-pipelined over the remaining slots so
         // that no instruction waits on the one before it: element op j does
         // the scaled score of element j, the exp of element j-1 and the row
-        // sum of element j-2 (elements in unit order, unit u = 8 weights of
-        // one P^T fragment); unit u is packed to bf16 after element op 8u+8.
+        // sum of element j-2 (elements in unit order, unit u = the 8 weights
+        // of P^T fragment (kp, c) = (u / NCT, u % NCT): values 0..3 of tile
+        // 2kp, then of tile 2kp + 1); unit u is packed to bf16 after element
+        // op 8u+8.
         constexpr int lo = ((s - MAXS) * NSOFT) / (NSLOT - MAXS);
         constexpr int hi = ((s - MAXS + 1) * NSOFT) / (NSLOT - MAXS);
         static_for<hi - lo>([&](auto otag) __attribute__((always_inline)) {
           constexpr int op = soft_op(lo + decltype(otag)::value, NE);
           if constexpr (op >= 0) {
             if constexpr (op < NE) {
-              constexpr int u = op / 8, cc = u / 4, kk = u % 4, v = 8 * (kk % 2) + op % 8;
-              f32x16& sv = sc.s[cc][kk / 2];
-              sv[v] = fmaf(sv[v], a.scale_log2, nmb[cc]);
-              pin(sv[v]);
+              constexpr int u = op / 8, x = op % 8, cc = u % NCT, kt4 = 2 * (u / NCT) + x / 4;
+              f32x4& sv = sc.s[kt4][cc];
+              sv[x % 4] = fmaf(sv[x % 4], a.scale_log2, -m_run[cc]);
+              pin(sv[x % 4]);
             }
             if constexpr (op >= 1 && op <= NE) {
-              constexpr int e = op - 1, u = e / 8, cc = u / 4, kk = u % 4, v = 8 * (kk % 2) + e % 8;
-              f32x16& sv = sc.s[cc][kk / 2];
-              sv[v] = fast_exp2(sv[v]);
-              pin(sv[v]);
+              constexpr int e = op - 1, u = e / 8, x = e % 8, cc = u % NCT, kt4 = 2 * (u / NCT) + x / 4;
+              f32x4& sv = sc.s[kt4][cc];
+              sv[x % 4] = fast_exp2(sv[x % 4]);
+              pin(sv[x % 4]);
             }
             if constexpr (op >= 2) {
-              constexpr int e = op - 2, u = e / 8, cc = u / 4, kk = u % 4, v = 8 * (kk % 2) + e % 8;
-              ps[cc] += sc.s[cc][kk / 2][v];
+              constexpr int e = op - 2, u = e / 8, x = e % 8, cc = u % NCT, kt4 = 2 * (u / NCT) + x / 4;
+              ps[cc] += sc.s[kt4][cc][x % 4];
               pin(ps[cc]);
             }
           } else {
-            constexpr int u = -1 - op, cc = u / 4, kk = u % 4;
-            const f32x16& sv = sc.s[cc][kk / 2];
+            constexpr int u = -1 - op, kp = u / NCT, cc = u % NCT;
 #pragma unroll
-            for (int x = 0; x < 8; ++x) pn.p[cc][kk][x] = (__bf16)sv[8 * (kk % 2) + x];
-            pin(pn.p[cc][kk]);
+            for (int x = 0; x < 8; ++x) pn.p[kp][cc][x] = (__bf16)sc.s[2 * kp + x / 4][cc][x % 4];
+            pin(pn.p[kp][cc]);
           }
         });
       }
       __builtin_amdgcn_sched_barrier(0);
     });
 #pragma unroll
-    for (int c = 0; c < CT; ++c) l_run[c] = l_run[c] * alpha[c] + ps[c];
+    for (int c = 0; c < NCT; ++c) l_run[c] = l_run[c] * alpha[c] + ps[c];
     const uint64_t any = __ballot(rb_any);
     if (any) {   // the exponent base moved on some lane: rescale O (rare)
-      fence_o<AG, CT, NDT>(o);
+      fence_o<AG>(o);
 #pragma unroll
-      for (int c = 0; c < CT; ++c)
+      for (int x = 0; x < NDT; ++x)
 #pragma unroll
-        for (int x = 0; x < NDT; ++x) o[c][x] *= alpha[c];
-      fence_o<AG, CT, NDT>(o);
+        for (int c = 0; c < NCT; ++c) o[x][c] *= alpha[c];
+      fence_o<AG>(o);
     }
     copies_landed(k_dma, v_dma);
     __syncthreads();
@@ -772,7 +819,7 @@ __global__ __launch_bounds__(64 * NW, CT == 1 ? 2 : 1) void paged_attention_kern
       step(P1{}, i + 1);
     }
     // PV of page n_pipe - 1 (odd: its P is PB, its V in v_s1)
-    fence_p<CT>(PB);
+    fence_p<NCT>(PB);
     pv_page(PB, v_s1);
     __syncthreads();
   }
@@ -802,66 +849,69 @@ __global__ __launch_bounds__(64 * NW, CT == 1 ? 2 : 1) void paged_attention_kern
       }
     }
     qk_page(SA, k_s0);
-    fence_s<CT>(SA);
+    fence_s<NCT>(SA);
     if (i >= n_main) {
       const int j = id_of(blk_cur, blk_nxt, i);
 #pragma unroll
-      for (int c = 0; c < CT; ++c) {
-        const int lim = qpos[c] - kPage * j - 8 * half;
+      for (int c = 0; c < NCT; ++c) {
+        const int lim = qpos[c] - kPage * j;
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int kp = 16 * (v >> 3) + 4 * ((v >> 2) & 1) + (v & 3);   // key - 8*half
-          if (kp > lim) SA.s[c][0][v] = -INFINITY;
-          if (kp + 32 > lim) SA.s[c][1][v] = -INFINITY;
-        }
+        for (int kt4 = 0; kt4 < 4; ++kt4)
+#pragma unroll
+          for (int v = 0; v < 4; ++v)
+            if (32 * (kt4 >> 1) + 8 * grp + 4 * (kt4 & 1) + v > lim) SA.s[kt4][c][v] = -INFINITY;
       }
     }
-    float alpha[CT];
+    float alpha[NCT];
     bool rb_any = false;
 #pragma unroll
-    for (int c = 0; c < CT; ++c) {
-      float mx = -INFINITY;
+    for (int c = 0; c < NCT; ++c) {
+      float mx = max2(SA.s[0][c][0], SA.s[1][c][0]);
 #pragma unroll
-      for (int k = 0; k < 16; ++k) mx = max3(mx, SA.s[c][0][k], SA.s[c][1][k]);
-      const float m = halves_max(mx) * a.scale_log2;
+      for (int v = 0; v < 4; ++v) {
+        if (v > 0) mx = max3(mx, SA.s[0][c][v], SA.s[1][c][v]);
+        mx = max3(mx, SA.s[2][c][v], SA.s[3][c][v]);
+      }
+      // a fully masked page (-inf) never moves the base
+      const float m = groups_max(mx) * a.scale_log2;
       const bool rebase = m > m_run[c] + kRescaleSlack;
-      alpha[c] = rebase ? fast_exp2(m_run[c] - m) : 1.0f;
-      m_run[c] = rebase ? m : m_run[c];
+      const float m_new = rebase ? m : m_run[c];
+      alpha[c] = fast_exp2(m_run[c] - m_new);
+      m_run[c] = m_new;
       rb_any |= rebase;
-      const float nmb = (m_run[c] == -INFINITY) ? 0.f : -m_run[c];
       float ps = 0.f;
 #pragma unroll
-      for (int h = 0; h < 2; ++h)
+      for (int kt4 = 0; kt4 < 4; ++kt4)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const float e = fast_exp2(fmaf(SA.s[c][h][v], a.scale_log2, nmb));
-          SA.s[c][h][v] = e;
+        for (int v = 0; v < 4; ++v) {
+          const float e = fast_exp2(fmaf(SA.s[kt4][c][v], a.scale_log2, -m_run[c]));
+          SA.s[kt4][c][v] = e;
           ps += e;
         }
       l_run[c] = l_run[c] * alpha[c] + ps;
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk)
+      for (int kp = 0; kp < 2; ++kp)
 #pragma unroll
-        for (int x = 0; x < 8; ++x) PA.p[c][kk][x] = (__bf16)SA.s[c][kk / 2][8 * (kk % 2) + x];
+        for (int x = 0; x < 8; ++x) PA.p[kp][c][x] = (__bf16)SA.s[2 * kp + x / 4][c][x % 4];
     }
     if (__ballot(rb_any)) {
-      fence_o<AG, CT, NDT>(o);
+      fence_o<AG>(o);
 #pragma unroll
-      for (int c = 0; c < CT; ++c)
+      for (int x = 0; x < NDT; ++x)
 #pragma unroll
-        for (int x = 0; x < NDT; ++x) o[c][x] *= alpha[c];
-      fence_o<AG, CT, NDT>(o);
+        for (int c = 0; c < NCT; ++c) o[x][c] *= alpha[c];
+      fence_o<AG>(o);
     }
-    fence_p<CT>(PA);
+    fence_p<NCT>(PA);
     pv_page(PA, v_s0);
     __syncthreads();
   }
-  fence_o<AG, CT, NDT>(o);
+  fence_o<AG>(o);
 
-  // epilogue
+  // epilogue: O^T tile (x, c) value v of lane group grp is d = 16x + 4grp + v
 #pragma unroll
-  for (int c = 0; c < CT; ++c) {
-    const float l_tot = halves_sum(l_run[c]);
+  for (int c = 0; c < NCT; ++c) {
+    const float l_tot = groups_sum(l_run[c]);
     const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
     const float lse_val = l_tot > 0.f ? (m_run[c] + log2f(l_tot)) * kLn2 : -INFINITY;
     const size_t qrow_idx = ((size_t)b * a.Hq + head[c]) * a.C + tq[c];
@@ -870,30 +920,23 @@ __global__ __launch_bounds__(64 * NW, CT == 1 ? 2 : 1) void paged_attention_kern
       uint16_t* orow = a.out + (((size_t)b * a.C + tq[c]) * a.Hq + head[c]) * D;
 #pragma unroll
       for (int x = 0; x < NDT; ++x) {
-#pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) {
-          const int d = 32 * x + 8 * q4 + 4 * half;
-          uint2 pk;
-          pk.x = pack_bf16x2(o[c][x][4 * q4 + 0] * inv, o[c][x][4 * q4 + 1] * inv);
-          pk.y = pack_bf16x2(o[c][x][4 * q4 + 2] * inv, o[c][x][4 * q4 + 3] * inv);
-          *reinterpret_cast<uint2*>(orow + d) = pk;
-        }
+        const int d = 16 * x + 4 * grp;
+        uint2 pk;
+        pk.x = pack_bf16x2(o[x][c][0] * inv, o[x][c][1] * inv);
+        pk.y = pack_bf16x2(o[x][c][2] * inv, o[x][c][3] * inv);
+        *reinterpret_cast<uint2*>(orow + d) = pk;
       }
-      if (a.lse != nullptr && half == 0) a.lse[qrow_idx] = lse_val;
+      if (a.lse != nullptr && grp == 0) a.lse[qrow_idx] = lse_val;
     } else {
       const size_t prow = (size_t)sp * a.B * a.Hq * a.C + qrow_idx;
       float* po = a.part_o + prow * D;
 #pragma unroll
       for (int x = 0; x < NDT; ++x) {
-#pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) {
-          const int d = 32 * x + 8 * q4 + 4 * half;
-          *reinterpret_cast<float4*>(po + d) =
-              make_float4(o[c][x][4 * q4 + 0] * inv, o[c][x][4 * q4 + 1] * inv,
-                          o[c][x][4 * q4 + 2] * inv, o[c][x][4 * q4 + 3] * inv);
-        }
+        const int d = 16 * x + 4 * grp;
+        *reinterpret_cast<float4*>(po + d) = make_float4(o[x][c][0] * inv, o[x][c][1] * inv,
+                                                         o[x][c][2] * inv, o[x][c][3] * inv);
       }
-      if (half == 0) a.part_lse[prow] = lse_val;
+      if (grp == 0) a.part_lse[prow] = lse_val;
     }
   }
 }
@@ -1100,7 +1143,7 @@ __global__ __launch_bounds__(256) void xcd_split_kernel(const int32_t* __restric
 }
 
 int attn_rows_per_workgroup(int table_mode) {
-  return 32 * kColTiles * (table_mode == kTablesPerQTile ? kWavesQTile : kWavesGroup);
+  return 16 * kColTiles * (table_mode == kTablesPerQTile ? kWavesQTile : kWavesGroup);
 }
 
 int attn_query_tile(int group_size, int table_mode) {

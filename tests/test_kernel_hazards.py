@@ -94,13 +94,16 @@ def _shortest_use(lines, labels, k):
     return best
 
 
-@pytest.fixture(scope="module")
-def attention_asm(tmp_path_factory):
+@pytest.fixture(scope="module", params=[2, 4])
+def attention_asm(request, tmp_path_factory):
+    """The kernel's gfx950 assembly as built (two waves per SIMD, 2 column tiles
+    per wave) and in its one-wave form (CA_COL_TILES=4)."""
     if not os.path.exists(HIPCC):
         pytest.skip("hipcc not available")
     out = tmp_path_factory.mktemp("asm") / "attention.s"
     cmd = [HIPCC, "--offload-arch=gfx950", "-O3", "-std=c++17", "-Xclang", "-target-feature",
            "-Xclang", "-packed-fp32-ops", "--cuda-device-only", "-S",
+           f"-DCA_COL_TILES={request.param}",
            "-I", os.path.join(ROOT, "include"), "-o", str(out), SRC]
     r = subprocess.run(cmd, capture_output=True, text=True, timeout=600)
     assert r.returncode == 0, r.stderr[-2000:]
@@ -109,7 +112,8 @@ def attention_asm(tmp_path_factory):
 
 def test_mfma_results_wait_before_use(attention_asm):
     kernels = list(_kernels(attention_asm))
-    # D in {64, 128} x waves in {2, 4} x {selected, dense} x V layout in {token-major, transposed}
+    # D in {64, 128} x {per-group, block-sparse} workgroups x {selected, dense} x
+    # V layout in {token-major, transposed}
     assert len(kernels) == 16
     for name, lines, labels in kernels:
         n_mfma = 0
@@ -129,7 +133,7 @@ def test_checker_flags_a_missing_fence(tmp_path):
     if not os.path.exists(HIPCC):
         pytest.skip("hipcc not available")
     src = open(SRC).read()
-    fenced = "    qk_page(SA, k_s0);\n    fence_s<CT>(SA);\n"
+    fenced = "    qk_page(SA, k_s0);\n    fence_s<NCT>(SA);\n"
     assert src.count(fenced) == 1
     bad = tmp_path / "attention.hip"
     bad.write_text(src.replace(fenced, "    qk_page(SA, k_s0);\n"))
