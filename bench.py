@@ -35,6 +35,9 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup-ms", type=float, default=300.0,
+                    help="untimed calls before each timed loop continue past --warmup until "
+                         "this much wall time has passed (power-management settling)")
     ap.add_argument("--workload", default="llama8b_128k_final")
     ap.add_argument("--rho", type=float, default=None,
                     help="override the query-direction weight (0 = literal iid inputs)")
@@ -205,8 +208,7 @@ def density_sweep(ca, p, w, q, kp, vp, pt, dense_ms, args, stream, ev):
         ca.validate_tables(p, gs, tabs)
         run = lambda: ca.chunk_attention(p, q, (kp, vp), pt, tabs, gs, w.sm_scale,
                                          num_splits=0, out=out, ws=aws)
-        for _ in range(args.warmup):
-            run()
+        warm(run, args.warmup)
         torch.cuda.synchronize()
         t0, t1 = ev(), ev()
         t0.record(stream)
@@ -314,8 +316,7 @@ def strategy_arms(ca, p, w, q, kp, vp, pt, masks, tables, ip, args, stream, ev):
     import torch
 
     def timed(fn):
-        for _ in range(args.warmup):
-            fn()
+        warm(fn, args.warmup)
         torch.cuda.synchronize()
         a0, a1 = ev(), ev()
         a0.record(stream)
@@ -466,6 +467,27 @@ def host_ahead(torch):
     torch.cuda._sleep(1_000_000)
 
 
+# Set from --warmup-ms in main().
+WARMUP_MS = [300.0]
+
+
+def warm(fn, n):
+    """n untimed calls of fn, continued until WARMUP_MS of them have run.  After
+    idle the MI355X's power management takes tens of milliseconds of sustained
+    load to settle: the attention kernel's launches are up to 25% longer during
+    the first ~30 of them.  The timed calls that follow then see the sustained
+    clock, not that transient."""
+    import torch
+    t0 = time.perf_counter()
+    for _ in range(n):
+        fn()
+    torch.cuda.synchronize()
+    while (time.perf_counter() - t0) * 1e3 < WARMUP_MS[0]:
+        for _ in range(4):
+            fn()
+        torch.cuda.synchronize()
+
+
 def literal_iid(ca, w, args, stream, ev, v_layout):
     """The same step on literal iid N(0, 1) inputs (rho = 0, the other reading
     of the configs' "bf16 N(0,1) Q/K/V"): mean-pooled block scores are then
@@ -504,8 +526,7 @@ def literal_iid(ca, w, args, stream, ev, v_layout):
                            ws=aws)
 
     def timed(fn):
-        for _ in range(args.warmup):
-            fn()
+        warm(fn, args.warmup)
         torch.cuda.synchronize()
         a0, a1 = ev(), ev()
         a0.record(stream)
@@ -560,8 +581,7 @@ def threshold_sweep(ca, p, w, q, kp, vp, pt, dense_ms, args, stream, ev):
 
     res = []
     for tau, alpha in THRESHOLD_POINTS:
-        for _ in range(args.warmup):
-            step(tau, alpha)
+        warm(lambda: step(tau, alpha), args.warmup)
         torch.cuda.synchronize()
         t0, t1 = ev(), ev()
         t0.record(stream)
@@ -586,12 +606,13 @@ def threshold_sweep(ca, p, w, q, kp, vp, pt, dense_ms, args, stream, ev):
 
 def main():
     args = parse()
+    WARMUP_MS[0] = args.warmup_ms
     if args.copy_calibration:
         copy_calibration()
         return
     if args.gpus != 1:
         print("bench.py measures one GPU: the path shards by (sequence, KV group) with no "
-              "exchange, and multi-GPU runs are not part of this build; use --gpus 1.",
+              "exchange, and it runs on one GPU only; use --gpus 1.",
               file=sys.stderr)
         sys.exit(2)
     import torch
@@ -646,8 +667,7 @@ def main():
         if marks:
             marks[3].record(stream)
 
-    for _ in range(args.warmup):
-        step()
+    warm(step, args.warmup)
     torch.cuda.synchronize()
 
     # ---- timed region: K whole steps ----
@@ -677,8 +697,7 @@ def main():
         if marks:
             marks[2].record(stream)
 
-    for _ in range(args.warmup):
-        step_fused()
+    warm(step_fused, args.warmup)
     torch.cuda.synchronize()
     f0, f1 = ev(), ev()
     f0.record(stream)
@@ -710,9 +729,8 @@ def main():
 
     # ---- the attention kernel alone, K launches (roofline timing) ----
     ca.build_block_tables(p, bufs["masks"], gs, out=tables, ws=tws)
-    for _ in range(args.warmup):
-        ca.chunk_attention(p, q, (kp, vp), pt, tables, gs, w.sm_scale, num_splits=0, out=out,
-                           lse=lse, ws=aws)
+    warm(lambda: ca.chunk_attention(p, q, (kp, vp), pt, tables, gs, w.sm_scale, num_splits=0,
+                                    out=out, lse=lse, ws=aws), args.warmup)
     torch.cuda.synchronize()
     a0, a1 = ev(), ev()
     a0.record(stream)
@@ -728,8 +746,7 @@ def main():
     vp_o = v_of(other)
     run_o = lambda: ca.chunk_attention(p_o, q, (kp, vp_o), pt, tables, gs, w.sm_scale,
                                        num_splits=0, out=out, lse=lse, ws=aws)
-    for _ in range(args.warmup):
-        run_o()
+    warm(run_o, args.warmup)
     torch.cuda.synchronize()
     a0o, a1o = ev(), ev()
     a0o.record(stream)
@@ -749,8 +766,8 @@ def main():
 
     # ---- dense paged baseline ----
     dargs = dict(num_splits=0, out=out_dense, ws=dws)
-    for _ in range(args.warmup):
-        ca.dense_paged_chunk_attention(p, q, (kp, vp), pt, w.sm_scale, **dargs)
+    warm(lambda: ca.dense_paged_chunk_attention(p, q, (kp, vp), pt, w.sm_scale, **dargs),
+         args.warmup)
     torch.cuda.synchronize()
     ds, de = ev(), ev()
     ds.record(stream)
@@ -778,6 +795,7 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "warmup_ms": args.warmup_ms,
         "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": False,
         "scaling": "weak",

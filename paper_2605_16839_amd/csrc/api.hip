@@ -307,6 +307,25 @@ ca_status ca_pool_k_blocks(const ca_problem* p, const uint16_t* k_pool,
                     "pool_k launch");
 }
 
+// Both pooling stages in one launch, with the checks of ca_pool_q_blocks and
+// ca_pool_k_blocks.
+static ca_status pool_both(const ca_problem* p, const uint16_t* q, const uint16_t* k_pool,
+                           const int32_t* page_table, int32_t first_block, float* q_mean,
+                           float* k_mean, void* stream) {
+  ca::Dims d;
+  ca_status s = check(p, 0, &d);
+  if (s != CA_OK) return s;
+  if ((s = need_device(p)) != CA_OK) return s;
+  if (!q || !q_mean || !k_pool || !page_table || !k_mean)
+    return fail(CA_ERR_NULL, "q, q_mean, k_pool, page_table and k_mean are required");
+  if ((s = need_aligned16("q, q_mean, k_pool and k_mean", q, q_mean, k_pool, k_mean)) != CA_OK)
+    return s;
+  if (first_block < 0) return fail(CA_ERR_SHAPE, "first_block must be >= 0");
+  return hip_status(ca::launch_pool(d, q, q_mean, k_pool, page_table, p->cached_len, first_block,
+                                    k_mean, static_cast<hipStream_t>(stream)),
+                    "pool launch");
+}
+
 ca_status ca_block_scores(const ca_problem* p, const float* q_mean, const float* k_mean,
                           float* scores, void* stream) {
   ca::Dims d;
@@ -363,9 +382,8 @@ ca_status ca_estimate_masks(const ca_problem* p, const uint16_t* q, const uint16
   ca_status s = need_aligned16("q, k_pool, q_mean, k_mean and scores", q, k_pool, q_mean, k_mean,
                                scores);
   if (s != CA_OK) return s;
-  s = ca_pool_q_blocks(p, q, q_mean, stream);
-  if (s != CA_OK) return s;
-  if ((s = ca_pool_k_blocks(p, k_pool, page_table, k_mean_first_block, k_mean, stream)) != CA_OK)
+  if ((s = pool_both(p, q, k_pool, page_table, k_mean_first_block, q_mean, k_mean, stream)) !=
+      CA_OK)
     return s;
   if ((s = ca_block_scores(p, q_mean, k_mean, scores, stream)) != CA_OK) return s;
   return ca_select_blocks(p, scores, top_frac, sink_blocks, local_blocks, masks, stream);
@@ -404,9 +422,8 @@ ca_status ca_estimate_tables(const ca_problem* p, const uint16_t* q, const uint1
   if ((s = select_lds_ready(d)) != CA_OK) return s;
   const hipStream_t st = static_cast<hipStream_t>(stream);
   uint64_t* words = static_cast<uint64_t*>(ws);
-  hipError_t e = ca::launch_pool_q(d, q, q_mean, st, words, (int)((size_t)rows * d.W));
-  if (e == hipSuccess)
-    e = ca::launch_pool_k(d, k_pool, page_table, p->cached_len, k_mean_first_block, k_mean, st);
+  hipError_t e = ca::launch_pool(d, q, q_mean, k_pool, page_table, p->cached_len,
+                                 k_mean_first_block, k_mean, st, words, (int)((size_t)rows * d.W));
   if (e == hipSuccess) e = ca::launch_scores(d, q_mean, k_mean, p->cached_len, scores, st);
   if (e == hipSuccess)
     e = ca::launch_select(d, scores, p->cached_len, top_frac, sink_blocks, local_blocks, nullptr,
@@ -457,9 +474,8 @@ ca_status ca_estimate_masks_threshold(const ca_problem* p, const uint16_t* q,
   if ((s = need_aligned16("q, k_pool, q_mean, k_mean and scores", q, k_pool, q_mean, k_mean,
                           scores)) != CA_OK)
     return s;
-  s = ca_pool_q_blocks(p, q, q_mean, stream);
-  if (s != CA_OK) return s;
-  if ((s = ca_pool_k_blocks(p, k_pool, page_table, k_mean_first_block, k_mean, stream)) != CA_OK)
+  if ((s = pool_both(p, q, k_pool, page_table, k_mean_first_block, q_mean, k_mean, stream)) !=
+      CA_OK)
     return s;
   if ((s = ca_block_scores(p, q_mean, k_mean, scores, stream)) != CA_OK) return s;
   return ca_select_blocks_threshold(p, scores, alpha, temperature, sm_scale, sink_blocks,

@@ -37,8 +37,9 @@
 //     dropped (tables are ascending);
 //   * the workgroups of one table row run on one of the 8 XCDs and share its
 //     L2, so each page comes from HBM once; by default every row is cut in
-//     two so that the XCDs carry equal loads (xcd_split_kernel), the two
-//     pieces merged by combine_kernel.
+//     two so that the XCDs carry equal loads (xcd_cut, computed by each
+//     workgroup from the table lengths), the two pieces merged by
+//     combine_kernel.
 #include <type_traits>
 #include <utility>
 
@@ -76,14 +77,96 @@ struct AttnArgs {
   int table_mode;          // kTablesPerGroup / kTablesPerQTile / kTablesPacked
   long long packed_pages;  // capacity of the packed pools (kTablesPacked)
   float scale_log2;
-  // XCD-balanced two-piece split (splits == 2): table row r is cut at entry
-  // split_at[r]; -1 = not cut, run whole as piece 0; -2 = not cut, run whole
-  // as piece 1; nullptr = every row cut in the middle
-  const int32_t* split_at;
+  // XCD-balanced two-piece split (splits == 2) when not nullptr: every
+  // workgroup computes its row's cut point (xcd_cut), and the first tile's
+  // first piece stores it in split_at[r] for the combine: the cut entry, or
+  // -1 = not cut, run whole as piece 0; -2 = not cut, run whole as piece 1
+  int32_t* split_at;
   int rows_per_unit;   // table rows that read one KV head's pages together
 };
 
 constexpr int kXcds = 8;   // MI355X: 8 accelerator complex dies, 32 CUs and one L2 each
+
+// 64-bit lane exchanges as two 32-bit ones.
+__device__ __forceinline__ long long shfl_xor_i64(long long v, int mask) {
+  const int lo = __shfl_xor((int)(unsigned int)v, mask, 64);
+  const int hi = __shfl_xor((int)(v >> 32), mask, 64);
+  return (long long)(((unsigned long long)(unsigned int)hi << 32) | (unsigned int)lo);
+}
+// Lane src's value, as a wave-uniform (scalar) value.
+__device__ __forceinline__ long long readlane_i64(long long v, int src) {
+  const int lo = __builtin_amdgcn_readlane((int)(unsigned int)v, src);
+  const int hi = __builtin_amdgcn_readlane((int)(v >> 32), src);
+  return (long long)(((unsigned long long)(unsigned int)hi << 32) | (unsigned int)lo);
+}
+
+// Cut point of table row r in the XCD-balanced two-piece split, from the
+// table lengths (every lane of the calling wave gets the same value).  The
+// R = 8m table rows are spread over the 8 XCDs by r % 8: XCD x holds rows
+// x, x+8, .., its load alone is L_x table entries.  XCD x runs the first C_x
+// entries of its own rows and the remaining L_{x-1} - C_{x-1} of the previous
+// XCD's rows, so its load is C_x + L_{x-1} - C_{x-1}; equal loads S = sum L / 8
+// give C_x = C_{x-1} + S - L_{x-1}, fixed up to the choice of C_0.  Any C_0
+// that keeps every 0 <= C_x <= L_x balances exactly; the largest keeps the
+// most entries on their own XCD and leaves whole the rows of every XCD with
+// C_x = L_x (or 0).  When no such C_0 exists the cuts are clamped.  C_x is
+// shared among the rows of XCD x in proportion to their lengths.  Dense
+// tables: row r has nKB_b entries.  Returns the cut entry, -1 (not cut, whole
+// row in piece 0) or -2 (not cut, whole row in piece 1).
+template <bool DENSE>
+__device__ int xcd_cut(const AttnArgs& a, int r) {
+  const int lane = threadIdx.x & 63;
+  const int R = a.B * a.G;
+  auto row_len = [&](int q) -> long long {
+    return DENSE ? (long long)blocks_for(a.cached_len[q / a.G] + a.C)
+                 : (long long)(a.kv_indptr[q + 1] - a.kv_indptr[q]);
+  };
+  // lane l sums rows l, l + 64, ..: all on XCD l % 8; then the 8 lanes of
+  // each XCD meet, so every lane holds L_{lane % 8}
+  long long v = 0;
+  for (int q = lane; q < R; q += 64) v += row_len(q);
+  v += shfl_xor_i64(v, 8);
+  v += shfl_xor_i64(v, 16);
+  v += shfl_xor_i64(v, 32);
+  long long L[kXcds], total = 0;
+#pragma unroll
+  for (int x = 0; x < kXcds; ++x) {
+    L[x] = readlane_i64(v, x);
+    total += L[x];
+  }
+  // D_x = sum_{k=1..x} (S - L_{k-1}) in units of 1/8 entry (S = total / 8);
+  // the range of 8 C_0 that keeps 0 <= C_x <= L_x
+  long long D8[kXcds];
+  D8[0] = 0;
+#pragma unroll
+  for (int x = 1; x < kXcds; ++x) D8[x] = D8[x - 1] + total - 8 * L[x - 1];
+  long long lo = 0, hi = 8 * L[0];
+#pragma unroll
+  for (int x = 0; x < kXcds; ++x) {
+    lo = lo > -D8[x] ? lo : -D8[x];
+    hi = hi < 8 * L[x] - D8[x] ? hi : 8 * L[x] - D8[x];
+  }
+  const long long c0 = lo <= hi ? hi : (lo + hi) / 2;   // lo > hi: clamped below
+  const int xr = r % kXcds;
+  long long Lx = 0, Dx = 0;
+#pragma unroll
+  for (int x = 0; x < kXcds; ++x)
+    if (x == xr) Lx = L[x], Dx = D8[x];
+  long long cx = (c0 + Dx) / 8;
+  cx = cx < 0 ? 0 : (cx > Lx ? Lx : cx);
+  // C_x over the rows of XCD x in proportion to their lengths: the entries of
+  // the rows before r on the same XCD
+  long long before = 0;
+  for (int q = xr + kXcds * lane; q < r; q += kXcds * 64) before += row_len(q);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) before += shfl_xor_i64(before, o);
+  before = readlane_i64(before, 0);
+  const long long len = row_len(r);
+  const long long a0 = Lx > 0 ? (before * cx) / Lx : 0;
+  const long long a1 = Lx > 0 ? ((before + len) * cx) / Lx : 0;
+  const long long c = a1 - a0;
+  return c >= len ? -1 : (c <= 0 ? -2 : (int)c);
+}
 
 // LDS page tiles: K pages and token-major V pages are 64 key rows x D; a
 // transposed V page is D rows x 64 keys.
@@ -475,7 +558,8 @@ __global__ __launch_bounds__(64 * NW, NCT == 4 ? 1 : 2) void paged_attention_ker
   int e0, e1;
   bool whole = a.splits == 1;   // the piece is the whole row: final output
   if (a.split_at != nullptr) {
-    int cut = a.split_at[rowid];
+    int cut = xcd_cut<DENSE>(a, rowid);
+    if (sp == 0 && qt == 0 && t == 0) a.split_at[rowid] = cut;   // for the combine
     if (cut < 0) {              // the row is not cut: one piece runs it, the other nothing
       if (sp != (cut == -1 ? 0 : 1)) return;
       whole = true;
@@ -1080,68 +1164,6 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
   if (lse != nullptr && sub == 0) lse[row] = wsum > 0.f ? mx + logf(wsum) : -INFINITY;
 }
 
-// Cut points of the XCD-balanced two-piece split.  The R = 8m table rows are
-// spread over the 8 XCDs by r % 8 (XCD x holds rows x, x+8, ..; its load
-// alone is L_x table entries).  XCD x runs the first C_x
-// entries of its own rows and the remaining L_{x-1} - C_{x-1} of the previous
-// XCD's rows, so its load is C_x + L_{x-1} - C_{x-1}; equal loads S = sum L / 8
-// give C_x = C_{x-1} + S - L_{x-1}, fixed up to the choice of C_0, which is
-// taken in the middle of the range that keeps every 0 <= C_x <= L_x (clamped
-// when no such choice exists).  C_x is shared among the rows of XCD x in
-// proportion to their lengths.  Dense tables: row r has nKB_b entries.
-__global__ __launch_bounds__(256) void xcd_split_kernel(const int32_t* __restrict__ kv_indptr,
-                                                        const int32_t* __restrict__ cached_len,
-                                                        int32_t* __restrict__ split_at, int R,
-                                                        int G, int C, int dense) {
-  __shared__ long long L[kXcds], Cx[kXcds];
-  const int m = R / kXcds;
-  const int t = threadIdx.x;
-  auto row_len = [&](int r) -> long long {
-    return dense ? (long long)blocks_for(cached_len[r / G] + C)
-                 : (long long)(kv_indptr[r + 1] - kv_indptr[r]);
-  };
-  if (t < kXcds) {   // L_x, one thread per XCD
-    long long v = 0;
-    for (int k = 0; k < m; ++k) v += row_len(t + kXcds * k);
-    L[t] = v;
-  }
-  __syncthreads();
-  if (t == 0) {
-    long long total = 0;
-    for (int x = 0; x < kXcds; ++x) total += L[x];
-    // D_x = sum_{k=1..x} (S - L_{k-1}) in units of 1/8 entry (S = total / 8);
-    // 8 C_0 is taken in the middle of the range keeping 0 <= C_x <= L_x
-    long long D8[kXcds];
-    D8[0] = 0;
-    for (int x = 1; x < kXcds; ++x) D8[x] = D8[x - 1] + total - 8 * L[x - 1];
-    long long lo = 0, hi = 8 * L[0];
-    for (int x = 0; x < kXcds; ++x) {
-      lo = lo > -D8[x] ? lo : -D8[x];
-      hi = hi < 8 * L[x] - D8[x] ? hi : 8 * L[x] - D8[x];
-    }
-    // any feasible C_0 balances; the largest keeps the most entries on their
-    // own XCD, and rows with C_x = L_x (or 0) are not cut at all
-    const long long c0 = lo <= hi ? hi : (lo + hi) / 2;   // lo > hi: clamped below
-    for (int x = 0; x < kXcds; ++x) {
-      long long cx = (c0 + D8[x]) / 8;
-      Cx[x] = cx < 0 ? 0 : (cx > L[x] ? L[x] : cx);
-    }
-  }
-  __syncthreads();
-  if (t < kXcds) {   // C_x over the rows of XCD x in proportion to their lengths
-    long long before = 0;
-    for (int k = 0; k < m; ++k) {
-      const int r = t + kXcds * k;
-      const long long len = row_len(r);
-      const long long a0 = L[t] > 0 ? (before * Cx[t]) / L[t] : 0;
-      const long long a1 = L[t] > 0 ? ((before + len) * Cx[t]) / L[t] : 0;
-      const long long c = a1 - a0;
-      split_at[r] = c >= len ? -1 : (c <= 0 ? -2 : (int32_t)c);
-      before += len;
-    }
-  }
-}
-
 int attn_rows_per_workgroup(int table_mode) {
   return 16 * kColTiles * (table_mode == kTablesPerQTile ? kWavesQTile : kWavesGroup);
 }
@@ -1211,15 +1233,8 @@ hipError_t launch_attention(const Dims& d, const AttnLaunch& L, hipStream_t st) 
   a.scale_log2 = L.sm_scale * kLog2e;
   a.split_at = nullptr;
   a.rows_per_unit = L.table_mode == kTablesPerQTile ? d.Hq / d.Hkv : 1;
-  if (L.xcd_balanced) {
-    const int R = d.B * a.G;
-    int32_t* cut = reinterpret_cast<int32_t*>(static_cast<char*>(L.ws) + attn_ws_bytes(d, 2));
-    xcd_split_kernel<<<1, 256, 0, st>>>(L.kv_indptr, L.cached_len, cut, R, a.G, d.C,
-                                        L.dense ? 1 : 0);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    a.split_at = cut;
-  }
+  if (L.xcd_balanced)
+    a.split_at = reinterpret_cast<int32_t*>(static_cast<char*>(L.ws) + attn_ws_bytes(d, 2));
   const int nwg = attn_base_workgroups(d, L.group_size, L.table_mode) * L.splits;
   const bool qtile = L.table_mode == kTablesPerQTile;
   if (d.D == 128) {

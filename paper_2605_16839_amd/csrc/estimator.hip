@@ -14,8 +14,34 @@ namespace ca {
 // ---------------------------------------------------------------------------
 // Pooling: one wavefront reduces `rows` rows of D bf16 (row stride `stride`
 // elements) to their fp32 mean.  Lane l reads 16 bytes of row (l / CPR) +
-// k*RPI, so each load instruction covers RPI whole rows contiguously.
+// k*RPI, so each load instruction covers RPI whole rows contiguously; the
+// lane adds its rows in ascending k, then the lanes holding the same chunk
+// meet in a butterfly.
 // ---------------------------------------------------------------------------
+__device__ __forceinline__ void add_bf16x8(float (&acc)[8], const uint4& v) {
+  acc[0] += bf16_lo(v.x); acc[1] += bf16_hi(v.x);
+  acc[2] += bf16_lo(v.y); acc[3] += bf16_hi(v.y);
+  acc[4] += bf16_lo(v.z); acc[5] += bf16_hi(v.z);
+  acc[6] += bf16_lo(v.w); acc[7] += bf16_hi(v.w);
+}
+
+template <int D>
+__device__ __forceinline__ void pool_store(float (&acc)[8], float* __restrict__ out, float scale) {
+  constexpr int CPR = D / 8;
+  const int l = lane_id();
+#pragma unroll
+  for (int o = CPR; o < kWave; o <<= 1) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] += __shfl_xor(acc[e], o, kWave);
+  }
+  if (l < CPR) {
+    float4* dst = reinterpret_cast<float4*>(out + (l % CPR) * 8);
+    dst[0] = make_float4(acc[0] * scale, acc[1] * scale, acc[2] * scale, acc[3] * scale);
+    dst[1] = make_float4(acc[4] * scale, acc[5] * scale, acc[6] * scale, acc[7] * scale);
+  }
+}
+
+// Any row count: one load per step of the loop.
 template <int D>
 __device__ __forceinline__ void pool_rows(const uint16_t* __restrict__ base, size_t stride,
                                           int rows, float* __restrict__ out, float scale) {
@@ -26,76 +52,94 @@ __device__ __forceinline__ void pool_rows(const uint16_t* __restrict__ base, siz
   float acc[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) acc[e] = 0.f;
-  for (int r = l / CPR; r < rows; r += RPI) {
-    const uint4 v = *reinterpret_cast<const uint4*>(base + (size_t)r * stride + chunk * 8);
-    acc[0] += bf16_lo(v.x); acc[1] += bf16_hi(v.x);
-    acc[2] += bf16_lo(v.y); acc[3] += bf16_hi(v.y);
-    acc[4] += bf16_lo(v.z); acc[5] += bf16_hi(v.z);
-    acc[6] += bf16_lo(v.w); acc[7] += bf16_hi(v.w);
-  }
-#pragma unroll
-  for (int o = CPR; o < kWave; o <<= 1) {
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc[e] += __shfl_xor(acc[e], o, kWave);
-  }
-  if (l < CPR) {
-    float4* dst = reinterpret_cast<float4*>(out + chunk * 8);
-    dst[0] = make_float4(acc[0] * scale, acc[1] * scale, acc[2] * scale, acc[3] * scale);
-    dst[1] = make_float4(acc[4] * scale, acc[5] * scale, acc[6] * scale, acc[7] * scale);
-  }
+  for (int r = l / CPR; r < rows; r += RPI)
+    add_bf16x8(acc, *reinterpret_cast<const uint4*>(base + (size_t)r * stride + chunk * 8));
+  pool_store<D>(acc, out, scale);
 }
 
-// One workgroup per (b, h, i): each wave sums a quarter of the Q-block's rows,
-// the four partial sums meet in LDS.  In the fused estimator-to-union path
-// this first stage also clears the group union words that the selection
-// ORs into (clear_words, n_clear; none otherwise).
+// Exactly N * RPI rows: all N loads are issued before the first add, so a
+// wave keeps N 16-byte loads per lane in flight instead of one (same adds,
+// same order as pool_rows).
+template <int D, int N>
+__device__ __forceinline__ void pool_rows_n(const uint16_t* __restrict__ base, size_t stride,
+                                            float* __restrict__ out, float scale) {
+  constexpr int CPR = D / 8;
+  constexpr int RPI = kWave / CPR;
+  const int l = lane_id();
+  const uint16_t* src = base + (size_t)(l / CPR) * stride + (l % CPR) * 8;
+  uint4 v[N];
+#pragma unroll
+  for (int k = 0; k < N; ++k) v[k] = *reinterpret_cast<const uint4*>(src + (size_t)k * RPI * stride);
+  float acc[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) acc[e] = 0.f;
+#pragma unroll
+  for (int k = 0; k < N; ++k) add_bf16x8(acc, v[k]);
+  pool_store<D>(acc, out, scale);
+}
+
+// One launch pools both operands of the scores:
+//   * workgroups [0, n_q_wg): one per (b, h, i) Q-block; each wave sums a
+//     quarter of the block's rows and the four partial sums meet in LDS (the
+//     chunk's last Q-block may hold fewer rows; its mean is over those);
+//   * the rest: 4 waves per workgroup, one K block (b, kvh, j) per wave, j in
+//     [first_block, nKB_b); a sequence's last block is pooled over its rows
+//     before the sequence end only.
+// In the fused estimator-to-union path the launch also clears the group union
+// words that the selection ORs into (clear_words, n_clear; none otherwise).
+struct PoolArgs {
+  const uint16_t* q;
+  float* q_mean;
+  int B, C, Hq, q_block, nqb, n_q_wg;
+  uint64_t* clear_words;
+  int n_clear;
+  const uint16_t* k_pool;
+  const int32_t* page_table;
+  const int32_t* cached_len;
+  float* k_mean;
+  int Hkv, max_kv_blocks, first_block, k_tiles;   // k_tiles workgroups per (b, kvh)
+};
+
 template <int D>
-__global__ __launch_bounds__(256) void pool_q_kernel(const uint16_t* __restrict__ q,
-                                                     float* __restrict__ q_mean, int B, int C,
-                                                     int Hq, int q_block, int nqb,
-                                                     uint64_t* __restrict__ clear_words,
-                                                     int n_clear) {
+__global__ __launch_bounds__(256) void pool_kernel(const PoolArgs a) {
   __shared__ __attribute__((aligned(16))) float part[4][D];
-  for (int x = blockIdx.x * 256 + threadIdx.x; x < n_clear; x += gridDim.x * 256)
-    clear_words[x] = 0ull;
-  const int w = blockIdx.x;
-  const int i = w % nqb;
-  const int h = (w / nqb) % Hq;
-  const int b = w / (nqb * Hq);
+  constexpr int RPI = kWave / (D / 8);
+  for (int x = blockIdx.x * 256 + threadIdx.x; x < a.n_clear; x += gridDim.x * 256)
+    a.clear_words[x] = 0ull;
   const int wv = threadIdx.x >> 6;
-  const int quarter = q_block / 4;
-  // the chunk's last Q-block may hold fewer rows; its mean is over those
-  const int n_valid = C - i * q_block < q_block ? C - i * q_block : q_block;
-  int rows = n_valid - wv * quarter;
-  rows = rows < 0 ? 0 : (rows > quarter ? quarter : rows);
-  const uint16_t* base =
-      q + (((size_t)b * C + (size_t)i * q_block + (size_t)wv * quarter) * Hq + h) * D;
-  pool_rows<D>(base, (size_t)Hq * D, rows, part[wv], 1.0f);
-  __syncthreads();
-  const int t = threadIdx.x;
-  if (t < D)
-    q_mean[(size_t)w * D + t] = ((part[0][t] + part[1][t]) + (part[2][t] + part[3][t])) *
-                                (1.0f / (float)n_valid);
-}
-
-// One wave per (b, kvh, j), j in [first_block, nKB_b).  A sequence's last
-// block is pooled over its rows before the sequence end only.
-template <int D>
-__global__ __launch_bounds__(256) void pool_k_kernel(const uint16_t* __restrict__ k_pool,
-                                                     const int32_t* __restrict__ page_table,
-                                                     const int32_t* __restrict__ cached_len,
-                                                     float* __restrict__ k_mean, int Hkv,
-                                                     int max_kv_blocks, int C,
-                                                     int first_block) {
-  const int bk = blockIdx.y;  // b * Hkv + kvh
-  const int b = bk / Hkv;
-  const int j = first_block + blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int seq = cached_len[b] + C;
+  if ((int)blockIdx.x < a.n_q_wg) {
+    const int w = blockIdx.x;
+    const int i = w % a.nqb;
+    const int h = (w / a.nqb) % a.Hq;
+    const int b = w / (a.nqb * a.Hq);
+    const int quarter = a.q_block / 4;
+    const int n_valid = a.C - i * a.q_block < a.q_block ? a.C - i * a.q_block : a.q_block;
+    int rows = n_valid - wv * quarter;
+    rows = rows < 0 ? 0 : (rows > quarter ? quarter : rows);
+    const uint16_t* base =
+        a.q + (((size_t)b * a.C + (size_t)i * a.q_block + (size_t)wv * quarter) * a.Hq + h) * D;
+    const size_t stride = (size_t)a.Hq * D;
+    if (rows == 8 * RPI) pool_rows_n<D, 8>(base, stride, part[wv], 1.0f);
+    else pool_rows<D>(base, stride, rows, part[wv], 1.0f);
+    __syncthreads();
+    const int t = threadIdx.x;
+    if (t < D)
+      a.q_mean[(size_t)w * D + t] = ((part[0][t] + part[1][t]) + (part[2][t] + part[3][t])) *
+                                    (1.0f / (float)n_valid);
+    return;
+  }
+  const int kw = blockIdx.x - a.n_q_wg;
+  const int bk = kw / a.k_tiles;   // b * Hkv + kvh
+  const int b = bk / a.Hkv;
+  const int j = a.first_block + (kw % a.k_tiles) * 4 + wv;
+  const int seq = a.cached_len[b] + a.C;
   if (j >= blocks_for(seq)) return;
   const int rows = seq - kPage * j < kPage ? seq - kPage * j : kPage;
-  const int page = page_table[(size_t)bk * max_kv_blocks + j];
-  pool_rows<D>(k_pool + (size_t)page * kPage * D, D, rows,
-               k_mean + ((size_t)bk * max_kv_blocks + j) * D, 1.0f / (float)rows);
+  const int page = a.page_table[(size_t)bk * a.max_kv_blocks + j];
+  const uint16_t* base = a.k_pool + (size_t)page * kPage * D;
+  float* out = a.k_mean + ((size_t)bk * a.max_kv_blocks + j) * D;
+  if (rows == kPage) pool_rows_n<D, kPage / RPI>(base, D, out, 1.0f / (float)kPage);
+  else pool_rows<D>(base, D, rows, out, 1.0f / (float)rows);
 }
 
 // ---------------------------------------------------------------------------
@@ -125,21 +169,35 @@ __global__ __launch_bounds__(256) void scores_kernel(const float* __restrict__ q
   const float* qrow = q_mean + row_base * D;
   const float* krow = k_mean + ((size_t)bk * max_kv_blocks) * D;
   const int t = threadIdx.x;
-  for (int x = t; x < TR * D / 4; x += 256) {
-    const int r = x / (D / 4), d4 = x % (D / 4);
-    const float4 v = (r0 + r < nrows)
-                         ? *reinterpret_cast<const float4*>(qrow + (size_t)(r0 + r) * D + 4 * d4)
-                         : make_float4(0.f, 0.f, 0.f, 0.f);
-    qs[r][4 * d4 + 0] = v.x; qs[r][4 * d4 + 1] = v.y;
-    qs[r][4 * d4 + 2] = v.z; qs[r][4 * d4 + 3] = v.w;
+  // every load of the two tiles is issued before the first LDS store, so a
+  // lane has all of them in flight at once
+  constexpr int QL = TR * D / 4 / 256, KL = TB * D / 4 / 256;
+  float4 qv[QL], kv[KL];
+#pragma unroll
+  for (int m = 0; m < QL; ++m) {
+    const int x = t + 256 * m, r = x / (D / 4), d4 = x % (D / 4);
+    qv[m] = (r0 + r < nrows)
+                ? *reinterpret_cast<const float4*>(qrow + (size_t)(r0 + r) * D + 4 * d4)
+                : make_float4(0.f, 0.f, 0.f, 0.f);
   }
-  for (int x = t; x < TB * D / 4; x += 256) {
-    const int r = x / (D / 4), d4 = x % (D / 4);
-    const float4 v = (j0 + r < nc)
-                         ? *reinterpret_cast<const float4*>(krow + (size_t)(j0 + r) * D + 4 * d4)
-                         : make_float4(0.f, 0.f, 0.f, 0.f);
-    ks[r][4 * d4 + 0] = v.x; ks[r][4 * d4 + 1] = v.y;
-    ks[r][4 * d4 + 2] = v.z; ks[r][4 * d4 + 3] = v.w;
+#pragma unroll
+  for (int m = 0; m < KL; ++m) {
+    const int x = t + 256 * m, r = x / (D / 4), d4 = x % (D / 4);
+    kv[m] = (j0 + r < nc)
+                ? *reinterpret_cast<const float4*>(krow + (size_t)(j0 + r) * D + 4 * d4)
+                : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+#pragma unroll
+  for (int m = 0; m < QL; ++m) {
+    const int x = t + 256 * m, r = x / (D / 4), d4 = x % (D / 4);
+    qs[r][4 * d4 + 0] = qv[m].x; qs[r][4 * d4 + 1] = qv[m].y;
+    qs[r][4 * d4 + 2] = qv[m].z; qs[r][4 * d4 + 3] = qv[m].w;
+  }
+#pragma unroll
+  for (int m = 0; m < KL; ++m) {
+    const int x = t + 256 * m, r = x / (D / 4), d4 = x % (D / 4);
+    ks[r][4 * d4 + 0] = kv[m].x; ks[r][4 * d4 + 1] = kv[m].y;
+    ks[r][4 * d4 + 2] = kv[m].z; ks[r][4 * d4 + 3] = kv[m].w;
   }
   __syncthreads();
   const int bc = t & 15, rg = t >> 4;   // blocks bc, bc+16; rows rg + 16a
@@ -222,7 +280,20 @@ __global__ __launch_bounds__(256) void select_kernel(const float* __restrict__ s
     k = k < 0 ? 0 : (k > nc ? nc : k);
   }
   const float* s = scores + (size_t)row * max_kv_blocks;
-  for (int j = t; j < nc; j += 256) keys[j] = order_key(s[j]);
+  // 8 loads per lane in flight per round (2048 scores)
+  for (int j0 = 0; j0 < nc; j0 += 8 * 256) {
+    float v[8];
+#pragma unroll
+    for (int m = 0; m < 8; ++m) {
+      const int j = j0 + t + 256 * m;
+      v[m] = j < nc ? s[j] : 0.f;
+    }
+#pragma unroll
+    for (int m = 0; m < 8; ++m) {
+      const int j = j0 + t + 256 * m;
+      if (j < nc) keys[j] = order_key(v[m]);
+    }
+  }
   __syncthreads();
 
   const bool take_all = (k == nc);
@@ -337,31 +408,49 @@ __global__ __launch_bounds__(256) void threshold_select_kernel(
 // ---------------------------------------------------------------------------
 // launchers
 // ---------------------------------------------------------------------------
+// q == nullptr: no Q pooling; k_pool == nullptr: no K pooling.
+hipError_t launch_pool(const Dims& d, const uint16_t* q, float* q_mean, const uint16_t* k_pool,
+                       const int32_t* page_table, const int32_t* cached_len, int first_block,
+                       float* k_mean, hipStream_t st, uint64_t* clear_words, int n_clear) {
+  PoolArgs a;
+  a.q = q;
+  a.q_mean = q_mean;
+  a.B = d.B;
+  a.C = d.C;
+  a.Hq = d.Hq;
+  a.q_block = d.q_block;
+  a.nqb = d.nqb;
+  a.n_q_wg = q != nullptr ? d.B * d.Hq * d.nqb : 0;
+  a.clear_words = clear_words;
+  a.n_clear = n_clear;
+  a.k_pool = k_pool;
+  a.page_table = page_table;
+  a.cached_len = cached_len;
+  a.k_mean = k_mean;
+  a.Hkv = d.Hkv;
+  a.max_kv_blocks = d.max_kv_blocks;
+  a.first_block = first_block;
+  const int span = d.max_nkb - first_block;
+  a.k_tiles = k_pool != nullptr && span > 0 ? (span + 3) / 4 : 0;
+  const long long nwg = (long long)a.n_q_wg + (long long)a.k_tiles * d.B * d.Hkv;
+  if (nwg == 0) return hipSuccess;
+  if (nwg > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+  if (d.D == 128) pool_kernel<128><<<(int)nwg, 256, 0, st>>>(a);
+  else pool_kernel<64><<<(int)nwg, 256, 0, st>>>(a);
+  return hipGetLastError();
+}
+
 hipError_t launch_pool_q(const Dims& d, const uint16_t* q, float* q_mean, hipStream_t st,
                          uint64_t* clear_words, int n_clear) {
-  dim3 grid(d.B * d.Hq * d.nqb);
-  if (d.D == 128)
-    pool_q_kernel<128><<<grid, 256, 0, st>>>(q, q_mean, d.B, d.C, d.Hq, d.q_block, d.nqb,
-                                             clear_words, n_clear);
-  else
-    pool_q_kernel<64><<<grid, 256, 0, st>>>(q, q_mean, d.B, d.C, d.Hq, d.q_block, d.nqb,
-                                            clear_words, n_clear);
-  return hipGetLastError();
+  return launch_pool(d, q, q_mean, nullptr, nullptr, nullptr, 0, nullptr, st, clear_words,
+                     n_clear);
 }
 
 hipError_t launch_pool_k(const Dims& d, const uint16_t* k_pool, const int32_t* page_table,
                          const int32_t* cached_len, int first_block, float* k_mean,
                          hipStream_t st) {
-  const int span = d.max_nkb - first_block;
-  if (span <= 0) return hipSuccess;
-  dim3 grid((span + 3) / 4, d.B * d.Hkv);
-  if (d.D == 128)
-    pool_k_kernel<128><<<grid, 256, 0, st>>>(k_pool, page_table, cached_len, k_mean, d.Hkv,
-                                             d.max_kv_blocks, d.C, first_block);
-  else
-    pool_k_kernel<64><<<grid, 256, 0, st>>>(k_pool, page_table, cached_len, k_mean, d.Hkv,
-                                            d.max_kv_blocks, d.C, first_block);
-  return hipGetLastError();
+  return launch_pool(d, nullptr, nullptr, k_pool, page_table, cached_len, first_block, k_mean,
+                     st, nullptr, 0);
 }
 
 hipError_t launch_scores(const Dims& d, const float* q_mean, const float* k_mean,

@@ -14,6 +14,12 @@ struct Dims {
   int max_nkb;       // max_b blocks of the sequence, ceil((cached_len_b + C) / page)
 };
 
+// Q-block and K-block pooling in one launch (q or k_pool may be nullptr to
+// skip that part); clear_words[0, n_clear) are zeroed by the same launch.
+hipError_t launch_pool(const Dims& d, const uint16_t* q, float* q_mean, const uint16_t* k_pool,
+                       const int32_t* page_table, const int32_t* cached_len, int first_block,
+                       float* k_mean, hipStream_t st, uint64_t* clear_words = nullptr,
+                       int n_clear = 0);
 hipError_t launch_pool_q(const Dims& d, const uint16_t* q, float* q_mean, hipStream_t st,
                          uint64_t* clear_words = nullptr, int n_clear = 0);
 hipError_t launch_pool_k(const Dims& d, const uint16_t* k_pool, const int32_t* page_table,

@@ -36,9 +36,19 @@ __global__ __launch_bounds__(256) void union_kernel(const uint64_t* __restrict__
   const uint64_t* src = masks + ((size_t)b * Hq + (size_t)g * group_size) * nqb * W;
   if (W <= 256 && (256 % W) == 0) {
     // fixed word per thread: OR privately, then one LDS atomic
-    const int w = t % W;
+    // 8 loads per lane in flight per round
+    const int w = t % W, step = 256 / W;
     unsigned long long v = 0ull;
-    for (int row = t / W; row < rows; row += 256 / W) v |= src[(size_t)row * W + w];
+    for (int row0 = t / W; row0 < rows; row0 += 8 * step) {
+      unsigned long long x[8];
+#pragma unroll
+      for (int m = 0; m < 8; ++m) {
+        const int row = row0 + m * step;
+        x[m] = row < rows ? src[(size_t)row * W + w] : 0ull;
+      }
+#pragma unroll
+      for (int m = 0; m < 8; ++m) v |= x[m];
+    }
     if (v) atomicOr(&acc[w], v);
   } else {
     for (int x = t; x < rows * W; x += 256) {
