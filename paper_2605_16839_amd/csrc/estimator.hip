@@ -4,8 +4,9 @@
 // The paper plugs any lightweight block-level pattern search in front of the
 // block union (Sec. 3.1, Sec. 3.2 first paragraph); per-chunk search cost is
 // first-order under chunked prefill (Sec. 2.1), so every stage here is a
-// single streaming pass: pooling is HBM-bound, scores are a tiny fp32
-// contraction, selection is an in-LDS radix select per mask row.
+// single streaming pass: pooling is HBM-bound, scores are a small fp32
+// contraction on the matrix cores, selection is an in-LDS radix select per
+// mask row.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -144,85 +145,62 @@ __global__ __launch_bounds__(256) void pool_kernel(const PoolArgs a) {
 
 // ---------------------------------------------------------------------------
 // Scores: for one (b, kvh), the ratio*nQB pooled query rows are contiguous in
-// q_mean and the matching score rows are contiguous too.  A workgroup
-// computes a 64-row x 32-block tile with fp32 FMAs (d ascending) from whole
-// rows of both operands staged in LDS; lanes 0..15 of a row group own 16
-// consecutive blocks, so the score stores are contiguous.
+// q_mean and the matching score rows are contiguous too.  One wave computes a
+// 32-row x 32-block tile with fp32 matrix instructions (v_mfma_f32_32x32x2_f32,
+// fp32 products and sums), its operands loaded straight into registers: lane
+// l holds row / block l % 32 and, for k-step (t, e), element
+// d = 8t + 4(l / 32) + e of both operands (the contraction over d may take
+// the d in any order as long as both operands share it), so each lane loads
+// its two rows as D/8 float4 pairs.  Four waves per workgroup.
 // ---------------------------------------------------------------------------
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
 template <int D>
 __global__ __launch_bounds__(256) void scores_kernel(const float* __restrict__ q_mean,
                                                      const float* __restrict__ k_mean,
                                                      const int32_t* __restrict__ cached_len,
                                                      float* __restrict__ scores, int Hq, int Hkv,
-                                                     int nqb, int max_kv_blocks) {
-  constexpr int TR = 64, TB = 32;
-  __shared__ float qs[TR][D + 1];
-  __shared__ float ks[TB][D + 1];
-  const int bk = blockIdx.z;
+                                                     int nqb, int max_kv_blocks, int n_jt) {
+  constexpr int NT = D / 8;
+  const int bk = blockIdx.y;
   const int b = bk / Hkv, kvh = bk % Hkv;
   const int ratio = Hq / Hkv;
   const int nrows = ratio * nqb;
   const int nc = cached_len[b] / kPage;
-  const int j0 = blockIdx.x * TB, r0 = blockIdx.y * TR;
-  if (j0 >= nc) return;
+  const int l = threadIdx.x & 63;
+  const int tile = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int n_rt = (nrows + 31) / 32;
+  const int rt = tile % n_rt, jt = tile / n_rt;
+  const int r0 = rt * 32, j0 = jt * 32;
+  if (jt >= n_jt || j0 >= nc) return;   // whole wave
   const size_t row_base = ((size_t)b * Hq + (size_t)kvh * ratio) * nqb;
-  const float* qrow = q_mean + row_base * D;
-  const float* krow = k_mean + ((size_t)bk * max_kv_blocks) * D;
-  const int t = threadIdx.x;
-  // every load of the two tiles is issued before the first LDS store, so a
-  // lane has all of them in flight at once
-  constexpr int QL = TR * D / 4 / 256, KL = TB * D / 4 / 256;
-  float4 qv[QL], kv[KL];
+  const int i = l & 31, h = l >> 5;
+  const bool q_ok = r0 + i < nrows, k_ok = j0 + i < nc;
+  const float* qrow = q_mean + (row_base + (q_ok ? r0 + i : 0)) * D + 4 * h;
+  const float* krow = k_mean + ((size_t)bk * max_kv_blocks + (k_ok ? j0 + i : 0)) * D + 4 * h;
+  float4 qa[NT], kb[NT];
 #pragma unroll
-  for (int m = 0; m < QL; ++m) {
-    const int x = t + 256 * m, r = x / (D / 4), d4 = x % (D / 4);
-    qv[m] = (r0 + r < nrows)
-                ? *reinterpret_cast<const float4*>(qrow + (size_t)(r0 + r) * D + 4 * d4)
-                : make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int t = 0; t < NT; ++t) {
+    qa[t] = q_ok ? *reinterpret_cast<const float4*>(qrow + 8 * t) : make_float4(0.f, 0.f, 0.f, 0.f);
+    kb[t] = k_ok ? *reinterpret_cast<const float4*>(krow + 8 * t) : make_float4(0.f, 0.f, 0.f, 0.f);
   }
+  f32x16 acc;
 #pragma unroll
-  for (int m = 0; m < KL; ++m) {
-    const int x = t + 256 * m, r = x / (D / 4), d4 = x % (D / 4);
-    kv[m] = (j0 + r < nc)
-                ? *reinterpret_cast<const float4*>(krow + (size_t)(j0 + r) * D + 4 * d4)
-                : make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int v = 0; v < 16; ++v) acc[v] = 0.f;
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qa[t].x, kb[t].x, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qa[t].y, kb[t].y, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qa[t].z, kb[t].z, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qa[t].w, kb[t].w, acc, 0, 0, 0);
   }
+  // result v of lane l: row 8(v/4) + 4(l/32) + v%4 of the tile, block l % 32
+  const int j = j0 + i;
+  if (j >= nc) return;
 #pragma unroll
-  for (int m = 0; m < QL; ++m) {
-    const int x = t + 256 * m, r = x / (D / 4), d4 = x % (D / 4);
-    qs[r][4 * d4 + 0] = qv[m].x; qs[r][4 * d4 + 1] = qv[m].y;
-    qs[r][4 * d4 + 2] = qv[m].z; qs[r][4 * d4 + 3] = qv[m].w;
-  }
-#pragma unroll
-  for (int m = 0; m < KL; ++m) {
-    const int x = t + 256 * m, r = x / (D / 4), d4 = x % (D / 4);
-    ks[r][4 * d4 + 0] = kv[m].x; ks[r][4 * d4 + 1] = kv[m].y;
-    ks[r][4 * d4 + 2] = kv[m].z; ks[r][4 * d4 + 3] = kv[m].w;
-  }
-  __syncthreads();
-  const int bc = t & 15, rg = t >> 4;   // blocks bc, bc+16; rows rg + 16a
-  float acc[4][2];
-#pragma unroll
-  for (int a = 0; a < 4; ++a) { acc[a][0] = 0.f; acc[a][1] = 0.f; }
-#pragma unroll 8
-  for (int d = 0; d < D; ++d) {
-    const float k0 = ks[bc][d], k1 = ks[bc + 16][d];
-#pragma unroll
-    for (int a = 0; a < 4; ++a) {
-      const float qv = qs[rg + 16 * a][d];
-      acc[a][0] = fmaf(qv, k0, acc[a][0]);
-      acc[a][1] = fmaf(qv, k1, acc[a][1]);
-    }
-  }
-#pragma unroll
-  for (int a = 0; a < 4; ++a) {
-    const int r = r0 + rg + 16 * a;
-    if (r >= nrows) continue;
-#pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      const int j = j0 + bc + 16 * c;
-      if (j < nc) scores[(row_base + r) * max_kv_blocks + j] = acc[a][c];
-    }
+  for (int v = 0; v < 16; ++v) {
+    const int r = r0 + 8 * (v / 4) + 4 * h + (v % 4);
+    if (r < nrows) scores[(row_base + r) * max_kv_blocks + j] = acc[v];
   }
 }
 
@@ -457,13 +435,15 @@ hipError_t launch_scores(const Dims& d, const float* q_mean, const float* k_mean
                          const int32_t* cached_len, float* scores, hipStream_t st) {
   if (d.max_nc <= 0) return hipSuccess;
   const int nrows = (d.Hq / d.Hkv) * d.nqb;
-  dim3 grid((d.max_nc + 31) / 32, (nrows + 63) / 64, d.B * d.Hkv);
+  const int n_jt = (d.max_nc + 31) / 32;
+  const int tiles = ((nrows + 31) / 32) * n_jt;
+  dim3 grid((tiles + 3) / 4, d.B * d.Hkv);
   if (d.D == 128)
     scores_kernel<128><<<grid, 256, 0, st>>>(q_mean, k_mean, cached_len, scores, d.Hq, d.Hkv,
-                                             d.nqb, d.max_kv_blocks);
+                                             d.nqb, d.max_kv_blocks, n_jt);
   else
     scores_kernel<64><<<grid, 256, 0, st>>>(q_mean, k_mean, cached_len, scores, d.Hq, d.Hkv,
-                                            d.nqb, d.max_kv_blocks);
+                                            d.nqb, d.max_kv_blocks, n_jt);
   return hipGetLastError();
 }
 
