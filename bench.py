@@ -28,6 +28,7 @@ if ROOT not in sys.path:
 
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+PEAK_CLOCK_MHZ = 2400.0       # MI355X peak engine clock the bf16 peak is rated at
 
 
 def parse():
@@ -467,6 +468,78 @@ def host_ahead(torch):
     torch.cuda._sleep(1_000_000)
 
 
+class PowerSampler:
+    """Reads the board power, its cap, the hotspot temperature and the current
+    GFX DPM clock from sysfs every few ms on a host thread while a timed loop
+    runs (no GPU call, nothing spawned).  Fields the node does not expose are
+    left out."""
+
+    def __init__(self, period_s=0.005):
+        import glob
+        import threading
+        self.period = period_s
+        self.dev = None
+        for d in sorted(glob.glob("/sys/class/drm/card*/device")):
+            if glob.glob(d + "/hwmon/hwmon*/power1_cap"):
+                self.dev = d
+                break
+        self.samples = []
+        self._stop = threading.Event()
+        self._t = threading.Thread(target=self._run, daemon=True)
+
+    def _read(self, pattern):
+        import glob
+        for f in glob.glob(self.dev + pattern):
+            try:
+                with open(f) as fh:
+                    return fh.read()
+            except OSError:
+                return None
+        return None
+
+    def _run(self):
+        while not self._stop.is_set():
+            s = {}
+            v = self._read("/hwmon/hwmon*/power1_input") or self._read("/hwmon/hwmon*/power1_average")
+            if v:
+                s["w"] = int(v) / 1e6
+            v = self._read("/hwmon/hwmon*/temp2_input")
+            if v:
+                s["c"] = int(v) / 1e3
+            v = self._read("/pp_dpm_sclk")
+            if v:
+                for line in v.splitlines():
+                    if line.strip().endswith("*"):
+                        num = "".join(ch for ch in line.split(":", 1)[-1] if ch.isdigit())
+                        if num:
+                            s["mhz"] = int(num)
+            self.samples.append(s)
+            self._stop.wait(self.period)
+
+    def __enter__(self):
+        if self.dev is not None:
+            self._t.start()
+        return self
+
+    def __exit__(self, *exc):
+        if self.dev is not None:
+            self._stop.set()
+            self._t.join()
+
+    def summary(self):
+        if self.dev is None or not self.samples:
+            return None
+        cap = self._read("/hwmon/hwmon*/power1_cap")
+        out = {"samples": len(self.samples)}
+        if cap:
+            out["cap_w"] = round(int(cap) / 1e6, 1)
+        for k, name in (("w", "median_w"), ("c", "median_hotspot_c"), ("mhz", "median_dpm_sclk_mhz")):
+            v = [x[k] for x in self.samples if k in x]
+            if v:
+                out[name] = round(float(np.median(v)), 1)
+        return out
+
+
 # Set from --warmup-ms in main().
 WARMUP_MS = [300.0]
 
@@ -729,16 +802,18 @@ def main():
 
     # ---- the attention kernel alone, K launches (roofline timing) ----
     ca.build_block_tables(p, bufs["masks"], gs, out=tables, ws=tws)
-    warm(lambda: ca.chunk_attention(p, q, (kp, vp), pt, tables, gs, w.sm_scale, num_splits=0,
-                                    out=out, lse=lse, ws=aws), args.warmup)
-    torch.cuda.synchronize()
-    a0, a1 = ev(), ev()
-    a0.record(stream)
-    for _ in range(args.steps):
-        ca.chunk_attention(p, q, (kp, vp), pt, tables, gs, w.sm_scale, num_splits=0, out=out,
-                           lse=lse, ws=aws)
-    a1.record(stream)
-    torch.cuda.synchronize()
+    # board power, cap and clock sampled over the warm-up and the timed launches
+    with PowerSampler() as power:
+        warm(lambda: ca.chunk_attention(p, q, (kp, vp), pt, tables, gs, w.sm_scale,
+                                        num_splits=0, out=out, lse=lse, ws=aws), args.warmup)
+        torch.cuda.synchronize()
+        a0, a1 = ev(), ev()
+        a0.record(stream)
+        for _ in range(args.steps):
+            ca.chunk_attention(p, q, (kp, vp), pt, tables, gs, w.sm_scale, num_splits=0,
+                               out=out, lse=lse, ws=aws)
+        a1.record(stream)
+        torch.cuda.synchronize()
     attn_ms = a0.elapsed_time(a1) / args.steps
     # the same launches on a pool in the other V page layout (bit-identical output)
     other = ca.V_TOKEN_MAJOR if v_layout == ca.V_TRANSPOSED else ca.V_TRANSPOSED
@@ -833,7 +908,13 @@ def main():
                      "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
                    "traffic": measured_traffic()},
         "kernel_source_sha256_16": kernel_source_hash(),
+        "attention_board_power": power.summary(),
     }
+    bp = res["attention_board_power"]
+    if bp and bp.get("median_dpm_sclk_mhz"):
+        # the same launches against the peak scaled to the clock they ran at
+        bp["frac_of_peak_at_sampled_clock"] = round(
+            attn_tflops / (PEAK_BF16_TFLOPS * bp["median_dpm_sclk_mhz"] / PEAK_CLOCK_MHZ), 4)
     if not args.no_arms:
         res["arms"] = strategy_arms(ca, p, w, q, kp, vp, pt, bufs["masks"], tables, ip,
                                     args, stream, ev)
