@@ -69,7 +69,8 @@
  *   block ids in kv_indices[kv_indptr[r] .. kv_indptr[r+1]).
  * - `stream` is a hipStream_t (NULL = the default stream).  Every call only
  *   enqueues work on it and returns without synchronising, except
- *   ca_validate_tables.
+ *   ca_validate_tables (and the attention calls of the debug build, see
+ *   ca_check_tables_host).
  * - Argument and shape errors are reported before anything is enqueued; a
  *   failed launch returns CA_ERR_HIP with the HIP error text available from
  *   ca_last_error_detail().
@@ -84,7 +85,7 @@
 extern "C" {
 #endif
 
-#define CA_ABI_VERSION 5
+#define CA_ABI_VERSION 6
 
 typedef enum ca_status {
   CA_OK = 0,
@@ -94,7 +95,7 @@ typedef enum ca_status {
   CA_ERR_GROUP = 4,         /* group_size does not divide Hq / Hkv              */
   CA_ERR_WORKSPACE = 5,     /* workspace missing or too small                   */
   CA_ERR_UNSUPPORTED = 6,   /* head_dim / page_size / q_block not built for     */
-  CA_ERR_INVALID_TABLE = 7, /* ca_validate_tables found a malformed table       */
+  CA_ERR_INVALID_TABLE = 7, /* a malformed table or page id (table checks)      */
   CA_ERR_HIP = 8            /* a HIP runtime call or kernel launch failed       */
 } ca_status;
 
@@ -376,6 +377,32 @@ ca_status ca_packed_chunk_attention(const ca_problem* p, const uint16_t* q,
 ca_status ca_validate_tables(const ca_problem* p, int32_t group_size,
                              const int32_t* kv_indptr, const int32_t* kv_indices,
                              int32_t require_chunk_open, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Host-only table check (no GPU, nothing enqueued): the checks of
+ * ca_validate_tables on HOST copies of the tables and, when page_table is not
+ * NULL (a HOST copy of the page table [B, Hkv, max_kv_blocks]), that the page
+ * of every listed block is in [0, pool_pages).  group_size >= 1: one row per
+ * (b, group), as ca_build_block_tables writes them; group_size == 0: one row
+ * per (b, h, Q-block), the block-sparse layout of ca_build_block_sparse_tables.
+ * Returns CA_ERR_INVALID_TABLE with a description in ca_last_error_detail()
+ * on the first violation; the arrays are only read.
+ *
+ * Debug build.  libcompactattn_debug.so (the same sources compiled with
+ * CA_DEBUG_CHECKS) runs this check before every attention launch
+ * (ca_chunk_attention, ca_dense_paged_chunk_attention,
+ * ca_block_sparse_chunk_attention, ca_packed_chunk_attention): it
+ * synchronises the stream, copies the tables and the page table to the host,
+ * takes pool_pages from the device allocations that hold k_pool and v_pool,
+ * and returns CA_ERR_INVALID_TABLE instead of launching when a table entry or
+ * a page id is out of range (for the packed pools: when the tables list more
+ * pages than the pools hold).  Results are otherwise identical to the
+ * release library's; every attention call then synchronises.
+ * ---------------------------------------------------------------------- */
+ca_status ca_check_tables_host(const ca_problem* p, int32_t group_size,
+                               const int32_t* kv_indptr, const int32_t* kv_indices,
+                               const int32_t* page_table, int64_t pool_pages,
+                               int32_t require_chunk_open);
 
 #ifdef __cplusplus
 }

@@ -10,9 +10,10 @@ from .binding import (  # noqa: F401
     dense_paged_chunk_attention, validate_tables, block_sparse_tables_workspace_bytes,
     build_block_sparse_tables, block_sparse_chunk_attention, gather_selected_pages,
     packed_chunk_attention, estimate_masks_threshold, select_blocks_threshold, estimate_tables,
-    build_block_tables_noalloc,
+    build_block_tables_noalloc, check_tables_host,
     EXPORTED,
     LIB_PATH,
+    DEBUG_LIB_PATH,
     V_TOKEN_MAJOR,
     V_TRANSPOSED,
 )

@@ -16,6 +16,9 @@ import torch
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libcompactattn.so")
+# the same sources built with CA_DEBUG_CHECKS: table and page-id checks before
+# every attention launch (see ca_check_tables_host in include/compactattn.h)
+DEBUG_LIB_PATH = os.path.join(_PKG, "libcompactattn_debug.so")
 
 _c_i32p = ctypes.POINTER(ctypes.c_int32)
 
@@ -28,7 +31,7 @@ EXPORTED = (
     "ca_block_sparse_tables_workspace_bytes", "ca_build_block_sparse_tables",
     "ca_block_sparse_chunk_attention", "ca_gather_selected_pages", "ca_packed_chunk_attention",
     "ca_select_blocks_threshold", "ca_estimate_masks_threshold", "ca_estimate_tables",
-    "ca_build_block_tables_noalloc",
+    "ca_build_block_tables_noalloc", "ca_check_tables_host",
 )
 
 
@@ -97,6 +100,7 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
         "ca_dense_paged_chunk_attention": ([P, vp, vp, vp, vp, f32, i32, vp, vp, vp, sz, vp],
                                            ctypes.c_int),
         "ca_validate_tables": ([P, i32, vp, vp, i32, vp], ctypes.c_int),
+        "ca_check_tables_host": ([P, i32, vp, vp, vp, i64, i32], ctypes.c_int),
         "ca_select_blocks_threshold": ([P, vp, f32, f32, f32, i32, i32, vp, vp], ctypes.c_int),
         "ca_estimate_masks_threshold": ([P, vp, vp, vp, f32, f32, f32, i32, i32, i32, vp, vp, vp,
                                          vp, vp], ctypes.c_int),
@@ -516,6 +520,19 @@ def packed_chunk_attention(p: Problem, q_chunk: torch.Tensor,
                                             k_packed.shape[0], _ptr(out), _ptr(lse), _ptr(ws),
                                             _nbytes(ws), _stream(stream)))
     return out, lse
+
+
+def check_tables_host(p: Problem, group_size: int, kv_indptr, kv_indices, page_table=None,
+                      pool_pages: int = 0, require_chunk_open: bool = False) -> None:
+    """Host-only check of host (numpy int32) tables and, with a page table, of the
+    page ids they reach; group_size 0 = the block-sparse (b, h, Q-block) rows."""
+    import numpy as np
+
+    arr = [None if a is None else np.ascontiguousarray(a, dtype=np.int32)
+           for a in (kv_indptr, kv_indices, page_table)]
+    ptr = lambda a: None if a is None else ctypes.c_void_p(a.ctypes.data)
+    _check(load().ca_check_tables_host(p.ref, group_size, ptr(arr[0]), ptr(arr[1]), ptr(arr[2]),
+                                       int(pool_pages), int(require_chunk_open)))
 
 
 def validate_tables(p: Problem, group_size: int, tables, require_chunk_open: bool = True,

@@ -151,6 +151,159 @@ ca_status need_aligned16(const char* names, const T*... ptrs) {
   return ok ? CA_OK : fail(CA_ERR_UNALIGNED, "%s must be 16-byte aligned", names);
 }
 
+// Rows of a table layout: group_size >= 1, one row per (b, group) (the group
+// union tables); group_size == 0, one row per (b, h, Q-block) (block-sparse).
+int table_rows(const ca::Dims& d, int group_size) {
+  return group_size > 0 ? d.B * (d.Hq / group_size) : d.B * d.Hq * d.nqb;
+}
+void row_owner(const ca::Dims& d, int group_size, int r, int* b, int* kvh) {
+  const int ratio = d.Hq / d.Hkv;
+  if (group_size > 0) {
+    const int G = d.Hq / group_size;
+    *b = r / G;
+    *kvh = ((r % G) * group_size) / ratio;
+  } else {
+    *b = r / (d.Hq * d.nqb);
+    *kvh = ((r / d.nqb) % d.Hq) / ratio;
+  }
+}
+
+// The table checks on host arrays: kv_indptr[0] == 0, non-decreasing row
+// bounds within the capacity, entries strictly ascending in [0, nKB_b), the
+// chunk blocks all present (require_chunk_open), and with a page table, the
+// page of every listed block in [0, pool_pages).
+ca_status check_tables(const ca_problem* p, const ca::Dims& d, int group_size,
+                       const int32_t* ip, const int32_t* ix, const int32_t* page_table,
+                       long long pool_pages, bool require_chunk_open) {
+  const int R = table_rows(d, group_size);
+  const size_t cap = (size_t)R * d.max_kv_blocks;
+  if (ip[0] != 0) return fail(CA_ERR_INVALID_TABLE, "kv_indptr[0] = %d, expected 0", ip[0]);
+  for (int r = 0; r < R; ++r)
+    if (ip[r + 1] < ip[r] || (size_t)ip[r + 1] > cap)
+      return fail(CA_ERR_INVALID_TABLE, "kv_indptr[%d..%d] = %d..%d is not a valid range", r,
+                  r + 1, ip[r], ip[r + 1]);
+  for (int r = 0; r < R; ++r) {
+    int b, kvh;
+    row_owner(d, group_size, r, &b, &kvh);
+    const int nc = p->cached_len_host[b] / d.page;
+    const int nkb = ca::blocks_for(p->cached_len_host[b] + d.C);
+    int prev = -1, chunk_seen = 0;
+    for (int x = ip[r]; x < ip[r + 1]; ++x) {
+      const int j = ix[x];
+      if (j <= prev || j < 0 || j >= nkb)
+        return fail(CA_ERR_INVALID_TABLE, "row %d entry %d = %d (previous %d, nKB %d)", r,
+                    x - ip[r], j, prev, nkb);
+      if (page_table) {
+        const int32_t pg = page_table[((size_t)b * d.Hkv + kvh) * d.max_kv_blocks + j];
+        if (pg < 0 || pg >= pool_pages)
+          return fail(CA_ERR_INVALID_TABLE,
+                      "row %d block %d: page %d outside the pool's %lld pages", r, j, pg,
+                      pool_pages);
+      }
+      if (j >= nc) ++chunk_seen;
+      prev = j;
+    }
+    if (require_chunk_open && chunk_seen != nkb - nc)
+      return fail(CA_ERR_INVALID_TABLE, "row %d holds %d of the %d chunk blocks", r, chunk_seen,
+                  nkb - nc);
+  }
+  return ok();
+}
+
+// Synchronises the stream and copies the tables (and the page table when
+// given) to the host.
+ca_status copy_tables(const ca::Dims& d, int group_size, const int32_t* kv_indptr,
+                      const int32_t* kv_indices, const int32_t* page_table, hipStream_t st,
+                      std::vector<int32_t>& ip, std::vector<int32_t>& ix,
+                      std::vector<int32_t>& pt) {
+  hipError_t e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return hip_status(e, "stream synchronize");
+  const int R = table_rows(d, group_size);
+  ip.assign(R + 1, 0);
+  if ((e = hipMemcpy(ip.data(), kv_indptr, (R + 1) * sizeof(int32_t), hipMemcpyDeviceToHost)) !=
+      hipSuccess)
+    return hip_status(e, "copy kv_indptr");
+  const size_t cap = (size_t)R * d.max_kv_blocks;
+  const size_t n = ip[R] > 0 && (size_t)ip[R] <= cap ? (size_t)ip[R] : 0;
+  ix.assign(n > 0 ? n : 1, 0);
+  if (n > 0 &&
+      (e = hipMemcpy(ix.data(), kv_indices, n * sizeof(int32_t), hipMemcpyDeviceToHost)) !=
+          hipSuccess)
+    return hip_status(e, "copy kv_indices");
+  if (page_table) {
+    pt.assign((size_t)d.B * d.Hkv * d.max_kv_blocks, 0);
+    if ((e = hipMemcpy(pt.data(), page_table, pt.size() * sizeof(int32_t),
+                       hipMemcpyDeviceToHost)) != hipSuccess)
+      return hip_status(e, "copy page_table");
+  }
+  return ok();
+}
+
+#ifdef CA_DEBUG_CHECKS
+// Pages of `page_elems` elements from `pool` to the end of the allocation that
+// holds it.
+ca_status pool_pages_of(const uint16_t* pool, size_t page_elems, long long* pages) {
+  void* base = nullptr;
+  size_t size = 0;
+  hipError_t e = hipMemGetAddressRange(&base, &size, const_cast<uint16_t*>(pool));
+  if (e != hipSuccess) return hip_status(e, "pool address range");
+  const size_t avail = static_cast<const char*>(base) + size - reinterpret_cast<const char*>(pool);
+  *pages = (long long)(avail / (page_elems * sizeof(uint16_t)));
+  return ok();
+}
+
+// The debug build's check before every attention launch: the tables and
+// every page the launch will read, against the allocations of the pools.
+ca_status debug_check_launch(const ca_problem* p, const ca::Dims& d, int group_size,
+                             int table_mode, bool dense, const uint16_t* k_pool,
+                             const uint16_t* v_pool, const int32_t* page_table,
+                             const int32_t* kv_indptr, const int32_t* kv_indices,
+                             long long packed_pages, hipStream_t st) {
+  const size_t page_elems = (size_t)d.page * d.D;
+  long long pk = 0, pv = 0;
+  ca_status s;
+  if ((s = pool_pages_of(k_pool, page_elems, &pk)) != CA_OK) return s;
+  if ((s = pool_pages_of(v_pool, page_elems, &pv)) != CA_OK) return s;
+  const long long pages = pk < pv ? pk : pv;
+  const int gs = table_mode == ca::kTablesPerQTile ? 0 : group_size;
+  std::vector<int32_t> ip, ix, pt;
+  if (dense) {
+    // identity tables: every block of every sequence
+    const int R = d.B * d.Hkv;
+    ip.assign(R + 1, 0);
+    for (int r = 0; r < R; ++r) {
+      const int b = r / d.Hkv;
+      const int nkb = ca::blocks_for(p->cached_len_host[b] + d.C);
+      ip[r + 1] = ip[r] + nkb;
+      for (int j = 0; j < nkb; ++j) ix.push_back(j);
+    }
+    hipError_t e = hipStreamSynchronize(st);
+    if (e != hipSuccess) return hip_status(e, "stream synchronize");
+    pt.assign((size_t)d.B * d.Hkv * d.max_kv_blocks, 0);
+    if ((e = hipMemcpy(pt.data(), page_table, pt.size() * sizeof(int32_t),
+                       hipMemcpyDeviceToHost)) != hipSuccess)
+      return hip_status(e, "copy page_table");
+    return check_tables(p, d, d.Hq / d.Hkv, ip.data(), ix.data(), pt.data(), pages, false);
+  }
+  const bool packed = table_mode == ca::kTablesPacked;
+  if ((s = copy_tables(d, gs, kv_indptr, kv_indices, packed ? nullptr : page_table, st, ip, ix,
+                       pt)) != CA_OK)
+    return s;
+  if ((s = check_tables(p, d, gs, ip.data(), ix.data(), packed ? nullptr : pt.data(), pages,
+                        false)) != CA_OK)
+    return s;
+  if (packed) {
+    // the packed pools hold the listed pages in table order
+    const long long listed = ip[table_rows(d, gs)];
+    const long long cap = packed_pages < pages ? packed_pages : pages;
+    if (listed > cap)
+      return fail(CA_ERR_INVALID_TABLE, "the tables list %lld pages, the packed pools hold %lld",
+                  listed, cap);
+  }
+  return ok();
+}
+#endif
+
 ca_status run_attention(const ca_problem* p, const uint16_t* q, const uint16_t* k_pool,
                         const uint16_t* v_pool, const int32_t* page_table,
                         const int32_t* kv_indptr, const int32_t* kv_indices, int32_t group_size,
@@ -214,6 +367,12 @@ ca_status run_attention(const ca_problem* p, const uint16_t* q, const uint16_t* 
   L.table_mode = table_mode;
   L.packed_pages = packed_pages;
   L.v_layout = p->v_layout == CA_V_TRANSPOSED ? ca::kVTransposed : ca::kVTokenMajor;
+#ifdef CA_DEBUG_CHECKS
+  if ((s = debug_check_launch(p, d, group_size, table_mode, dense, k_pool, v_pool, page_table,
+                              kv_indptr, kv_indices, packed_pages,
+                              static_cast<hipStream_t>(stream))) != CA_OK)
+    return s;
+#endif
   return hip_status(ca::launch_attention(d, L, static_cast<hipStream_t>(stream)),
                     dense ? "dense paged attention launch" : "chunk attention launch");
 }
@@ -661,6 +820,20 @@ ca_status ca_packed_chunk_attention(const ca_problem* p, const uint16_t* q,
                        ca::kTablesPacked, capacity_pages);
 }
 
+ca_status ca_check_tables_host(const ca_problem* p, int32_t group_size,
+                               const int32_t* kv_indptr, const int32_t* kv_indices,
+                               const int32_t* page_table, int64_t pool_pages,
+                               int32_t require_chunk_open) {
+  ca::Dims d;
+  if (group_size < 0) return fail(CA_ERR_GROUP, "group_size must be >= 0");
+  ca_status s = check(p, group_size, &d);
+  if (s != CA_OK) return s;
+  if (!kv_indptr || !kv_indices) return fail(CA_ERR_NULL, "kv_indptr and kv_indices are required");
+  if (page_table && pool_pages < 0) return fail(CA_ERR_SHAPE, "pool_pages must be >= 0");
+  return check_tables(p, d, group_size, kv_indptr, kv_indices, page_table, pool_pages,
+                      require_chunk_open != 0);
+}
+
 ca_status ca_validate_tables(const ca_problem* p, int32_t group_size, const int32_t* kv_indptr,
                              const int32_t* kv_indices, int32_t require_chunk_open,
                              void* stream) {
@@ -669,43 +842,12 @@ ca_status ca_validate_tables(const ca_problem* p, int32_t group_size, const int3
   ca_status s = check(p, group_size, &d);
   if (s != CA_OK) return s;
   if (!kv_indptr || !kv_indices) return fail(CA_ERR_NULL, "kv_indptr and kv_indices are required");
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  hipError_t e = hipStreamSynchronize(st);
-  if (e != hipSuccess) return hip_status(e, "stream synchronize");
-  const int G = d.Hq / group_size;
-  const int R = d.B * G;
-  const size_t cap = (size_t)R * d.max_kv_blocks;
-  std::vector<int32_t> ip(R + 1);
-  if ((e = hipMemcpy(ip.data(), kv_indptr, (R + 1) * sizeof(int32_t), hipMemcpyDeviceToHost)) !=
-      hipSuccess)
-    return hip_status(e, "copy kv_indptr");
-  if (ip[0] != 0) return fail(CA_ERR_INVALID_TABLE, "kv_indptr[0] = %d, expected 0", ip[0]);
-  for (int r = 0; r < R; ++r)
-    if (ip[r + 1] < ip[r] || (size_t)ip[r + 1] > cap)
-      return fail(CA_ERR_INVALID_TABLE, "kv_indptr[%d..%d] = %d..%d is not a valid range", r,
-                  r + 1, ip[r], ip[r + 1]);
-  std::vector<int32_t> ix(ip[R] > 0 ? ip[R] : 1);
-  if (ip[R] > 0 && (e = hipMemcpy(ix.data(), kv_indices, ip[R] * sizeof(int32_t),
-                                  hipMemcpyDeviceToHost)) != hipSuccess)
-    return hip_status(e, "copy kv_indices");
-  for (int r = 0; r < R; ++r) {
-    const int b = r / G;
-    const int nc = p->cached_len_host[b] / d.page;
-    const int nkb = ca::blocks_for(p->cached_len_host[b] + d.C);
-    int prev = -1, chunk_seen = 0;
-    for (int x = ip[r]; x < ip[r + 1]; ++x) {
-      const int j = ix[x];
-      if (j <= prev || j < 0 || j >= nkb)
-        return fail(CA_ERR_INVALID_TABLE, "row %d entry %d = %d (previous %d, nKB %d)", r,
-                    x - ip[r], j, prev, nkb);
-      if (j >= nc) ++chunk_seen;
-      prev = j;
-    }
-    if (require_chunk_open && chunk_seen != nkb - nc)
-      return fail(CA_ERR_INVALID_TABLE, "row %d holds %d of the %d chunk blocks", r, chunk_seen,
-                  nkb - nc);
-  }
-  return ok();
+  std::vector<int32_t> ip, ix, pt;
+  if ((s = copy_tables(d, group_size, kv_indptr, kv_indices, nullptr,
+                       static_cast<hipStream_t>(stream), ip, ix, pt)) != CA_OK)
+    return s;
+  return check_tables(p, d, group_size, ip.data(), ix.data(), nullptr, 0,
+                      require_chunk_open != 0);
 }
 
 }  // extern "C"

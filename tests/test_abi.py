@@ -5,6 +5,7 @@ import ctypes
 import os
 import re
 
+import numpy as np
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -290,3 +291,78 @@ def test_noalloc_tables_size_limit(lib):
     st = lambda s: lib.ca_status_string(s).decode()
     assert st(lib.ca_build_block_tables_noalloc(p.ref, fake, 3, fake, fake, None)) == "CA_ERR_GROUP"
     assert st(lib.ca_build_block_tables_noalloc(p.ref, None, 4, fake, fake, None)) == "CA_ERR_NULL"
+
+
+def _small_tables():
+    """B = 2, Hq = 4, Hkv = 2, D = 64, q_block 64, C = 128, cached 100 / 256 tokens:
+    nC = 1 / 4, nKB = 4 / 6; group_size 2 gives 4 rows (b, g), g reading KV head g."""
+    p = ca.Problem(2, 4, 2, 64, 64, 128, 8, [100, 256], device=None)
+    ip = np.array([0, 4, 8, 12, 16], dtype=np.int32)
+    ix = np.array([0, 1, 2, 3, 0, 1, 2, 3, 0, 2, 4, 5, 1, 3, 4, 5], dtype=np.int32)
+    pt = np.arange(2 * 2 * 8, dtype=np.int32).reshape(2, 2, 8)   # 32 distinct pages
+    return p, ip, ix, pt
+
+
+def _table_status(p, gs, ip, ix, pt=None, pages=0, chunk_open=0):
+    ptr = lambda a: None if a is None else ctypes.c_void_p(np.ascontiguousarray(a).ctypes.data)
+    arrs = [None if a is None else np.ascontiguousarray(a, dtype=np.int32) for a in (ip, ix, pt)]
+    return ca.load().ca_check_tables_host(p.ref, gs, *[ptr(a) for a in arrs], pages, chunk_open)
+
+
+def test_check_tables_host(lib):
+    """The host table check that the debug build runs before every attention
+    launch: CSR shape, entry order and range, chunk blocks, and page ids."""
+    INV = 7
+    p, ip, ix, pt = _small_tables()
+    assert _table_status(p, 2, ip, ix) == 0
+    assert _table_status(p, 2, ip, ix, pt, 32, 1) == 0
+    ca.check_tables_host(p, 2, ip, ix, pt, 32, True)          # the Python wrapper
+    bad = ix.copy(); bad[9], bad[10] = bad[10], bad[9]       # row 2 not ascending
+    assert _table_status(p, 2, ip, bad) == INV
+    bad = ix.copy(); bad[3] = 4                              # b = 0 has nKB = 4
+    assert _table_status(p, 2, ip, bad) == INV
+    bad = ix.copy(); bad[8] = -1
+    assert _table_status(p, 2, ip, bad) == INV
+    with pytest.raises(ca.CAError) as e:
+        ca.check_tables_host(p, 2, ip, bad)
+    assert e.value.name == "CA_ERR_INVALID_TABLE"
+    # page ids: only the pages of listed blocks are checked, against [0, pool_pages)
+    q = pt.copy(); q[1, 1, 3] = 32                           # row 3 lists block 3 of KV head 1
+    assert _table_status(p, 2, ip, ix, q, 32) == INV
+    assert _table_status(p, 2, ip, ix, q, 33) == 0
+    q = pt.copy(); q[1, 0, 2] = -1                           # row 2 lists block 2 of KV head 0
+    assert _table_status(p, 2, ip, ix, q, 32) == INV
+    q = pt.copy(); q[1, 0, 1] = 999                          # block 1 of b = 1, KV head 0: not listed
+    assert _table_status(p, 2, ip, ix, q, 32) == 0
+    q = pt.copy(); q[0, 0, 7] = -5                           # past nKB: never read
+    assert _table_status(p, 2, ip, ix, q, 32) == 0
+    # chunk blocks 4, 5 of b = 1 must all be present when asked
+    ip2 = np.array([0, 4, 8, 11, 15], dtype=np.int32)
+    ix2 = np.array([0, 1, 2, 3, 0, 1, 2, 3, 0, 2, 4, 1, 3, 4, 5], dtype=np.int32)
+    assert _table_status(p, 2, ip2, ix2) == 0
+    assert _table_status(p, 2, ip2, ix2, chunk_open=1) == INV
+    # CSR bounds
+    bad_ip = ip.copy(); bad_ip[0] = 1
+    assert _table_status(p, 2, bad_ip, ix) == INV
+    bad_ip = ip.copy(); bad_ip[2] = 3                        # decreasing bound
+    assert _table_status(p, 2, bad_ip, ix) == INV
+    bad_ip = ip.copy(); bad_ip[4] = 4 * 8 + 1                # beyond B*G*max_kv_blocks
+    assert _table_status(p, 2, bad_ip, ix) == INV
+    # argument errors
+    assert _table_status(p, -1, ip, ix) == 4                 # CA_ERR_GROUP
+    assert _table_status(p, 3, ip, ix) == 4                  # 3 does not divide Hq / Hkv
+    assert ca.load().ca_check_tables_host(p.ref, 2, None, None, None, 0, 0) == 1   # CA_ERR_NULL
+
+
+def test_check_tables_host_block_sparse_rows(lib):
+    """group_size 0: one row per (b, h, Q-block); row (b, h, i) reads KV head h / 2."""
+    p, _, _, pt = _small_tables()
+    nqb = 2
+    rows = 2 * 4 * nqb
+    ip = np.arange(rows + 1, dtype=np.int32)                 # every row lists block 0
+    ix = np.zeros(rows, dtype=np.int32)
+    assert _table_status(p, 0, ip, ix, pt, 32) == 0
+    q = pt.copy(); q[1, 1, 0] = 40                           # (b = 1, h = 2 or 3) rows
+    assert _table_status(p, 0, ip, ix, q, 32) == 7
+    q = pt.copy(); q[1, 1, 1] = 40                           # block 1: listed by no row
+    assert _table_status(p, 0, ip, ix, q, 32) == 0
