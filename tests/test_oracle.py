@@ -621,3 +621,27 @@ def test_threshold_masks_hand_built_unaligned():
     # b = 2: 63 cached tokens: positions 63..126 -> blocks 0..1, 127..162 -> 0..2
     assert _bits(masks[2, 0, 0, 0]) == {0, 1}
     assert _bits(masks[2, 0, 1, 0]) == {0, 1, 2}
+
+
+def test_union_densities_hand_built():
+    """Densities of cached blocks before and after each union, worked out by hand.
+
+    One sequence with nC = 4 cached blocks, 4 heads x 2 Q-blocks, groups of 2
+    heads.  Kept cached blocks per (head, Q-block): h0 {0} {1}, h1 {0} {0},
+    h2 {3} {}, h3 {2, 3} {2}; every row also holds chunk block 5, which no
+    density counts.  Pre-union: 8 of 32 = 0.25.  Q-block union per head:
+    {0,1} {0} {3} {2,3} = 6 of 16 = 0.375.  Group union: {0,1} {2,3} = 4 of 8
+    = 0.5.  A second sequence with no cached block is left out of every mean."""
+    rows = {(0, 0): [0], (0, 1): [1], (1, 0): [0], (1, 1): [0], (2, 0): [3], (2, 1): [],
+            (3, 0): [2, 3], (3, 1): [2]}
+    masks = np.zeros((2, 4, 2, 1), dtype=np.uint64)
+    for (h, i), js in rows.items():
+        for j in js + [5]:
+            masks[0, h, i, 0] |= np.uint64(1) << np.uint64(j)
+    masks[1, :, :, 0] = np.uint64(0b111)       # nC = 0: chunk blocks only
+    dens = oracle.union_densities(masks, 2, [4, 0])
+    assert dens == {"pre_union": 0.25, "q_union": 0.375, "group_union": 0.5}
+    # groups of 4 heads: one group {0, 1, 2, 3} = 4 of 4
+    assert oracle.union_densities(masks, 4, [4, 0])["group_union"] == 1.0
+    # group size 1: the group union is the Q-block union
+    assert oracle.union_densities(masks, 1, [4, 0])["group_union"] == 0.375
