@@ -617,6 +617,47 @@ def test_attention_xcd_split_unbalanceable_tables(workload_inputs):
     assert np.abs(got0 - got1).max() <= 2e-2 and np.abs(lse0 - lse1).max() <= 1e-3
 
 
+_D64 = {}
+
+
+def test_attention_d64_xcd_split():
+    """head_dim 64 at a shape whose query tiles fill the GPU (32 / 8 heads, a
+    2048-token chunk after 30720 cached tokens: 8 groups x 32 tiles), so the
+    default schedule is the XCD-balanced two-piece split with the D = 64
+    kernel.  Random tables at 0.3 cached density with group rows of different
+    lengths; rows on every (group, tile) against the oracle, for the default
+    schedule and for one pass per tile, then the dense baseline."""
+    if "d" not in _D64:
+        _D64["d"] = synth.make_inputs(synth.get_workload("llama8b_32k", head_dim=64))
+    d = _D64["d"]
+    w = d["workload"]
+    assert w.head_dim == 64
+    p = _problem(w)
+    x = device_inputs(d)
+    nc, nkb = w.n_cached_blocks(0), w.n_kv_blocks(0)
+    ip, ix = synth.random_tables(w.seed + 64, w.batch, w.num_groups, [nc], nkb - nc, 0.3)
+    # drop a different number of cached entries from each group row: unequal lengths
+    rows_T = []
+    for r in range(w.num_groups):
+        row = ix[ip[r]:ip[r + 1]].tolist()
+        cached = [j for j in row if j < nc]
+        rows_T.append(cached[: max(1, len(cached) - 20 * r)] + [j for j in row if j >= nc])
+    T = [rows_T]
+    csr = oracle.tables_to_csr(T)
+    rows = sorted(set(sample_rows(w.batch, w.num_q_heads, w.chunk_len, seed=w.seed + 3)) |
+                  set(tile_rows(w.batch, w.num_q_heads, w.chunk_len, w.group_size, seed=w.seed)))
+    ref, ref_lse = _oracle_rows(d, T, w.group_size, w.sm_scale, rows)
+    for splits in (0, 1):
+        got, lse = _run_attention(p, x, csr, w.group_size, w.sm_scale, num_splits=splits)
+        print("d64 splits", splits, len(rows), "rows", compare_attention(got, lse, ref, ref_lse, rows))
+    # dense baseline: every block, one table per KV head
+    ratio = w.num_q_heads // w.num_kv_heads
+    dense_T = [[list(range(nkb))] * w.num_kv_heads]
+    got, lse = _run_attention(p, x, None, ratio, w.sm_scale, dense=True)
+    ref, ref_lse = _oracle_rows(d, dense_T, ratio, w.sm_scale, rows[::4])
+    print("d64 dense", compare_attention(got, lse, ref, ref_lse, rows[::4]))
+
+
 @pytest.mark.parametrize("name", ["llama8b_32k", "batched_ragged_4seq", "llama8b_unaligned"])
 def test_dense_baseline_sampled(name, workload_inputs):
     d = workload_inputs(name)
