@@ -617,6 +617,54 @@ def test_attention_xcd_split_unbalanceable_tables(workload_inputs):
     assert np.abs(got0 - got1).max() <= 2e-2 and np.abs(lse0 - lse1).max() <= 1e-3
 
 
+_MAX = {}
+
+
+def test_max_context_whole_path():
+    """The largest page table the library takes: one sequence of 16384 blocks
+    (1046528 cached + 2048 chunk tokens), 4 / 1 heads, head_dim 64 (a 256 MiB
+    KV pool).  Estimator masks against the oracle (near ties only), tables bit
+    for bit against the oracle union of the GPU masks (256 mask words per row),
+    and attention on rows of every query tile against the oracle: the 32 tiles
+    of the single group row run with 8 uniform splits, so the general combine
+    runs at its widest here; then the dense baseline on a few rows."""
+    if "d" not in _MAX:
+        w = synth.get_workload("tiny_gqa_1k", cached_lens=(16384 * 64 - 2048,), chunk_len=2048,
+                               max_kv_blocks=16384, mask_kind="estimator", top_frac=0.02)
+        d = synth.make_inputs(w)
+        _MAX["d"] = d
+        _MAX["est"] = oracle.estimate_masks(
+            d["q"], d["k_pool"], d["page_table"], d["cached_len"], w.page_size, w.q_block,
+            w.chunk_len, w.words, _params(w), return_parts=True)
+    d, (ref_masks, parts) = _MAX["d"], _MAX["est"]
+    w = d["workload"]
+    assert w.n_kv_blocks(0) == w.max_kv_blocks == 16384 and w.words == 256
+    p = _problem(w)
+    x = device_inputs(d)
+    gm_t, _ = ca.estimate_masks(p, x["q"], x["k"], x["pt"], w.top_frac, w.sink_blocks,
+                                w.local_blocks)
+    torch.cuda.synchronize()
+    gm = u64_host(gm_t)
+    print("max context:", _near_tie_check(gm, ref_masks, parts["scores"], w, tol=1e-5),
+          "near-tie rows differ")
+    T = oracle.block_tables(gm, w.group_size, [w.n_kv_blocks(0)])
+    rip, rix = oracle.tables_to_csr(T)
+    ip, ix = ca.build_block_tables(p, gm_t, w.group_size)
+    torch.cuda.synchronize()
+    assert np.array_equal(ip.cpu().numpy(), rip)
+    assert np.array_equal(ix.cpu().numpy()[:rip[-1]], rix)
+    got, lse = _run_attention(p, x, (ip, ix), w.group_size, w.sm_scale, num_splits=0)
+    rows = sorted(set(sample_rows(w.batch, w.num_q_heads, w.chunk_len, seed=w.seed + 17)) |
+                  set(tile_rows(w.batch, w.num_q_heads, w.chunk_len, w.group_size, seed=w.seed)))
+    ref, ref_lse = _oracle_rows(d, T, w.group_size, w.sm_scale, rows)
+    print("max context attention", len(rows), "rows",
+          compare_attention(got, lse, ref, ref_lse, rows))
+    got, lse = _run_attention(p, x, None, w.group_size, w.sm_scale, dense=True)
+    dense_T = [[list(range(w.n_kv_blocks(0)))]]
+    ref, ref_lse = _oracle_rows(d, dense_T, w.group_size, w.sm_scale, rows[::8])
+    print("max context dense", compare_attention(got, lse, ref, ref_lse, rows[::8]))
+
+
 _D64 = {}
 
 
