@@ -617,6 +617,40 @@ def test_attention_xcd_split_unbalanceable_tables(workload_inputs):
     assert np.abs(got0 - got1).max() <= 2e-2 and np.abs(lse0 - lse1).max() <= 1e-3
 
 
+@pytest.mark.parametrize("splits", [0, 1, 3])
+def test_attention_empty_and_unseen_rows(splits, workload_inputs):
+    """Tables that leave queries with nothing to see (reading R15: output 0,
+    lse = -inf) next to normal rows, at a shape whose default schedule is the
+    XCD-balanced split: group 0 empty, group 1 only the sink block, group 2
+    only the chunk's last block (every query before it sees nothing), group 3
+    the last cached block and the chunk, the others random at 0.3 density."""
+    d = workload_inputs("llama8b_32k")
+    w = d["workload"]
+    p = _problem(w)
+    x = device_inputs(d)
+    nc, nkb = w.n_cached_blocks(0), w.n_kv_blocks(0)
+    ip, ix = synth.random_tables(w.seed + 15, w.batch, w.num_groups, [nc], nkb - nc, 0.3)
+    rows_T = [ix[ip[r]:ip[r + 1]].tolist() for r in range(w.num_groups)]
+    rows_T[0] = []
+    rows_T[1] = [0]
+    rows_T[2] = [nkb - 1]
+    rows_T[3] = [nc - 1] + list(range(nc, nkb))
+    T = [rows_T]
+    got, lse = _run_attention(p, x, oracle.tables_to_csr(T), w.group_size, w.sm_scale,
+                              num_splits=splits)
+    rows = sorted(set(tile_rows(w.batch, w.num_q_heads, w.chunk_len, w.group_size,
+                                seed=w.seed + splits)) |
+                  {(0, h, t) for h in (0, 5, 9, 13) for t in (0, 1, 1983, 1984, 2047)})
+    ref, ref_lse = _oracle_rows(d, T, w.group_size, w.sm_scale, rows)
+    print(splits, compare_attention(got, lse, ref, ref_lse, rows))
+    # group 0 (heads 0-3): nothing at all; group 2 (heads 8-11): nothing before the
+    # last block's first key
+    assert np.all(got[0, :, 0:4] == 0) and np.all(np.isneginf(lse[0, 0:4]))
+    first = (nkb - 1) * 64 - w.cached_lens[0]
+    assert np.all(got[0, :first, 8:12] == 0) and np.all(np.isneginf(lse[0, 8:12, :first]))
+    assert np.all(np.isfinite(lse[0, 8:12, first:]))
+
+
 _MAX = {}
 
 
