@@ -886,6 +886,10 @@ def main():
         # algorithmic bytes / stage time (attention: the back-to-back launch time)
         "stage_GBps": {k: round(v / ((attn_ms if k == "attention" else st_ms[k]) * 1e-3) / 1e9, 1)
                        for k, v in stage_bytes(w, ip, ix).items()},
+        # the same rates as fractions of the 8 TB/s HBM peak
+        "stage_hbm_frac": {k: round(v / ((attn_ms if k == "attention" else st_ms[k]) * 1e-3)
+                                    / 1e9 / PEAK_HBM_GBS, 4)
+                           for k, v in stage_bytes(w, ip, ix).items()},
         "fused_step_ms": round(fused_ms, 4),
         "fused_estimate_tables_ms": round(fused_est_ms, 4),
         "dense_ms": round(dense_ms, 4),
