@@ -168,12 +168,14 @@ def _bs_oracle_rows(d, bits, sm_scale, rows):
     return ref, ref_lse
 
 
-@pytest.mark.parametrize("name", ["llama8b_32k", "batched_ragged_4seq", "llama8b_unaligned"])
-def test_block_sparse_attention_sampled(name, workload_inputs, oracle_estimate):
+@pytest.mark.parametrize("name,v_layout", [("llama8b_32k", 0), ("batched_ragged_4seq", 0),
+                                           ("llama8b_unaligned", 0), ("llama8b_unaligned", 1)])
+def test_block_sparse_attention_sampled(name, v_layout, workload_inputs, oracle_estimate):
+    """v_layout 0: token-major V pages, 1: transposed (NaN past each sequence end)."""
     d = workload_inputs(name)
     w = d["workload"]
-    p = ca.Problem.from_workload(w)
-    x = device_inputs(d)
+    p = ca.Problem.from_workload(w, v_layout=v_layout)
+    x = device_inputs(d, v_layout)
     masks, _ = oracle_estimate(name)
     bits = oracle.unpack_masks(masks)
     tabs = ca.build_block_sparse_tables(p, u64_dev(masks))
