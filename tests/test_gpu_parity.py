@@ -699,6 +699,84 @@ def test_max_context_whole_path():
     print("max context dense", compare_attention(got, lse, ref, ref_lse, rows[::8]))
 
 
+def _trunc_div(a, b):
+    """Integer division rounding toward zero (as the kernel's C++ does)."""
+    q = abs(a) // abs(b)
+    return q if (a >= 0) == (b >= 0) else -q
+
+
+def _xcd_cut_points(lengths):
+    """The XCD-balanced split's cut point of every table row, from its rule: row r
+    runs on XCD r % 8; XCD x keeps the first C_x entries of its rows and runs the
+    rest of XCD x-1's rows; equal loads give C_x = C_{x-1} + S - L_{x-1} (S = sum L
+    / 8) up to C_0, the largest C_0 that keeps every 0 <= C_x <= L_x (clamped when
+    none does); C_x is shared among the XCD's rows in proportion to their lengths.
+    -1: row not cut (whole in the first piece), -2: not cut (whole in the second)."""
+    R = len(lengths)
+    L = [sum(lengths[x::8]) for x in range(8)]
+    total = sum(L)
+    D8 = [0] * 8
+    for x in range(1, 8):
+        D8[x] = D8[x - 1] + total - 8 * L[x - 1]
+    lo, hi = 0, 8 * L[0]
+    for x in range(8):
+        lo, hi = max(lo, -D8[x]), min(hi, 8 * L[x] - D8[x])
+    c0 = hi if lo <= hi else _trunc_div(lo + hi, 2)
+    cuts = []
+    for r in range(R):
+        x = r % 8
+        cx = min(max(_trunc_div(c0 + D8[x], 8), 0), L[x])
+        before = sum(lengths[x:r:8])
+        a0 = before * cx // L[x] if L[x] else 0
+        a1 = (before + lengths[r]) * cx // L[x] if L[x] else 0
+        c = a1 - a0
+        cuts.append(-1 if c >= lengths[r] else (-2 if c <= 0 else c))
+    return cuts
+
+
+@pytest.mark.parametrize("name,dense", [("llama8b_128k_final", False),
+                                        ("batched_ragged_4seq", False),
+                                        ("batched_ragged_4seq", True)])
+def test_xcd_cut_points(name, dense, workload_inputs, oracle_estimate):
+    """The cut points each attention workgroup computes (stored for the combine in the
+    workspace after the two partial results) equal the balancing rule evaluated on the
+    host from the table lengths, and the XCD loads they give are equal to within the
+    rounding of the cuts (a schedule property: a wrong cut changes no output, only the
+    balance)."""
+    d = workload_inputs(name)
+    w = d["workload"]
+    gs = w.group_size if not dense else w.num_q_heads // w.num_kv_heads
+    p = _problem(w)
+    x = device_inputs(d)
+    nbytes = ca.attention_workspace_bytes(p, gs, 0)
+    ws = torch.zeros(nbytes, dtype=torch.uint8, device="cuda")
+    if dense:
+        ca.dense_paged_chunk_attention(p, x["q"], (x["k"], x["v"]), x["pt"], w.sm_scale,
+                                       num_splits=0, ws=ws)
+        G = w.num_kv_heads
+        lengths = [w.n_kv_blocks(r // G) for r in range(w.batch * G)]
+    else:
+        masks, _ = oracle_estimate(name)
+        T, csr = _oracle_tables(masks, w)
+        ca.chunk_attention(p, x["q"], (x["k"], x["v"]), x["pt"], (i32_dev(csr[0]), i32_dev(csr[1])),
+                           gs, w.sm_scale, num_splits=0, ws=ws)
+        lengths = np.diff(csr[0]).tolist()
+    torch.cuda.synchronize()
+    R = len(lengths)
+    assert R % 8 == 0
+    off = 2 * w.batch * w.num_q_heads * w.chunk_len * (w.head_dim + 1) * 4
+    got = ws[off:off + 4 * R].cpu().numpy().view(np.int32).tolist()
+    want = _xcd_cut_points(lengths)
+    assert got == want, (got, want)
+    # loads per XCD: first pieces of its own rows + second pieces of the previous XCD's
+    first = [len_ if c == -1 else (0 if c == -2 else c) for len_, c in zip(lengths, got)]
+    loads = [sum(first[x::8]) + sum(l - f for l, f in zip(lengths[(x - 1) % 8::8],
+                                                          first[(x - 1) % 8::8]))
+             for x in range(8)]
+    print(name, "dense" if dense else "selected", "XCD loads", loads)
+    assert max(loads) - min(loads) <= 8 * (R // 8) + 1
+
+
 _D64 = {}
 
 
