@@ -4,9 +4,10 @@ One step = the whole path on the 128K final chunk (LLaMA-3.1-8B layer shape:
 32 query / 8 KV heads, head_dim 128, 129024 cached tokens + a 2048-token
 chunk, bf16): estimate masks (Q/K block pooling over the whole cache, block
 scores, top-5% + sink + local + causal selection) -> block-union tables ->
-zero-copy paged attention (+ split combine when used).  Inputs are seeded
-synthetic tensors already resident in HBM.  The dense paged baseline (same
-attention kernel over every block) is timed in the same run.
+zero-copy paged attention (one launch: the XCD-balanced split merges its two
+pieces inside it).  Inputs are seeded synthetic tensors already resident in
+HBM.  The dense paged baseline (same attention kernel over every block) is
+timed in the same run.
 
 Prints ONE JSON line (see the repository's bench contract).
 """

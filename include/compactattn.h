@@ -21,7 +21,9 @@
  * --------------------------------
  * - All pointers are DEVICE memory unless the name ends in _host.  The
  *   caller allocates and owns every buffer; the library allocates nothing
- *   and keeps no state besides a thread-local error string.
+ *   and keeps no state besides a thread-local error string, the scratch
+ *   array of ca_build_block_tables_noalloc and a launch counter that tags
+ *   the split attention launches.
  * - bf16 tensors are passed as uint16_t bit patterns.  All tensors are dense
  *   row-major (C order) with the shapes given below.  The bf16 and fp32
  *   tensors (q, k_pool, v_pool, out, q_mean, k_mean, scores, packed pools)
@@ -275,6 +277,15 @@ ca_status ca_estimate_tables(const ca_problem* p, const uint16_t* q, const uint1
  *      - otherwise splits only when the query tiles alone cannot fill the
  *        GPU and the workspace is large enough.
  *    The result does not depend on the choice beyond floating-point rounding.
+ *    The XCD-balanced split merges its two pieces inside the same launch:
+ *    the second piece of each query tile to finish reads the other's fp32
+ *    partial result from the workspace and writes the tile's output rows.
+ *    It learns that it is second from one counter per tile in the
+ *    workspace, which each launch tags with its own 56-bit value.  Uniform
+ *    splits (num_splits > 1) are merged by a second launch on the stream.
+ *    Either way the workspace needs no clearing and may hold anything on
+ *    entry (a launch leaves its counters at zero), and two launches that run
+ *    at the same time must not share a workspace.
  *    Workspace: ca_attention_workspace_bytes(p, group_size, num_splits)
  *    bytes (0 when no split is needed; for num_splits = 0 it returns the
  *    size that lets the library pick freely).

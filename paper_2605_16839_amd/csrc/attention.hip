@@ -1,6 +1,6 @@
 // Zero-copy paged chunk attention over per-group block tables (Sec. 3.3,
 // App. B.2), bf16 MFMA with fp32 online softmax, and the split-KV
-// log-sum-exp combine.
+// log-sum-exp merge.
 //
 // Work decomposition: one workgroup = NW wavefronts, 16*NCT (head, query)
 // rows per wave: NCT = 2 runs two waves per SIMD (256 registers each), NCT = 4
@@ -38,8 +38,14 @@
 //   * the workgroups of one table row run on one of the 8 XCDs and share its
 //     L2, so each page comes from HBM once; by default every row is cut in
 //     two so that the XCDs carry equal loads (xcd_cut, computed by each
-//     workgroup from the table lengths), the two pieces merged by
-//     combine_kernel.
+//     workgroup from the table lengths);
+//   * the XCD-balanced split's two pieces are merged inside the kernel: the
+//     second piece of a query tile to finish (an arrival counter per tile)
+//     reads the other's partial result and writes the output rows; uniform
+//     splits are merged by combine_kernel.
+#include <atomic>
+#include <chrono>
+#include <random>
 #include <type_traits>
 #include <utility>
 
@@ -73,14 +79,20 @@ struct AttnArgs {
   float* lse;
   float* part_o;     // [splits, B*Hq*C, D] when splits > 1
   float* part_lse;   // [splits, B*Hq*C]
+  // XCD-balanced split: one arrival counter per query tile (rowid * n_qtiles
+  // + qt), (tag << 8) | the number of the tile's pieces that stored their
+  // partial; a value with another tag counts 0, and the merging piece leaves
+  // 0 behind.  nullptr otherwise (uniform splits: combine_kernel merges)
+  unsigned long long* arrive;
+  unsigned long long tag;   // this launch's tag, < 2^56 and never 0
   int B, Hq, Hkv, C, max_kv_blocks, group_size, G, n_qtiles, splits;
   int table_mode;          // kTablesPerGroup / kTablesPerQTile / kTablesPacked
   long long packed_pages;  // capacity of the packed pools (kTablesPacked)
   float scale_log2;
   // XCD-balanced two-piece split (splits == 2) when not nullptr: every
   // workgroup computes its row's cut point (xcd_cut), and the first tile's
-  // first piece stores it in split_at[r] for the combine: the cut entry, or
-  // -1 = not cut, run whole as piece 0; -2 = not cut, run whole as piece 1
+  // first piece records it in split_at[r]: the cut entry, or -1 = not cut,
+  // run whole as piece 0; -2 = not cut, run whole as piece 1
   int32_t* split_at;
   int rows_per_unit;   // table rows that read one KV head's pages together
 };
@@ -565,7 +577,7 @@ __global__ __launch_bounds__(64 * NW, NCT == 4 ? 1 : 2) void paged_attention_ker
   bool whole = a.splits == 1;   // the piece is the whole row: final output
   if (a.split_at != nullptr) {
     int cut = xcd_cut<DENSE>(a, rowid);
-    if (sp == 0 && qt == 0 && t == 0) a.split_at[rowid] = cut;   // for the combine
+    if (sp == 0 && qt == 0 && t == 0) a.split_at[rowid] = cut;   // a record of the schedule
     if (cut < 0) {              // the row is not cut: one piece runs it, the other nothing
       if (sp != (cut == -1 ? 0 : 1)) return;
       whole = true;
@@ -999,35 +1011,145 @@ __global__ __launch_bounds__(64 * NW, NCT == 4 ? 1 : 2) void paged_attention_ker
   fence_o<AG>(o);
 
   // epilogue: O^T tile (x, c) value v of lane group grp is d = 16x + 4grp + v
+  float inv[NCT], lse_val[NCT];
+  size_t qrow_idx[NCT];
 #pragma unroll
   for (int c = 0; c < NCT; ++c) {
     const float l_tot = groups_sum(l_run[c]);
-    const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
-    const float lse_val = l_tot > 0.f ? (m_run[c] + log2f(l_tot)) * kLn2 : -INFINITY;
-    const size_t qrow_idx = ((size_t)b * a.Hq + head[c]) * a.C + tq[c];
-    if (!valid[c]) continue;
-    if (whole) {
-      uint16_t* orow = a.out + (((size_t)b * a.C + tq[c]) * a.Hq + head[c]) * D;
+    inv[c] = l_tot > 0.f ? 1.0f / l_tot : 0.f;
+    lse_val[c] = l_tot > 0.f ? (m_run[c] + log2f(l_tot)) * kLn2 : -INFINITY;
+    qrow_idx[c] = ((size_t)b * a.Hq + head[c]) * a.C + tq[c];
+  }
+  auto store_out = [&](int c, const float (&v)[NDT][4], float scale, float lse_row) {
+    uint16_t* orow = a.out + (((size_t)b * a.C + tq[c]) * a.Hq + head[c]) * D;
 #pragma unroll
-      for (int x = 0; x < NDT; ++x) {
-        const int d = 16 * x + 4 * grp;
-        uint2 pk;
-        pk.x = pack_bf16x2(o[x][c][0] * inv, o[x][c][1] * inv);
-        pk.y = pack_bf16x2(o[x][c][2] * inv, o[x][c][3] * inv);
-        *reinterpret_cast<uint2*>(orow + d) = pk;
-      }
-      if (a.lse != nullptr && grp == 0) a.lse[qrow_idx] = lse_val;
-    } else {
-      const size_t prow = (size_t)sp * a.B * a.Hq * a.C + qrow_idx;
+    for (int x = 0; x < NDT; ++x) {
+      uint2 pk;
+      pk.x = pack_bf16x2(v[x][0] * scale, v[x][1] * scale);
+      pk.y = pack_bf16x2(v[x][2] * scale, v[x][3] * scale);
+      *reinterpret_cast<uint2*>(orow + 16 * x + 4 * grp) = pk;
+    }
+    if (a.lse != nullptr && grp == 0) a.lse[qrow_idx[c]] = lse_row;
+  };
+  if (whole) {
+#pragma unroll
+    for (int c = 0; c < NCT; ++c) {
+      if (!valid[c]) continue;
+      float v[NDT][4];
+#pragma unroll
+      for (int x = 0; x < NDT; ++x)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[x][e] = o[x][c][e];
+      store_out(c, v, inv[c], lse_val[c]);
+    }
+    return;
+  }
+
+  // One piece of a split row tile: its result is the normalised partial
+  // output o * inv with its log-sum-exp.
+  const size_t nrows = (size_t)a.B * a.Hq * a.C;
+  auto store_part = [&]() {
+#pragma unroll
+    for (int c = 0; c < NCT; ++c) {
+      if (!valid[c]) continue;
+      const size_t prow = (size_t)sp * nrows + qrow_idx[c];
       float* po = a.part_o + prow * D;
 #pragma unroll
-      for (int x = 0; x < NDT; ++x) {
-        const int d = 16 * x + 4 * grp;
-        *reinterpret_cast<float4*>(po + d) = make_float4(o[x][c][0] * inv, o[x][c][1] * inv,
-                                                         o[x][c][2] * inv, o[x][c][3] * inv);
-      }
-      if (grp == 0) a.part_lse[prow] = lse_val;
+      for (int x = 0; x < NDT; ++x)
+        *reinterpret_cast<float4*>(po + 16 * x + 4 * grp) =
+            make_float4(o[x][c][0] * inv[c], o[x][c][1] * inv[c], o[x][c][2] * inv[c],
+                        o[x][c][3] * inv[c]);
+      if (grp == 0) a.part_lse[prow] = lse_val[c];
     }
+  };
+  if (a.arrive == nullptr) {   // uniform splits: a merge launch follows
+    store_part();
+    return;
+  }
+
+  // The XCD-balanced split's two pieces are merged here, by the second to
+  // finish; the first stores its partial and counts itself in.  The piece
+  // that finds the other counted merges at once and stores nothing of its own.
+  // The two pieces run on different XCDs, whose L2s are not coherent with
+  // each other: thread 0 makes one agent-scope release (the count's swap,
+  // which writes this XCD's L2 back to memory) and one agent-scope acquire
+  // (which invalidates it) for the whole workgroup.  Such a fence acts on the
+  // whole L2, so a fence in every wave costs far more (4% of the 128K final
+  // chunk's attention time, measured).
+  unsigned long long* const ctr = a.arrive + (size_t)rowid * a.n_qtiles + qt;
+  __shared__ int s_last;
+  if (t == 0) {
+    const unsigned long long w = __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    s_last = w == ((a.tag << 8) | 1ull);
+    // the other piece has counted itself in after its release
+    if (s_last) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  }
+  __syncthreads();
+  if (!s_last) {
+    store_part();
+    // every wave's stores have reached this XCD's L2 before thread 0's
+    // release writes the L2 back
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (t == 0) {
+      unsigned long long w = __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      int counted = 0;
+      // the swap fails only if the other piece's swap succeeded in between
+      for (int it = 0; it < 2; ++it) {
+        const unsigned long long nw = (w >> 8) == a.tag ? w + 1 : (a.tag << 8) | 1ull;
+        if (__hip_atomic_compare_exchange_strong(ctr, &w, nw, __ATOMIC_ACQ_REL, __ATOMIC_RELAXED,
+                                                 __HIP_MEMORY_SCOPE_AGENT)) {
+          counted = (int)(nw & 0xff);
+          break;
+        }
+      }
+      s_last = counted == 2;
+    }
+    __syncthreads();
+    if (!s_last) return;
+  }
+  // The merging piece (thread 0 has acquired, through the peek or the swap):
+  // the other piece has counted itself in, so nothing else touches the
+  // counter in this launch; leave it at 0 for the next one.
+  if (t == 0) __hip_atomic_store(ctr, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+  for (int c = 0; c < NCT; ++c) {
+    if (!valid[c]) continue;
+    const size_t row = qrow_idx[c];
+    float mine[NDT][4], other[NDT][4], acc[NDT][4];
+    const float* po = a.part_o + ((size_t)(1 - sp) * nrows + row) * D + 4 * grp;
+#pragma unroll
+    for (int x = 0; x < NDT; ++x) {
+      const float4 f = *reinterpret_cast<const float4*>(po + 16 * x);
+      other[x][0] = f.x, other[x][1] = f.y, other[x][2] = f.z, other[x][3] = f.w;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        mine[x][e] = o[x][c][e] * inv[c];
+        acc[x][e] = 0.f;
+      }
+    }
+    // lse = log(exp(lse_0) + exp(lse_1)); out = sum_i exp(lse_i - lse) o_i,
+    // pieces in order (the arithmetic of the merge launch)
+    const float lo = a.part_lse[(size_t)(1 - sp) * nrows + row];
+    const float l0 = sp == 0 ? lse_val[c] : lo, l1 = sp == 0 ? lo : lse_val[c];
+    const float mx = fmaxf(l0, l1);
+    float wsum = 0.f;
+    if (mx != -INFINITY) {
+      const float w0 = l0 == -INFINITY ? 0.f : expf(l0 - mx);
+      const float w1 = l1 == -INFINITY ? 0.f : expf(l1 - mx);
+      wsum = w0 + w1;
+      auto sum2 = [&](const float (&v0)[NDT][4], const float (&v1)[NDT][4]) {
+#pragma unroll
+        for (int x = 0; x < NDT; ++x)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            acc[x][e] = (w0 > 0.f ? w0 * v0[x][e] : 0.f) + (w1 > 0.f ? w1 * v1[x][e] : 0.f);
+      };
+      if (sp == 0) sum2(mine, other);   // sp is uniform over the workgroup
+      else sum2(other, mine);
+    }
+    store_out(c, acc, wsum > 0.f ? 1.0f / wsum : 0.f, wsum > 0.f ? mx + logf(wsum) : -INFINITY);
   }
 }
 
@@ -1086,17 +1208,16 @@ hipError_t launch_gather(const Dims& d, const uint16_t* k_pool, const uint16_t* 
   return hipGetLastError();
 }
 
-// Split-KV merge: lse = log sum_i exp(lse_i), out = sum_i exp(lse_i - lse) o_i.
-// One 32-lane half-wave per (b, h, t) row, 4 floats of d per lane (D = 128)
-// or 2 (D = 64).
+// Merge of uniform split-KV pieces: lse = log sum_i exp(lse_i),
+// out = sum_i exp(lse_i - lse) o_i, pieces in order.  One 32-lane half-wave
+// per (b, h, t) row, 4 floats of d per lane (D = 128) or 2 (D = 64).  (The
+// XCD-balanced split merges its two pieces inside the attention launch.)
 template <int D>
 __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ part_o,
                                                       const float* __restrict__ part_lse,
                                                       uint16_t* __restrict__ out,
                                                       float* __restrict__ lse, int B, int Hq,
-                                                      int C, int splits,
-                                                      const int32_t* __restrict__ split_at,
-                                                      int G, int group_size) {
+                                                      int C, int splits) {
   constexpr int PER = D / 32;
   const size_t nrows = (size_t)B * Hq * C;
   const size_t row = (size_t)blockIdx.x * 8 + (threadIdx.x >> 5);
@@ -1117,17 +1238,11 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
   for (int x = 0; x < PER; ++x) acc[x] = 0.f;
   float wsum = 0.f, mx = -INFINITY;
   if (splits == 2) {
-    // Two pieces (the XCD-balanced split): every load is issued before any
-    // result is needed, so the row costs one memory latency instead of three.
-    // The slots of an uncut row are stale; they are loaded but never used.
+    // every load is issued before any result is needed: one memory latency
     float v0[PER], v1[PER];
-    const int cut = split_at != nullptr
-        ? split_at[(int)(row / ((size_t)C * Hq)) * G + (int)((row / C) % Hq) / group_size]
-        : 0;
     const float l0 = part_lse[row], l1 = part_lse[nrows + row];
     load_part(0, v0);
     load_part(1, v1);
-    if (cut < 0) return;   // a table row that was not cut wrote its output already
     mx = fmaxf(l0, l1);
     if (mx != -INFINITY) {
       const float w0 = l0 == -INFINITY ? 0.f : expf(l0 - mx);
@@ -1138,22 +1253,18 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
         acc[x] = (w0 > 0.f ? w0 * v0[x] : 0.f) + (w1 > 0.f ? w1 * v1[x] : 0.f);
     }
   } else {
-    if (split_at != nullptr) {   // a table row that was not cut wrote its output already
-      const int hh = (int)((row / C) % Hq), bb = (int)(row / ((size_t)C * Hq));
-      if (split_at[bb * G + hh / group_size] < 0) return;
-    }
     for (int i = 0; i < splits; ++i) mx = fmaxf(mx, part_lse[(size_t)i * nrows + row]);
-  }
-  if (splits != 2 && mx != -INFINITY) {
-    for (int i = 0; i < splits; ++i) {
-      const float li = part_lse[(size_t)i * nrows + row];
-      if (li == -INFINITY) continue;
-      const float wgt = expf(li - mx);
-      wsum += wgt;
-      float v[PER];
-      load_part(i, v);
+    if (mx != -INFINITY) {
+      for (int i = 0; i < splits; ++i) {
+        const float li = part_lse[(size_t)i * nrows + row];
+        if (li == -INFINITY) continue;
+        const float wgt = expf(li - mx);
+        wsum += wgt;
+        float v[PER];
+        load_part(i, v);
 #pragma unroll
-      for (int x = 0; x < PER; ++x) acc[x] = fmaf(wgt, v[x], acc[x]);
+        for (int x = 0; x < PER; ++x) acc[x] = fmaf(wgt, v[x], acc[x]);
+      }
     }
   }
   const float inv = wsum > 0.f ? 1.0f / wsum : 0.f;
@@ -1188,14 +1299,43 @@ int attn_resident_workgroups(int table_mode) {
   return 256 * kWavesPerCu / (table_mode == kTablesPerQTile ? kWavesQTile : kWavesGroup);
 }
 
+// Workspace of a split launch: the partial outputs [splits, B*Hq*C, D] and
+// log-sum-exps [splits, B*Hq*C] (fp32); the XCD-balanced split adds its cut
+// points [B*G] (int32) and, at the next 8-byte boundary, one arrival counter
+// per query tile [B*G*n_qtiles] (uint64).
+static size_t attn_partial_bytes(const Dims& d, int splits) {
+  return (size_t)splits * d.B * d.Hq * d.C * (d.D + 1) * sizeof(float);
+}
+
+static size_t align8(size_t x) { return (x + 7) & ~(size_t)7; }
+
 size_t attn_ws_bytes(const Dims& d, int splits) {
-  if (splits <= 1) return 0;
-  const size_t rows = (size_t)d.B * d.Hq * d.C;
-  return (size_t)splits * rows * (d.D + 1) * sizeof(float);
+  return splits <= 1 ? 0 : attn_partial_bytes(d, splits);
+}
+
+static size_t attn_xcd_counters_at(const Dims& d, int group_size) {
+  return align8(attn_partial_bytes(d, 2) + (size_t)d.B * (d.Hq / group_size) * sizeof(int32_t));
 }
 
 size_t attn_xcd_ws_bytes(const Dims& d, int group_size) {
-  return attn_ws_bytes(d, 2) + (size_t)d.B * (d.Hq / group_size) * sizeof(int32_t);
+  return attn_xcd_counters_at(d, group_size) +
+         (size_t)attn_base_workgroups(d, group_size, kTablesPerGroup) * 8;
+}
+
+// A tag per launch for the arrival counters: consecutive values from a
+// per-process random start, kept below 2^56 and never 0.  A counter left with
+// another tag (an earlier launch, or whatever the workspace held) counts 0.
+static unsigned long long next_arrival_tag() {
+  static std::atomic<unsigned long long> next{[] {
+    std::random_device rd;
+    const unsigned long long hi = rd(), lo = rd();
+    return (hi << 32) ^ lo ^
+           (unsigned long long)std::chrono::steady_clock::now().time_since_epoch().count();
+  }()};
+  for (;;) {
+    const unsigned long long t = next.fetch_add(1) & ((1ull << 56) - 1);
+    if (t != 0) return t;
+  }
 }
 
 template <int D, int NW, int VL>
@@ -1224,6 +1364,8 @@ hipError_t launch_attention(const Dims& d, const AttnLaunch& L, hipStream_t st) 
   const size_t rows = (size_t)d.B * d.Hq * d.C;
   a.part_o = L.splits > 1 ? static_cast<float*>(L.ws) : nullptr;
   a.part_lse = L.splits > 1 ? static_cast<float*>(L.ws) + (size_t)L.splits * rows * d.D : nullptr;
+  a.arrive = nullptr;
+  a.tag = 0;
   a.B = d.B;
   a.Hq = d.Hq;
   a.Hkv = d.Hkv;
@@ -1240,8 +1382,15 @@ hipError_t launch_attention(const Dims& d, const AttnLaunch& L, hipStream_t st) 
   a.split_at = nullptr;
   a.rows_per_unit = L.table_mode == kTablesPerQTile ? d.Hq / d.Hkv : 1;
   if (L.xcd_balanced)
-    a.split_at = reinterpret_cast<int32_t*>(static_cast<char*>(L.ws) + attn_ws_bytes(d, 2));
+    a.split_at = reinterpret_cast<int32_t*>(static_cast<char*>(L.ws) + attn_partial_bytes(d, 2));
   const int nwg = attn_base_workgroups(d, L.group_size, L.table_mode) * L.splits;
+  if (L.xcd_balanced) {
+    // per-group rows (selected or packed tables): the tiles attn_xcd_ws_bytes counts
+    if (L.splits != 2 || L.table_mode == kTablesPerQTile) return hipErrorInvalidValue;
+    a.arrive = reinterpret_cast<unsigned long long*>(static_cast<char*>(L.ws) +
+                                                     attn_xcd_counters_at(d, L.group_size));
+    a.tag = next_arrival_tag();
+  }
   const bool qtile = L.table_mode == kTablesPerQTile;
   if (d.D == 128) {
     if (qtile) launch_layout<128, kWavesQTile>(a, L.dense, L.v_layout, nwg, st);
@@ -1251,14 +1400,14 @@ hipError_t launch_attention(const Dims& d, const AttnLaunch& L, hipStream_t st) 
     else launch_layout<64, kWavesGroup>(a, L.dense, L.v_layout, nwg, st);
   }
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || L.splits == 1) return e;
+  if (e != hipSuccess || L.splits == 1 || L.xcd_balanced) return e;
   const int cgrid = (int)((rows + 7) / 8);
   if (d.D == 128)
     combine_kernel<128><<<cgrid, 256, 0, st>>>(a.part_o, a.part_lse, L.out, L.lse, d.B, d.Hq,
-                                               d.C, L.splits, a.split_at, a.G, L.group_size);
+                                               d.C, L.splits);
   else
     combine_kernel<64><<<cgrid, 256, 0, st>>>(a.part_o, a.part_lse, L.out, L.lse, d.B, d.Hq,
-                                              d.C, L.splits, a.split_at, a.G, L.group_size);
+                                              d.C, L.splits);
   return hipGetLastError();
 }
 

@@ -74,7 +74,7 @@ struct AttnLaunch {
   int group_size;
   float sm_scale;
   int splits;        // >= 1
-  void* ws;          // partials when splits > 1
+  void* ws;          // partials when splits > 1 (+ cuts and counters: XCD split)
   bool dense;
   int table_mode = kTablesPerGroup;
   long long packed_pages = 0;

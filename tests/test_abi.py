@@ -99,8 +99,9 @@ def test_workspace_sizes(lib):
     assert ca.attention_workspace_bytes(p, 4, 1) == 0
     assert ca.attention_workspace_bytes(p, 4, 2) == 2 * 32 * 2048 * 129 * 4
     # 256 query tiles fill the GPU and the 8 table rows spread over the 8 XCDs:
-    # the automatic choice cuts every row in two (two partial sets + 8 cut points)
-    assert ca.attention_workspace_bytes(p, 4, 0) == 2 * 32 * 2048 * 129 * 4 + 8 * 4
+    # the automatic choice cuts every row in two (two partial sets + 8 cut
+    # points + one 8-byte arrival counter per query tile, 8 rows x 32 tiles)
+    assert ca.attention_workspace_bytes(p, 4, 0) == 2 * 32 * 2048 * 129 * 4 + 8 * 4 + 8 * 256
     # 6 table rows do not spread evenly over the XCDs: the uniform choice, here
     # 2 splits because 192 query tiles cannot fill the 256 resident workgroups
     six = _prob(num_q_heads=24, num_kv_heads=6)

@@ -457,8 +457,8 @@ def test_attention_first_chunk_no_cache():
     got, lse = _run_attention(p, x, csr, w.group_size, w.sm_scale, num_splits=1)
     compare_attention(got, lse, ref, ref_lse)
     # dense with splits: the early query tiles see fewer blocks than later
-    # splits start at (those splits are empty; with 2 pieces the combine's
-    # two-piece path meets an empty piece next to stale partial slots)
+    # splits start at (those splits are empty: the merge meets pieces with
+    # no entries and a log-sum-exp of -inf)
     for splits in (1, 2, 3):
         got, lse = _run_attention(p, x, None, w.group_size, w.sm_scale, num_splits=splits,
                                   dense=True)
@@ -660,7 +660,7 @@ def test_max_context_whole_path():
     KV pool).  Estimator masks against the oracle (near ties only), tables bit
     for bit against the oracle union of the GPU masks (256 mask words per row),
     and attention on rows of every query tile against the oracle: the 32 tiles
-    of the single group row run with 8 uniform splits, so the general combine
+    of the single group row run with 8 uniform splits, so the general merge
     runs at its widest here; then the dense baseline on a few rows."""
     if "d" not in _MAX:
         w = synth.get_workload("tiny_gqa_1k", cached_lens=(16384 * 64 - 2048,), chunk_len=2048,
@@ -738,8 +738,8 @@ def _xcd_cut_points(lengths):
                                         ("batched_ragged_4seq", False),
                                         ("batched_ragged_4seq", True)])
 def test_xcd_cut_points(name, dense, workload_inputs, oracle_estimate):
-    """The cut points each attention workgroup computes (stored for the combine in the
-    workspace after the two partial results) equal the balancing rule evaluated on the
+    """The cut points each attention workgroup computes (recorded in the workspace
+    after the two partial results) equal the balancing rule evaluated on the
     host from the table lengths, and the XCD loads they give are equal to within the
     rounding of the cuts (a schedule property: a wrong cut changes no output, only the
     balance)."""
