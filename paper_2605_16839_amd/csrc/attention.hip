@@ -624,10 +624,13 @@ __global__ __launch_bounds__(64 * NW, NCT == 4 ? 1 : 2) void paged_attention_ker
 #pragma unroll
       for (int v = 0; v < 4; ++v) o[x][c][v] = 0.f;
   fence_o<AG>(o);
-  float m_run[NCT], l_run[NCT];
+  // m_thr = m_run + the slack, kept with m_run: the pipelined steps compare
+  // against it and move both only in the rare rescale branch
+  float m_run[NCT], l_run[NCT], m_thr[NCT];
 #pragma unroll
   for (int c = 0; c < NCT; ++c) {
     m_run[c] = kNoBase;
+    m_thr[c] = kNoBase + kRescaleSlack;
     l_run[c] = 0.f;
   }
 
@@ -791,12 +794,9 @@ __global__ __launch_bounds__(64 * NW, NCT == 4 ? 1 : 2) void paged_attention_ker
     // No hazard fence here: the last MFMA writing S and the last pack writing
     // P come well before their first readers in this step (end of step,
     // barrier, page pointers); the hazard test checks the distance.
-    float mx[NCT][2], alpha[NCT], ps[NCT];
+    float mx[NCT][2], m_old[NCT], ps[NCT];
 #pragma unroll
-    for (int c = 0; c < NCT; ++c) {
-      alpha[c] = 1.f;
-      ps[c] = 0.f;
-    }
+    for (int c = 0; c < NCT; ++c) ps[c] = 0.f;
     bool rb_any = false;
     bf16x8 fr[NFRAG];
 #pragma unroll
@@ -843,18 +843,17 @@ __global__ __launch_bounds__(64 * NW, NCT == 4 ? 1 : 2) void paged_attention_ker
           pin(mx[cc][0]);
         }
         if constexpr (part == 1) {
-          // the page maximum in log2 units; the base moves only past the slack,
-          // and alpha = exp2(old - new) is exactly 1 when it does not
+          // the page maximum in log2 units; the base moves only past the slack
           const float m = mx[cc][0] * a.scale_log2;
-          const bool rebase = m > m_run[cc] + kRescaleSlack;
+          const bool rebase = m > m_thr[cc];
           mx[cc][1] = rebase ? m : m_run[cc];
           rb_any |= rebase;
           pin(mx[cc][1]);
         }
         if constexpr (part == MAXB - 1) {
-          alpha[cc] = fast_exp2(m_run[cc] - mx[cc][1]);
+          m_old[cc] = m_run[cc];
           m_run[cc] = mx[cc][1];
-          pin(alpha[cc]);
+          pin(m_old[cc]);
           pin(m_run[cc]);
         }
       } else {
@@ -897,10 +896,20 @@ __global__ __launch_bounds__(64 * NW, NCT == 4 ? 1 : 2) void paged_attention_ker
       }
       __builtin_amdgcn_sched_barrier(0);
     });
-#pragma unroll
-    for (int c = 0; c < NCT; ++c) l_run[c] = l_run[c] * alpha[c] + ps[c];
+    // The rescale factor alpha = exp2(old - new base) is exactly 1 where the
+    // base did not move, so it is computed, with the new threshold, only when
+    // it moved on some lane; that branch folds the page's row sum into l_run
+    // with it (one rounding, as l_run * alpha + ps) and leaves ps at 0.
     const uint64_t any = __ballot(rb_any);
     if (any) {   // the exponent base moved on some lane: rescale O (rare)
+      float alpha[NCT];
+#pragma unroll
+      for (int c = 0; c < NCT; ++c) {
+        alpha[c] = fast_exp2(m_old[c] - m_run[c]);   // exactly 1 where it did not move
+        l_run[c] = fmaf(l_run[c], alpha[c], ps[c]);
+        ps[c] = 0.f;
+        m_thr[c] = m_run[c] + kRescaleSlack;
+      }
       fence_o<AG>(o);
 #pragma unroll
       for (int x = 0; x < NDT; ++x)
@@ -908,6 +917,8 @@ __global__ __launch_bounds__(64 * NW, NCT == 4 ? 1 : 2) void paged_attention_ker
         for (int c = 0; c < NCT; ++c) o[x][c] *= alpha[c];
       fence_o<AG>(o);
     }
+#pragma unroll
+    for (int c = 0; c < NCT; ++c) l_run[c] += ps[c];
     copies_landed(k_dma, v_dma);
     __syncthreads();
   };
