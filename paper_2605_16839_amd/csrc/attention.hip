@@ -304,10 +304,14 @@ __device__ __forceinline__ float max3(float a, float b, float c) {
   return __builtin_elementwise_maximum(__builtin_elementwise_maximum(a, b), c);
 }
 
-// Lazy rescaling threshold (log2 units): the running max used as the
-// exponent base is only moved when a new score exceeds it by more than this,
-// so the weights stay <= 2^kRescaleSlack and most pages skip the O rescale.
+// Lazy rescaling (log2 units): the exponent base (a running maximum of the
+// scaled scores) moves only when a weight could exceed 2^kRescaleSlack, so
+// most pages skip the O rescale.  The unpipelined pages test their page
+// maximum against base + kRescaleSlack; the pipelined steps compute no page
+// maximum and test each lane's partial row sum over the page against
+// kSumLimit, which bounds every weight in it.
 constexpr float kRescaleSlack = 8.0f;
+constexpr float kSumLimit = 256.0f;   // 2^kRescaleSlack
 // Exponent base before the first page: finite and below any score, so the
 // first page with a finite score always moves it (its alpha exp2(kNoBase - m)
 // is 0, which clears the empty O and row sum), and no -inf test is needed.
@@ -474,15 +478,9 @@ __global__ __launch_bounds__(64 * NW, NCT == 4 ? 1 : 2) void paged_attention_ker
   constexpr int FD = 3;                // fragment prefetch distance
   constexpr int DMA_PER_STEP = 2 * (64 * D * 2) / 1024 / NW;   // copy instructions per wave
   constexpr int DMA_STRIDE = (NSLOT / 2) / DMA_PER_STEP > 0 ? (NSLOT / 2) / DMA_PER_STEP : 1;
-  // softmax slots: the page maximum (8 max3 per column over MAXA slots), then
-  // per column the reduction over the lane groups and the exponent-base
-  // decision (MAXB slots per column), then the weights over the remaining slots
+  // softmax slots: the weights of the page over all slots
   constexpr int NE = 16 * NCT;         // softmax weights per lane per page
   constexpr int NSOFT = soft_ops(NE);
-  constexpr int MAXA = NSLOT / 8;
-  constexpr int MAXB = NSLOT / (8 * NCT);
-  constexpr int MAXS = MAXA + NCT * MAXB;
-  static_assert((8 * NCT) % MAXA == 0 && MAXB >= 2, "slot plan");
   __shared__ __attribute__((aligned(1024))) uint16_t k_s0[PAGE];
   __shared__ __attribute__((aligned(1024))) uint16_t k_s1[PAGE];
   __shared__ __attribute__((aligned(1024))) uint16_t v_s0[PAGE];
@@ -624,13 +622,10 @@ __global__ __launch_bounds__(64 * NW, NCT == 4 ? 1 : 2) void paged_attention_ker
 #pragma unroll
       for (int v = 0; v < 4; ++v) o[x][c][v] = 0.f;
   fence_o<AG>(o);
-  // m_thr = m_run + the slack, kept with m_run: the pipelined steps compare
-  // against it and move both only in the rare rescale branch
-  float m_run[NCT], l_run[NCT], m_thr[NCT];
+  float m_run[NCT], l_run[NCT];
 #pragma unroll
   for (int c = 0; c < NCT; ++c) {
     m_run[c] = kNoBase;
-    m_thr[c] = kNoBase + kRescaleSlack;
     l_run[c] = 0.f;
   }
 
@@ -794,10 +789,9 @@ __global__ __launch_bounds__(64 * NW, NCT == 4 ? 1 : 2) void paged_attention_ker
     // No hazard fence here: the last MFMA writing S and the last pack writing
     // P come well before their first readers in this step (end of step,
     // barrier, page pointers); the hazard test checks the distance.
-    float mx[NCT][2], m_old[NCT], ps[NCT];
+    float ps[NCT], wt[NE];
 #pragma unroll
     for (int c = 0; c < NCT; ++c) ps[c] = 0.f;
-    bool rb_any = false;
     bf16x8 fr[NFRAG];
 #pragma unroll
     for (int f = 0; f < FD; ++f) fr[f] = load_frag(f, v_rd, k_rd);
@@ -822,93 +816,79 @@ __global__ __launch_bounds__(64 * NW, NCT == 4 ? 1 : 2) void paged_attention_ker
         if constexpr (ks == 0) mfma_s0<AG>(sn.s[kt4][c], fr[F], qf[c][ks]);
         else mfma_s<AG>(sn.s[kt4][c], fr[F], qf[c][ks]);
       }
-      // softmax work of this slot
-      if constexpr (s < MAXA) {
-        // the page maximum of every column, two independent chains per column
-        // (tiles 0, 1 and tiles 2, 3): 8 max3 per column over MAXA slots
-        constexpr int PER = 8 * NCT / MAXA;     // max3 per slot
-        static_for<PER>([&](auto xtag) __attribute__((always_inline)) {
-          constexpr int k = s * PER + decltype(xtag)::value;   // 0 .. 8 * NCT - 1
-          constexpr int cc = k / 8, ch = (k / 4) % 2, v = k % 4;
-          if constexpr (v == 0) mx[cc][ch] = max2(sc.s[2 * ch][cc][0], sc.s[2 * ch + 1][cc][0]);
-          else mx[cc][ch] = max3(mx[cc][ch], sc.s[2 * ch][cc][v], sc.s[2 * ch + 1][cc][v]);
-          pin(mx[cc][ch]);
-        });
-      } else if constexpr (s < MAXS) {
-        // per column: the maximum over the 4 lane groups, then the base decision
-        // (a dependent chain, spread over the column's slots)
-        constexpr int cc = (s - MAXA) / MAXB, part = (s - MAXA) % MAXB;
-        if constexpr (part == 0) {
-          mx[cc][0] = groups_max(max2(mx[cc][0], mx[cc][1]));
-          pin(mx[cc][0]);
-        }
-        if constexpr (part == 1) {
-          // the page maximum in log2 units; the base moves only past the slack
-          const float m = mx[cc][0] * a.scale_log2;
-          const bool rebase = m > m_thr[cc];
-          mx[cc][1] = rebase ? m : m_run[cc];
-          rb_any |= rebase;
-          pin(mx[cc][1]);
-        }
-        if constexpr (part == MAXB - 1) {
-          m_old[cc] = m_run[cc];
-          m_run[cc] = mx[cc][1];
-          pin(m_old[cc]);
-          pin(m_run[cc]);
-        }
-      } else {
-        // Weights of the page, software-pipelined over the remaining slots so
-        // that no instruction waits on the one before it: element op j does
-        // the scaled score of element j, the exp of element j-1 and the row
-        // sum of element j-2 (elements in unit order, unit u = the 8 weights
-        // of P^T fragment (kp, c) = (u / NCT, u % NCT): values 0..3 of tile
-        // 2kp, then of tile 2kp + 1); unit u is packed to bf16 after element
-        // op 8u+8.
-        constexpr int lo = ((s - MAXS) * NSOFT) / (NSLOT - MAXS);
-        constexpr int hi = ((s - MAXS + 1) * NSOFT) / (NSLOT - MAXS);
+      // softmax work of this slot: the weights of the page against the
+      // current base, software-pipelined over all slots so that no
+      // instruction waits on the one before it: element op j does the scaled
+      // score of element j, the exp of element j-1 and the row sum of element
+      // j-2 (elements in unit order, unit u = the 8 weights of P^T fragment
+      // (kp, c) = (u / NCT, u % NCT): values 0..3 of tile 2kp, then of tile
+      // 2kp + 1); unit u is packed to bf16 after element op 8u+8.  The raw
+      // scores stay in sc for the rare rebase below.
+      {
+        constexpr int lo = (s * NSOFT) / NSLOT;
+        constexpr int hi = ((s + 1) * NSOFT) / NSLOT;
         static_for<hi - lo>([&](auto otag) __attribute__((always_inline)) {
           constexpr int op = soft_op(lo + decltype(otag)::value, NE);
           if constexpr (op >= 0) {
             if constexpr (op < NE) {
               constexpr int u = op / 8, x = op % 8, cc = u % NCT, kt4 = 2 * (u / NCT) + x / 4;
-              f32x4& sv = sc.s[kt4][cc];
-              sv[x % 4] = fmaf(sv[x % 4], a.scale_log2, -m_run[cc]);
-              pin(sv[x % 4]);
+              wt[op] = fmaf(sc.s[kt4][cc][x % 4], a.scale_log2, -m_run[cc]);
+              pin(wt[op]);
             }
             if constexpr (op >= 1 && op <= NE) {
-              constexpr int e = op - 1, u = e / 8, x = e % 8, cc = u % NCT, kt4 = 2 * (u / NCT) + x / 4;
-              f32x4& sv = sc.s[kt4][cc];
-              sv[x % 4] = fast_exp2(sv[x % 4]);
-              pin(sv[x % 4]);
+              constexpr int e = op - 1;
+              wt[e] = fast_exp2(wt[e]);
+              pin(wt[e]);
             }
             if constexpr (op >= 2) {
-              constexpr int e = op - 2, u = e / 8, x = e % 8, cc = u % NCT, kt4 = 2 * (u / NCT) + x / 4;
-              ps[cc] += sc.s[kt4][cc][x % 4];
+              constexpr int e = op - 2, u = e / 8, cc = u % NCT;
+              ps[cc] += wt[e];
               pin(ps[cc]);
             }
           } else {
             constexpr int u = -1 - op, kp = u / NCT, cc = u % NCT;
 #pragma unroll
-            for (int x = 0; x < 8; ++x) pn.p[kp][cc][x] = (__bf16)sc.s[2 * kp + x / 4][cc][x % 4];
+            for (int x = 0; x < 8; ++x) pn.p[kp][cc][x] = (__bf16)wt[8 * u + x];
             pin(pn.p[kp][cc]);
           }
         });
       }
       __builtin_amdgcn_sched_barrier(0);
     });
-    // The rescale factor alpha = exp2(old - new base) is exactly 1 where the
-    // base did not move, so it is computed, with the new threshold, only when
-    // it moved on some lane; that branch folds the page's row sum into l_run
-    // with it (one rounding, as l_run * alpha + ps) and leaves ps at 0.
-    const uint64_t any = __ballot(rb_any);
-    if (any) {   // the exponent base moved on some lane: rescale O (rare)
+    // A lane's partial row sum over its 16 keys of the page bounds each of its
+    // weights: while it stays <= 2^slack no weight exceeds 2^slack and the
+    // base stays (inf or NaN, from the first page's base, fail the test too).
+    bool big = false;
+#pragma unroll
+    for (int c = 0; c < NCT; ++c) big |= !(ps[c] <= kSumLimit);
+    if (__ballot(big)) {
+      // Rare: every column moves its base to the page maximum where that is
+      // higher (where it is not the base stays and alpha is 1), recomputes
+      // the page's weights, row sum and packs against it, and rescales O and
+      // l_run by alpha = exp2(old - new base).
       float alpha[NCT];
 #pragma unroll
       for (int c = 0; c < NCT; ++c) {
-        alpha[c] = fast_exp2(m_old[c] - m_run[c]);   // exactly 1 where it did not move
-        l_run[c] = fmaf(l_run[c], alpha[c], ps[c]);
+        float mx = max2(sc.s[0][c][0], sc.s[1][c][0]);
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          if (v > 0) mx = max3(mx, sc.s[0][c][v], sc.s[1][c][v]);
+          mx = max3(mx, sc.s[2][c][v], sc.s[3][c][v]);
+        }
+        const float m_new = max2(m_run[c], groups_max(mx) * a.scale_log2);
+        alpha[c] = fast_exp2(m_run[c] - m_new);
+        m_run[c] = m_new;
+        float sum = 0.f;
+#pragma unroll
+        for (int kp = 0; kp < 2; ++kp)
+#pragma unroll
+          for (int x = 0; x < 8; ++x) {
+            const float w = fast_exp2(fmaf(sc.s[2 * kp + x / 4][c][x % 4], a.scale_log2, -m_new));
+            sum += w;
+            pn.p[kp][c][x] = (__bf16)w;
+          }
+        l_run[c] = fmaf(l_run[c], alpha[c], sum);
         ps[c] = 0.f;
-        m_thr[c] = m_run[c] + kRescaleSlack;
       }
       fence_o<AG>(o);
 #pragma unroll
