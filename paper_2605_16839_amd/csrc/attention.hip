@@ -708,8 +708,8 @@ __global__ __launch_bounds__(64 * NW, NCT == 4 ? 1 : 2) void paged_attention_ker
     }
   }
   // fragment F of a step: F < NPV is V^T fragment (kp = F / NDT, d tile
-  // x = F % NDT), otherwise K fragment (key tile (F - NPV) / NKS, k-step
-  // (F - NPV) % NKS)
+  // x = F % NDT), otherwise K fragment (key tile (F - NPV) % 4, k-step
+  // (F - NPV) / 4: the 4 MFMAs that build one S^T tile are 8 slots apart)
   auto load_frag = [&](int F, const uint16_t* vt, const uint16_t* kt) -> bf16x8 {
     if (F < NPV) {
       const int kp = F / NDT, x = F % NDT;
@@ -725,7 +725,7 @@ __global__ __launch_bounds__(64 * NW, NCT == 4 ? 1 : 2) void paged_attention_ker
         return __builtin_bit_cast(bf16x8, w);
       }
     }
-    const int G2 = F - NPV, kt4 = G2 / NKS, ks = G2 % NKS;
+    const int G2 = F - NPV, kt4 = G2 % 4, ks = G2 / 4;
     const char* p = reinterpret_cast<const char*>(kt) + kofs[ks] +
                     (32 * (kt4 >> 1) + 4 * (kt4 & 1)) * D * 2;
     return *reinterpret_cast<const bf16x8*>(p);
@@ -734,7 +734,7 @@ __global__ __launch_bounds__(64 * NW, NCT == 4 ? 1 : 2) void paged_attention_ker
   // Whole-page contractions (outside the pipelined loop).
   auto qk_page = [&](SPage<NCT>& st, const uint16_t* kt) __attribute__((always_inline)) {
     static_for<NQK>([&](auto gtag) __attribute__((always_inline)) {
-      constexpr int G2 = decltype(gtag)::value, kt4 = G2 / NKS, ks = G2 % NKS;
+      constexpr int G2 = decltype(gtag)::value, kt4 = G2 % 4, ks = G2 / 4;
       const bf16x8 kf = load_frag(NPV + G2, kt, kt);
 #pragma unroll
       for (int c = 0; c < NCT; ++c) {
@@ -812,7 +812,7 @@ __global__ __launch_bounds__(64 * NW, NCT == 4 ? 1 : 2) void paged_attention_ker
       if constexpr (F < NPV) {
         mfma_o<AG>(o[F % NDT][c], fr[F], po.p[F / NDT][c]);
       } else {
-        constexpr int G2 = F - NPV, kt4 = G2 / NKS, ks = G2 % NKS;
+        constexpr int G2 = F - NPV, kt4 = G2 % 4, ks = G2 / 4;
         if constexpr (ks == 0) mfma_s0<AG>(sn.s[kt4][c], fr[F], qf[c][ks]);
         else mfma_s<AG>(sn.s[kt4][c], fr[F], qf[c][ks]);
       }
