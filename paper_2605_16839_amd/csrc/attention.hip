@@ -376,18 +376,28 @@ __device__ __forceinline__ void mfma_s(f32x4& s, const bf16x8& a, const bf16x8& 
   else asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+v"(s) : "v"(a), "v"(b));
 }
 
-// Whole-tuple fence on the O^T accumulators: an MFMA result read or
-// overwritten by VALU code, or a VALU result read by an MFMA, needs wait
-// states the compiler cannot see through inline asm.
+// Fence on the O^T accumulators: an MFMA result read or overwritten by VALU
+// code, or a VALU result read by an MFMA, needs wait states the compiler
+// cannot see through inline asm.  One set of wait states serves every tuple.
+// Volatile asm statements keep their order, so empty statements that take
+// each tuple as an operand pin the writes of every tuple above the wait (the
+// statements before it) and the reads of every tuple below it (the
+// statements after it); the MFMAs, also volatile asm, stay on their side.
 template <bool AG, int NDT, int NCT>
-__device__ __forceinline__ void fence_o(f32x4 (&o)[NDT][NCT]) {
+__device__ __forceinline__ void tie_o(f32x4 (&o)[NDT][NCT]) {
 #pragma unroll
   for (int x = 0; x < NDT; ++x)
 #pragma unroll
     for (int c = 0; c < NCT; ++c) {
-      if constexpr (AG) asm volatile("s_nop 7\n s_nop 7\n s_nop 7" : "+a"(o[x][c]));
-      else asm volatile("s_nop 7\n s_nop 7\n s_nop 7" : "+v"(o[x][c]));
+      if constexpr (AG) asm volatile("" : "+a"(o[x][c]));
+      else asm volatile("" : "+v"(o[x][c]));
     }
+}
+template <bool AG, int NDT, int NCT>
+__device__ __forceinline__ void fence_o(f32x4 (&o)[NDT][NCT]) {
+  tie_o<AG>(o);
+  asm volatile("s_nop 7\n s_nop 7\n s_nop 7");
+  tie_o<AG>(o);
 }
 
 // Fences on S^T tiles (MFMA results about to be read by the softmax) and on
