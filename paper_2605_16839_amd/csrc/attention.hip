@@ -1213,6 +1213,9 @@ hipError_t launch_gather(const Dims& d, const uint16_t* k_pool, const uint16_t* 
 // out = sum_i exp(lse_i - lse) o_i, pieces in order.  One 32-lane half-wave
 // per (b, h, t) row, 4 floats of d per lane (D = 128) or 2 (D = 64).  (The
 // XCD-balanced split merges its two pieces inside the attention launch.)
+// Up to kCombineInFlight pieces are loaded all at once.
+constexpr int kCombineInFlight = 8;
+
 template <int D>
 __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ part_o,
                                                       const float* __restrict__ part_lse,
@@ -1252,6 +1255,30 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
 #pragma unroll
       for (int x = 0; x < PER; ++x)
         acc[x] = (w0 > 0.f ? w0 * v0[x] : 0.f) + (w1 > 0.f ? w1 * v1[x] : 0.f);
+    }
+  } else if (splits <= kCombineInFlight) {
+    // every piece's lse and partial loaded before the first is needed (one
+    // memory latency), then the same merge as the general loop below
+    float l[kCombineInFlight], v[kCombineInFlight][PER];
+#pragma unroll
+    for (int i = 0; i < kCombineInFlight; ++i) {
+      if (i < splits) {
+        l[i] = part_lse[(size_t)i * nrows + row];
+        load_part(i, v[i]);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < kCombineInFlight; ++i)
+      if (i < splits) mx = fmaxf(mx, l[i]);
+    if (mx != -INFINITY) {
+#pragma unroll
+      for (int i = 0; i < kCombineInFlight; ++i) {
+        if (i >= splits || l[i] == -INFINITY) continue;
+        const float wgt = expf(l[i] - mx);
+        wsum += wgt;
+#pragma unroll
+        for (int x = 0; x < PER; ++x) acc[x] = fmaf(wgt, v[i][x], acc[x]);
+      }
     }
   } else {
     for (int i = 0; i < splits; ++i) mx = fmaxf(mx, part_lse[(size_t)i * nrows + row]);
