@@ -492,11 +492,12 @@ def test_attention_workloads_sampled(name, workload_inputs, oracle_estimate):
     print(name, "sharp", compare_attention(got, lse, ref, ref_lse, rows[::3]))
 
 
-@pytest.mark.parametrize("splits", [3, 4])
+@pytest.mark.parametrize("splits", [3, 4, 9, 12])
 def test_attention_d128_explicit_splits(splits, workload_inputs, oracle_estimate):
-    """head_dim 128 with 3 and 4 uniform splits: the general log-sum-exp merge
-    of more than two pieces, rows on every (group, query tile) vs the oracle
-    and the whole output vs one pass per tile."""
+    """head_dim 128 with 3, 4, 9 and 12 uniform splits: the log-sum-exp merge
+    of more than two pieces (up to 8 pieces loaded at once, more in a loop),
+    rows on every (group, query tile) vs the oracle and the whole output vs
+    one pass per tile."""
     name = "llama8b_32k"
     d = workload_inputs(name)
     w = d["workload"]
