@@ -491,6 +491,7 @@ __global__ __launch_bounds__(64 * NW, NCT == 4 ? 1 : 2) void paged_attention_ker
   // softmax slots: the weights of the page over all slots
   constexpr int NE = 16 * NCT;         // softmax weights per lane per page
   constexpr int NSOFT = soft_ops(NE);
+  constexpr bool EVEN = NSLOT >= 2 * NE;   // softmax spread one instruction per slot
   __shared__ __attribute__((aligned(1024))) uint16_t k_s0[PAGE];
   __shared__ __attribute__((aligned(1024))) uint16_t k_s1[PAGE];
   __shared__ __attribute__((aligned(1024))) uint16_t v_s0[PAGE];
@@ -827,14 +828,45 @@ __global__ __launch_bounds__(64 * NW, NCT == 4 ? 1 : 2) void paged_attention_ker
         else mfma_s<AG>(sn.s[kt4][c], fr[F], qf[c][ks]);
       }
       // softmax work of this slot: the weights of the page against the
-      // current base, software-pipelined over all slots so that no
-      // instruction waits on the one before it: element op j does the scaled
-      // score of element j, the exp of element j-1 and the row sum of element
-      // j-2 (elements in unit order, unit u = the 8 weights of P^T fragment
-      // (kp, c) = (u / NCT, u % NCT): values 0..3 of tile 2kp, then of tile
-      // 2kp + 1); unit u is packed to bf16 after element op 8u+8.  The raw
-      // scores stay in sc for the rare rebase below.
-      {
+      // current base, spread over the slots so that no instruction waits on
+      // the one before it (elements in unit order, unit u = the 8 weights of
+      // P^T fragment (kp, c) = (u / NCT, u % NCT): values 0..3 of tile 2kp,
+      // then of tile 2kp + 1).  The raw scores stay in sc for the rare rebase
+      // below.
+      if constexpr (EVEN) {
+        // Two slots per element, one or two instructions per slot: element
+        // e's scaled score in slot 2e, its exp in slot 2e + 1, its row-sum add
+        // in slot 2e + 2; half h of unit u's packs (its last exp in slot
+        // 16u + 15) in slot 16u + 16 + 2h; the last add and the last unit's
+        // packs after the slots.  (Whole element ops, three instructions each
+        // in about every other slot, left the VALU work in bursts that the
+        // MFMAs of the two waves hid less well.)
+        constexpr int e = s / 2;
+        if constexpr (s % 2 == 0) {
+          if constexpr (e < NE) {
+            constexpr int u = e / 8, x = e % 8, cc = u % NCT, kt4 = 2 * (u / NCT) + x / 4;
+            wt[e] = fmaf(sc.s[kt4][cc][x % 4], a.scale_log2, -m_run[cc]);
+            pin(wt[e]);
+          }
+          if constexpr (e >= 1 && e <= NE) {
+            constexpr int e1 = e - 1, cc = (e1 / 8) % NCT;
+            ps[cc] += wt[e1];
+            pin(ps[cc]);
+          }
+          if constexpr (s >= 16 && (s - 16) % 16 < 4 && (s - 16) / 16 < NE / 8) {
+            constexpr int u = (s - 16) / 16, h = ((s - 16) % 16) / 2, kp = u / NCT, cc = u % NCT;
+#pragma unroll
+            for (int x = 4 * h; x < 4 * h + 4; ++x) pn.p[kp][cc][x] = (__bf16)wt[8 * u + x];
+            pin(pn.p[kp][cc]);
+          }
+        } else if constexpr (e < NE) {
+          wt[e] = fast_exp2(wt[e]);
+          pin(wt[e]);
+        }
+      } else {
+        // one slot per element (D = 64): element op j does the scaled score
+        // of element j, the exp of element j-1 and the row sum of element
+        // j-2; unit u is packed to bf16 after element op 8u+8
         constexpr int lo = (s * NSOFT) / NSLOT;
         constexpr int hi = ((s + 1) * NSOFT) / NSLOT;
         static_for<hi - lo>([&](auto otag) __attribute__((always_inline)) {
@@ -865,6 +897,13 @@ __global__ __launch_bounds__(64 * NW, NCT == 4 ? 1 : 2) void paged_attention_ker
       }
       __builtin_amdgcn_sched_barrier(0);
     });
+    if constexpr (EVEN) {
+      // the last add and the last unit's packs (slots 2 NE and after)
+      constexpr int e1 = NE - 1, u = NE / 8 - 1, kp = u / NCT, cc = u % NCT;
+      ps[(e1 / 8) % NCT] += wt[e1];
+#pragma unroll
+      for (int x = 0; x < 8; ++x) pn.p[kp][cc][x] = (__bf16)wt[8 * u + x];
+    }
     // A lane's partial row sum over its 16 keys of the page bounds each of its
     // weights: while it stays <= 2^slack no weight exceeds 2^slack and the
     // base stays (inf or NaN, from the first page's base, fail the test too).
