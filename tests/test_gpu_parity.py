@@ -492,6 +492,45 @@ def test_attention_workloads_sampled(name, workload_inputs, oracle_estimate):
     print(name, "sharp", compare_attention(got, lse, ref, ref_lse, rows[::3]))
 
 
+def test_attention_rising_scores_rebase_every_step(workload_inputs):
+    """Scores that rise from page to page: a shared unit direction u is added to
+    every query, and c * j * u to every key row of block j, with c^2 * sm_scale
+    * log2(e) = 2, so a query's scores grow by about two log2 units per block.
+    The tables keep one cached block in 12 (about 9 blocks apart): about 3 in 4
+    of a query's consecutive pages raise its page maximum by more than the
+    lazy-rescale slack (8 log2 units), so with 32 columns per wave nearly every
+    pipelined step takes the rebase path (page maximum, weights and packs
+    recomputed, O and the row sums rescaled).  Rows on every (group, query
+    tile) against the fp64 oracle on the same bf16 inputs."""
+    from synth.gen import bf16_bits_to_f32, bf16_round
+    d = dict(workload_inputs("llama8b_32k"))
+    w = d["workload"]
+    D, G = w.head_dim, w.num_q_heads // w.group_size
+    rng = np.random.default_rng(w.seed + 101)
+    u = rng.standard_normal(D)
+    u /= np.linalg.norm(u)
+    c = math.sqrt(2.0 / (w.sm_scale * math.log2(math.e)))
+    d["q"] = bf16_round(bf16_bits_to_f32(d["q"]) + np.float32(c) * u.astype(np.float32))
+    k = bf16_bits_to_f32(d["k_pool"]).copy()
+    pt = d["page_table"]
+    for b in range(w.batch):
+        nkb = w.n_kv_blocks(b)
+        ramp = (c * np.arange(nkb, dtype=np.float64))[:, None, None] * u[None, None, :]
+        for kvh in range(w.num_kv_heads):
+            k[pt[b, kvh, :nkb]] += ramp.astype(np.float32)
+    d["k_pool"] = bf16_round(k)
+    ncs = [w.n_cached_blocks(b) for b in range(w.batch)]
+    ip, ix = synth.random_tables(w.seed + 7, w.batch, G, ncs, w.chunk_len // w.page_size, 1 / 12)
+    T = [[ix[ip[b * G + g]:ip[b * G + g + 1]].tolist() for g in range(G)]
+         for b in range(w.batch)]
+    p = _problem(w)
+    x = device_inputs(d)
+    got, lse = _run_attention(p, x, (ip, ix), w.group_size, w.sm_scale, num_splits=0)
+    rows = tile_rows(w.batch, w.num_q_heads, w.chunk_len, w.group_size, seed=w.seed + 11)
+    ref, ref_lse = _oracle_rows(d, T, w.group_size, w.sm_scale, rows)
+    print("rising scores", len(rows), "rows", compare_attention(got, lse, ref, ref_lse, rows))
+
+
 @pytest.mark.parametrize("splits", [3, 4, 9, 12])
 def test_attention_d128_explicit_splits(splits, workload_inputs, oracle_estimate):
     """head_dim 128 with 3, 4, 9 and 12 uniform splits: the log-sum-exp merge
