@@ -531,6 +531,26 @@ def test_attention_rising_scores_rebase_every_step(workload_inputs):
     print("rising scores", len(rows), "rows", compare_attention(got, lse, ref, ref_lse, rows))
 
 
+@pytest.mark.parametrize("gs", [1, 2])
+def test_attention_d128_small_groups(gs, workload_inputs, oracle_estimate):
+    """head_dim 128 with execution groups of 1 and 2 heads (query tiles of 256
+    and 128 chunk queries, so 4 and 2 causally masked pages per tile; 32 and 16
+    table rows through the XCD-balanced split), tables of the estimator's masks
+    at that group size: rows of every (group, query tile) against the oracle."""
+    name = "llama8b_32k"
+    d = workload_inputs(name)
+    w = d["workload"]
+    masks, _ = oracle_estimate(name)
+    nkb = [w.n_kv_blocks(b) for b in range(w.batch)]
+    T = oracle.block_tables(masks, gs, nkb)
+    p = _problem(w)
+    x = device_inputs(d)
+    got, lse = _run_attention(p, x, oracle.tables_to_csr(T), gs, w.sm_scale, num_splits=0)
+    rows = tile_rows(w.batch, w.num_q_heads, w.chunk_len, gs, seed=w.seed + gs)
+    ref, ref_lse = _oracle_rows(d, T, gs, w.sm_scale, rows)
+    print("gs", gs, len(rows), "rows", compare_attention(got, lse, ref, ref_lse, rows))
+
+
 @pytest.mark.parametrize("splits", [3, 4, 9, 12])
 def test_attention_d128_explicit_splits(splits, workload_inputs, oracle_estimate):
     """head_dim 128 with 3, 4, 9 and 12 uniform splits: the log-sum-exp merge
