@@ -446,6 +446,29 @@ def test_attention_unaligned_edges(C, cached):
     compare_attention(got, lse, ref, ref_lse)
 
 
+@pytest.mark.parametrize("C,cached", [(1, (8191, 64, 0)), (63, (4113,)), (130, (2047, 5))])
+def test_attention_d128_unaligned_edges(C, cached):
+    """The same edges at head_dim 128 over caches long enough for the pipelined
+    loop to run many pages (single-token and near-page chunks, caches of 0, 5,
+    64, 2047, 4113 and 8191 tokens): dense and all-open-table attention against
+    the oracle, every row, with one pass per tile and the automatic schedule."""
+    nkb = max(-(-(c + C) // 64) for c in cached)
+    w = synth.get_workload("llama8b_unaligned", chunk_len=C, cached_lens=cached,
+                           batch=len(cached), max_kv_blocks=nkb)
+    d = synth.make_inputs(w)
+    p = _problem(w)
+    x = device_inputs(d)
+    T = oracle.dense_tables([w.n_kv_blocks(b) for b in range(w.batch)], w.num_groups)
+    ref, ref_lse = oracle.chunk_attention(d["q"], d["k_pool"], d["v_pool"], d["page_table"],
+                                          d["cached_len"], T, w.group_size, w.sm_scale)
+    for splits in (1, 0):
+        got, lse = _run_attention(p, x, oracle.tables_to_csr(T), w.group_size, w.sm_scale,
+                                  num_splits=splits)
+        compare_attention(got, lse, ref, ref_lse)
+    got, lse = _run_attention(p, x, None, w.group_size, w.sm_scale, num_splits=0, dense=True)
+    compare_attention(got, lse, ref, ref_lse)
+
+
 def test_attention_first_chunk_no_cache():
     w = synth.get_workload("tiny_gqa_1k", cached_lens=(0,), max_kv_blocks=4)
     d = synth.make_inputs(w)
