@@ -812,9 +812,10 @@ __global__ __launch_bounds__(64 * NW, NCT == 4 ? 1 : 2) void paged_attention_ker
       if constexpr (c == 0 && F + FD < NFRAG) fr[F + FD] = load_frag(F + FD, v_rd, k_rd);
       // the copies of K(i+2) and V(i), one instruction every DMA_STRIDE slots
       // over the first half of the step (issued all at once they queue in
-      // the address unit and stall the wave)
-      if constexpr (s % DMA_STRIDE == 0 && s / DMA_STRIDE < DMA_PER_STEP) {
-        constexpr int m = s / DMA_STRIDE;
+      // the address unit and stall the wave), from slot 1: slot 0 issues the
+      // step's first fragment reads right after the barrier
+      if constexpr (s >= 1 && (s - 1) % DMA_STRIDE == 0 && (s - 1) / DMA_STRIDE < DMA_PER_STEP) {
+        constexpr int m = (s - 1) / DMA_STRIDE;
         if constexpr (m < DMA_PER_STEP / 2)
           page_part_to_lds<D, NW, kTileK>(k_src, k_dma, wv, lane, m);
         else
